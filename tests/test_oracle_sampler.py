@@ -1,0 +1,250 @@
+"""Pins for the oracle's accept/reject/resample step.
+
+What the paper fixes (DiP-SD, Sec. II-A step 2 and eq. (1)): verification
+stops at the first rejected draft and always emits one more token, and under
+i.i.d. acceptance with rate alpha the expected number of tokens per round is
+(1 - alpha^(l+1)) / (1 - alpha).  The accept/resample rule comes from the
+speculative-sampling work the paper cites in Sec. I, whose defining property
+is that emitted tokens follow the target distribution.  Each test below
+checks one of these facts on toy tables where the exact answer is known.
+"""
+import math
+
+import numpy as np
+import pytest
+from scipy import stats
+
+import oracle
+
+
+def _tables(rng, L, V, zero_p=None, zero_q=None):
+    """Per-slot target p (L+1 rows) and draft q (L rows) distributions."""
+    p = rng.dirichlet(np.ones(V), size=L + 1)
+    q = rng.dirichlet(np.ones(V), size=L)
+    if zero_p is not None:
+        p[:, zero_p] = 0.0
+        p /= p.sum(1, keepdims=True)
+    if zero_q is not None:
+        q[:, zero_q] = 0.0
+        q /= q.sum(1, keepdims=True)
+    return p, q
+
+
+def _logits(p):
+    with np.errstate(divide="ignore"):
+        return np.log(p).astype(np.float32)
+
+
+def _batch(p, q, B, rng, drafts=None):
+    """B independent trials of the same per-slot tables; drafts ~ q."""
+    L = q.shape[0]
+    V = p.shape[1]
+    logits = np.tile(_logits(p), (B, 1))
+    qq = np.tile(q.astype(np.float32), (B, 1))
+    if drafts is None:
+        drafts = np.empty((B, L), np.int32)
+        for j in range(L):
+            drafts[:, j] = rng.choice(V, size=B, p=q[j])
+    return logits, qq, drafts.reshape(-1)
+
+
+def _emitted(res, drafts, L):
+    """Emitted sequence per trial: accepted drafts then the final token."""
+    out = []
+    d = drafts.reshape(-1, L)
+    for b in range(d.shape[0]):
+        a = int(res["n_acc"][b])
+        out.append(list(d[b, :a]) + [int(res["token"][b])])
+    return out
+
+
+def _chi2_ok(counts, probs, alpha=1e-3):
+    counts = np.asarray(counts, float)
+    probs = np.asarray(probs, float)
+    n = counts.sum()
+    keep = probs > 0
+    assert np.all(counts[~keep] == 0), "a zero-probability token was emitted"
+    exp = probs[keep] * n
+    chi2 = ((counts[keep] - exp) ** 2 / exp).sum()
+    pval = stats.chi2.sf(chi2, keep.sum() - 1)
+    return pval > alpha, pval
+
+
+def test_q_equals_p_accepts_everything():
+    rng = np.random.default_rng(10)
+    L, V, B = 4, 7, 4000
+    p, _ = _tables(rng, L, V)
+    q = p[:L].copy()
+    logits, qq, drafts = _batch(p, q, B, rng)
+    res = oracle.sample("stochastic", np.arange(B), np.full(B, L), logits, drafts, qq, seed=1)
+    assert np.all(res["n_acc"] == L)
+
+
+def test_target_distribution_is_preserved():
+    """Each emitted token follows the target row of its position, including
+    tokens q never proposes (only the residual can supply them) and never
+    tokens p forbids."""
+    rng = np.random.default_rng(11)
+    L, V, B = 3, 6, 30000
+    p, q = _tables(rng, L, V, zero_p=5, zero_q=2)
+    logits, qq, drafts = _batch(p, q, B, rng)
+    res = oracle.sample("stochastic", np.arange(B), np.full(B, L), logits, drafts, qq, seed=7, round_=3)
+    seqs = _emitted(res, drafts, L)
+    for k in range(L + 1):
+        toks = [s[k] for s in seqs if len(s) > k]
+        counts = np.bincount(toks, minlength=V)
+        ok, pv = _chi2_ok(counts, p[k])
+        assert ok, f"position {k}: chi2 p-value {pv}"
+
+
+def test_residual_distribution_after_rejection():
+    """A rejected draft is replaced by a draw from norm(max(0, p - q))."""
+    rng = np.random.default_rng(12)
+    V, B = 8, 30000
+    p, q = _tables(rng, 1, V)
+    d = int(np.argmin(p[0] / q[0]))  # p(d) < q(d), so rejection is possible
+    assert p[0, d] / q[0, d] < 0.9
+    logits, qq, drafts = _batch(p, q, B, rng, drafts=np.full((B, 1), d, np.int32))
+    u = np.full(B, 0.9999, np.float32)  # above r: always reject
+    res = oracle.sample("stochastic", np.arange(B), np.ones(B), logits, drafts, qq, accept_u=u, seed=3)
+    assert np.all(res["n_acc"] == 0)
+    w = np.maximum(0.0, p[0] - q[0])
+    ok, pv = _chi2_ok(np.bincount(res["token"], minlength=V), w / w.sum())
+    assert ok, pv
+
+
+def test_bonus_token_follows_last_row():
+    rng = np.random.default_rng(13)
+    L, V, B = 2, 5, 20000
+    p, q = _tables(rng, L, V)
+    logits, qq, drafts = _batch(p, q, B, rng)
+    u = np.zeros(B * L, np.float32)  # u = 0 < r: always accept
+    res = oracle.sample("stochastic", np.arange(B), np.full(B, L), logits, drafts, qq, accept_u=u, seed=4)
+    assert np.all(res["n_acc"] == L)
+    ok, pv = _chi2_ok(np.bincount(res["token"], minlength=V), p[L])
+    assert ok, pv
+
+
+def test_accept_probability_is_min_one_ratio():
+    """With a stratified grid of accept uniforms the accepted fraction is
+    min(1, p(d)/q(d)) to the grid resolution, and u == r rejects."""
+    rng = np.random.default_rng(14)
+    V, G = 6, 4096
+    p, q = _tables(rng, 1, V)
+    u = ((np.arange(G) + 0.5) / G).astype(np.float32)
+    for d in range(V):
+        logits, qq, drafts = _batch(p, q, G, rng, drafts=np.full((G, 1), d, np.int32))
+        res = oracle.sample("stochastic", np.arange(G), np.ones(G), logits, drafts, qq, accept_u=u)
+        frac = res["n_acc"].mean()
+        assert abs(frac - min(1.0, p[0, d] / q[0, d])) <= 1.0 / G + 1e-6
+        r = res["ratio"][0]
+        if r < 1:
+            res2 = oracle.sample("stochastic", [0], [1], logits[:2], drafts[:1], qq[:1],
+                                 accept_u=np.array([r], np.float32))
+            assert res2["n_acc"][0] == 0
+
+
+@pytest.mark.parametrize("alpha,L", [(0.78, 7), (0.5, 3), (0.95, 12)])
+def test_geometric_mean_eq1(alpha, L):
+    """q = alpha * p + (1 - alpha) * delta_z with p(z) = 0 gives acceptance
+    rate exactly alpha per draft; the mean tokens per round must equal
+    (1 - alpha^(L+1)) / (1 - alpha) (eq. 1) and n_acc must follow the
+    truncated geometric law."""
+    rng = np.random.default_rng(int(alpha * 100) + L)
+    V, B = 9, 20000
+    z = V - 1
+    p = rng.dirichlet(np.ones(V), size=L + 1)
+    p[:, z] = 0.0
+    p /= p.sum(1, keepdims=True)
+    q = alpha * p[:L].copy()
+    q[:, z] += 1.0 - alpha
+    logits, qq, drafts = _batch(p, q, B, rng)
+    res = oracle.sample("stochastic", np.arange(B), np.full(B, L), logits, drafts, qq, seed=5, round_=1)
+    tokens = res["n_acc"] + 1
+    mean = (1 - alpha ** (L + 1)) / (1 - alpha)
+    pk = np.array([alpha ** k * (1 - alpha) for k in range(L)] + [alpha ** L])
+    var = float(((np.arange(L + 1) + 1) ** 2 * pk).sum() - mean ** 2)
+    assert abs(tokens.mean() - mean) < 4 * math.sqrt(var / B)
+    ok, pv = _chi2_ok(np.bincount(res["n_acc"], minlength=L + 1), pk)
+    assert ok, pv
+
+
+def test_greedy_accepts_longest_matching_prefix():
+    rng = np.random.default_rng(15)
+    L, V, B = 5, 11, 50
+    logits = rng.normal(size=(B * (L + 1), V)).astype(np.float32)
+    am = logits.argmax(1).reshape(B, L + 1)
+    k = rng.integers(0, L + 1, size=B)  # first planted mismatch (L = none)
+    drafts = am[:, :L].copy()
+    for b in range(B):
+        if k[b] < L:
+            drafts[b, k[b]] = (am[b, k[b]] + 1 + rng.integers(0, V - 1)) % V
+            drafts[b, k[b] + 1:] = rng.integers(0, V, size=L - k[b] - 1)
+    res = oracle.sample("greedy", np.arange(B), np.full(B, L), logits, drafts.reshape(-1),
+                        np.zeros((0, V), np.float32))
+    assert np.array_equal(res["n_acc"], k)
+    assert np.array_equal(res["token"], am[np.arange(B), k])
+
+
+def test_greedy_ties_break_to_lowest_index():
+    V = 6
+    row = np.array([0.1, 2.0, 0.3, 2.0, -1.0, 2.0], np.float32)
+    logits = np.stack([row, row])
+    res = oracle.sample("greedy", [0], [1], logits, np.array([3], np.int32), np.zeros((0, V), np.float32))
+    assert res["n_acc"][0] == 0 and res["token"][0] == 1
+    res = oracle.sample("greedy", [0], [1], logits, np.array([1], np.int32), np.zeros((0, V), np.float32))
+    assert res["n_acc"][0] == 1 and res["token"][0] == 1
+
+
+def test_force_mode_accepts_all():
+    rng = np.random.default_rng(16)
+    L, V = 3, 9
+    logits = rng.normal(size=(L + 1, V)).astype(np.float32)
+    res = oracle.sample("force", [0], [L], logits, np.array([1, 2, 3], np.int32), np.zeros((0, V), np.float32))
+    assert res["n_acc"][0] == L and res["token"][0] == int(logits[L].argmax())
+
+
+def test_zero_residual_falls_back_to_target():
+    """If max(0, p - q) is zero everywhere the correction is drawn from p."""
+    rng = np.random.default_rng(17)
+    V, B = 5, 20000
+    p = rng.dirichlet(np.ones(V), size=2)
+    q = (p[:1] * 1.01).astype(np.float32)  # q >= p elementwise: residual is empty
+    logits, qq, drafts = _batch(p, q, B, rng, drafts=np.zeros((B, 1), np.int32))
+    res = oracle.sample("stochastic", np.arange(B), np.ones(B), logits, drafts, qq,
+                        accept_u=np.full(B, 0.9999, np.float32), seed=9)
+    assert np.all(res["n_acc"] == 0)
+    ok, pv = _chi2_ok(np.bincount(res["token"], minlength=V), p[0])
+    assert ok, pv
+
+
+def test_zero_draft_probability_edge_cases():
+    """p/0 = +inf accepts; 0/0 = NaN rejects (IEEE semantics of r = p/q)."""
+    p = np.array([[0.5, 0.5, 0.0], [0.2, 0.3, 0.5]])
+    q = np.array([[0.0, 0.0, 1.0]], np.float32)
+    logits = _logits(p)
+    r1 = oracle.sample("stochastic", [0], [1], logits, np.array([0], np.int32), q,
+                       accept_u=np.array([0.999], np.float32))
+    assert r1["n_acc"][0] == 1 and np.isinf(r1["ratio"][0])
+    q2 = np.array([[0.5, 0.5, 0.0]], np.float32)
+    r2 = oracle.sample("stochastic", [0], [1], logits, np.array([2], np.int32), q2,
+                       accept_u=np.array([0.0], np.float32))
+    assert r2["n_acc"][0] == 0 and np.isnan(r2["ratio"][0])
+
+
+def test_draws_depend_on_user_not_batch_position():
+    """Counter-based draws are keyed by the global user id: permuting the
+    batch permutes the results."""
+    rng = np.random.default_rng(18)
+    L, V, B = 2, 7, 6
+    p, q = _tables(rng, L, V)
+    logits, qq, drafts = _batch(p, q, B, rng)
+    users = np.array([3, 9, 12, 40, 41, 77])
+    res = oracle.sample("stochastic", users, np.full(B, L), logits, drafts, qq, seed=2, round_=5)
+    perm = np.array([5, 0, 3, 1, 4, 2])
+    lg = logits.reshape(B, L + 1, V)[perm].reshape(-1, V)
+    qp = qq.reshape(B, L, V)[perm].reshape(-1, V)
+    dp = drafts.reshape(B, L)[perm].reshape(-1)
+    res2 = oracle.sample("stochastic", users[perm], np.full(B, L), lg, dp, qp, seed=2, round_=5)
+    assert np.array_equal(res2["n_acc"], res["n_acc"][perm])
+    assert np.array_equal(res2["token"], res["token"][perm])
