@@ -1,0 +1,232 @@
+/*
+ * sd_verify.h -- C ABI of the batched speculative-verify library (gfx950).
+ *
+ * The library runs the edge server's verification step of distributed
+ * speculative decoding (DiP-SD, arXiv 2604.20919, Sec. II-A step 2): one
+ * target-model forward over a batch of users, each bringing its cached
+ * prefix plus l_m drafted tokens, then per-user accept/reject with one bonus
+ * or resampled token.  A batch is one column n of the user-to-batch
+ * assignment x_mn (eq. 7-8), every user in it has an integer draft length
+ * l_m >= 1 (eq. 9), and a declared batch is never empty (eq. 10).
+ *
+ * Conventions for every entry point:
+ *   - Every call returns an sd_status (0 = SD_OK, negative = error).  No call
+ *     throws or aborts.  On any error return nothing has changed: no user
+ *     state, page, or pending batch is modified and nothing was enqueued.
+ *   - "device" pointers are HIP device allocations on the context's device;
+ *     "host" pointers are ordinary host memory.  The caller owns every buffer
+ *     it passes; the library keeps device pointers (weights, KV pool,
+ *     workspace) until sd_verify_destroy and never allocates or frees device
+ *     memory itself.
+ *   - Streams are hipStream_t values passed as sd_stream (NULL = the null
+ *     stream).  Work is enqueued asynchronously; sd_accept is the only call
+ *     that waits for the GPU.
+ *   - One context must not be used from two host threads at once.
+ *   - The tensor element type is set by sd_config.dtype: SD_BF16 (bf16
+ *     weights, bf16 KV cache, bf16 GEMM inputs, fp32 residual stream) or
+ *     SD_F32 (everything fp32).  Norm gains use the same type.
+ */
+#ifndef SD_VERIFY_H
+#define SD_VERIFY_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t sd_status;
+enum {
+    SD_OK = 0,
+    SD_EINVAL = -1,   /* bad argument (range, shape, unknown user, empty batch) */
+    SD_ENOMEM = -2,   /* KV page pool exhausted or workspace too small */
+    SD_EHIP = -3,     /* a HIP runtime call failed */
+    SD_ESTATE = -4,   /* call out of order (batch pending / not pending) */
+    SD_EDEVICE = -5,  /* the GPU found bad input data (token id out of range) */
+    SD_ENOTIMPL = -6, /* configuration not supported by this build */
+    SD_ENODEV = -7    /* no usable gfx950 device */
+};
+
+enum { SD_F32 = 0, SD_BF16 = 1 };
+
+/* verification modes */
+enum {
+    SD_GREEDY = 0,     /* accept a draft iff it is the target's argmax; the
+                          correction / bonus token is the argmax */
+    SD_STOCHASTIC = 1, /* speculative sampling: accept iff u < p(d)/q(d); on the
+                          first rejection draw from norm(max(0, p - q)); if all
+                          drafts pass draw the bonus token from p */
+    SD_FORCE = 2       /* teacher forcing: every draft is accepted; the returned
+                          token is the argmax after the last draft (prefill) */
+};
+
+typedef void* sd_stream; /* a hipStream_t */
+
+typedef struct sd_config {
+    int32_t n_layers;     /* J */
+    int32_t d_model;      /* h1 */
+    int32_t n_q_heads;
+    int32_t n_kv_heads;   /* n_q_heads must be a multiple */
+    int32_t head_dim;     /* 64 or 128 */
+    int32_t d_ffn;        /* h2 (SwiGLU width) */
+    int32_t vocab;
+    int32_t qk_norm;      /* 1: per-head RMSNorm on q and k before RoPE */
+    int32_t dtype;        /* SD_BF16 or SD_F32 */
+    int32_t page_tokens;  /* KV page size in tokens; must be 16 */
+    int32_t n_pages;      /* pages in the KV pool */
+    int32_t max_users;    /* user ids are 0 .. max_users-1 */
+    int32_t max_draft;    /* largest l_m accepted (<= 64) */
+    int32_t max_batch_users;  /* most users in one batch */
+    int32_t max_batch_tokens; /* most query slots sum(l_m + 1) in one batch */
+    int32_t max_ctx;      /* largest i_m + l_m + 1 of any user */
+    int32_t max_pending;  /* batches that may be in flight at once (1..8) */
+    float rope_base;      /* RoPE base (1e6 for Qwen3 shapes) */
+    float rms_eps;        /* RMSNorm epsilon */
+} sd_config;
+
+/* Device pointers of one decoder layer, each row-major [out][in] so that
+ * y = W x; element type sd_config.dtype. */
+typedef struct sd_layer_weights {
+    const void* wq;     /* [n_q_heads*head_dim][d_model] */
+    const void* wk;     /* [n_kv_heads*head_dim][d_model] */
+    const void* wv;     /* [n_kv_heads*head_dim][d_model] */
+    const void* wo;     /* [d_model][n_q_heads*head_dim] */
+    const void* wg;     /* [d_ffn][d_model]  (SwiGLU gate) */
+    const void* wu;     /* [d_ffn][d_model]  (SwiGLU up) */
+    const void* wd;     /* [d_model][d_ffn]  (down) */
+    const void* norm1;  /* [d_model] pre-attention RMSNorm gain */
+    const void* norm2;  /* [d_model] pre-FFN RMSNorm gain */
+    const void* qnorm;  /* [head_dim] (ignored unless qk_norm) */
+    const void* knorm;  /* [head_dim] (ignored unless qk_norm) */
+} sd_layer_weights;
+
+typedef struct sd_weights {
+    const void* embed;    /* device [vocab][d_model] */
+    const void* lm_head;  /* device [vocab][d_model] (untied) */
+    const void* norm_f;   /* device [d_model] final RMSNorm gain */
+    const sd_layer_weights* layers; /* host array of n_layers entries (copied) */
+} sd_weights;
+
+typedef struct sd_ctx sd_ctx;
+
+/* Device memory the caller must provide for `cfg`.
+ * kv_pool_bytes: the paged KV cache, n_pages pages of page_tokens tokens for
+ *   every layer and KV head (K and V), in dtype.
+ * workspace_bytes: activations, logits and per-batch staging for max_pending
+ *   batches of up to max_batch_tokens slots.
+ * Returns SD_EINVAL if cfg is inconsistent. Host-only; needs no device. */
+sd_status sd_verify_query_sizes(const sd_config* cfg, uint64_t* kv_pool_bytes,
+                                uint64_t* workspace_bytes);
+
+/* Create a context on the current HIP device.
+ * w: weights as above (device pointers, kept until destroy).
+ * kv_pool / workspace: device buffers of at least the queried sizes, 256-byte
+ *   aligned, owned by the caller, kept until destroy.  The workspace is
+ *   initialised here (stream-ordered on the null stream, then synchronised).
+ * out: receives the context.  Errors: SD_EINVAL (cfg, NULL pointer),
+ * SD_ENODEV (current device is not gfx950), SD_EHIP. */
+sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_pool,
+                         void* workspace, sd_ctx** out);
+
+/* Destroy a context (waits for pending work; frees host state only). */
+sd_status sd_verify_destroy(sd_ctx* ctx);
+
+/* Start (or restart) user `user` with a cached context of prefix_len tokens
+ * i_m (positions 0..i_m-1, Sec. II-A: the prompt plus accepted tokens) and
+ * root token root_token (the last emitted token, not yet in the cache; it is
+ * query slot 0 of the next verify).  Reserves ceil(i_m / page_tokens) pages;
+ * pages the user already held are kept in order, so re-calling with a
+ * shorter or equal length keeps the cached entries.  New pages hold
+ * undefined data until written with sd_kv_write.
+ * Errors: SD_EINVAL (user, length or token out of range), SD_ESTATE (user is
+ * in a pending batch), SD_ENOMEM (pool exhausted). */
+sd_status sd_user_reset(sd_ctx* ctx, int32_t user, int32_t prefix_len, int32_t root_token);
+
+/* Drop user `user` and return its pages. SD_ESTATE if it is in a pending batch. */
+sd_status sd_user_release(sd_ctx* ctx, int32_t user);
+
+/* Read a user's state: cached length i_m and root token (host out-params). */
+sd_status sd_user_state(sd_ctx* ctx, int32_t user, int32_t* prefix_len, int32_t* root_token);
+
+/* Copy keys/values of positions pos0..pos0+n-1 of `user`, layer `layer`, into
+ * the paged cache.  k, v: device [n][n_kv_heads][head_dim] in dtype (k after
+ * QK-norm and RoPE, as the forward stores it).  Requires pos0 + n <= the
+ * user's prefix_len.  Enqueued on `stream`. */
+sd_status sd_kv_write(sd_ctx* ctx, int32_t user, int32_t layer, int32_t pos0, int32_t n,
+                      const void* k, const void* v, sd_stream stream);
+
+/* Inverse of sd_kv_write (for tests): k, v device [n][n_kv_heads][head_dim];
+ * positions may reach prefix_len + l_m + 1 of the user's pending batch. */
+sd_status sd_kv_read(sd_ctx* ctx, int32_t user, int32_t layer, int32_t pos0, int32_t n,
+                     void* k, void* v, sd_stream stream);
+
+/*
+ * Enqueue the verification of batch `batch` on `stream`.
+ *   n_users:      M, the length of assign / draft_len
+ *   assign:       host [M], batch index of each user (x_mn as one index per
+ *                 user); users m with assign[m] == batch form the batch, in
+ *                 ascending m.  User ids are 0..M-1 and must have been started
+ *                 with sd_user_reset.
+ *   draft_len:    host [M], l_m for users in the batch (1..max_draft)
+ *   draft_tokens: device int32 [sum l_m], the batch users' drafts in order
+ *   q:            device fp32 [sum l_m][vocab], the draft distribution each
+ *                 draft was sampled from (dense rows; read only in
+ *                 SD_STOCHASTIC mode; may be NULL otherwise)
+ *   mode:         SD_GREEDY, SD_STOCHASTIC or SD_FORCE
+ *   seed, round:  key of the Philox-4x64-10 stream for this round's draws
+ *   accept_u:     device fp32 [sum l_m] accept uniforms, or NULL to draw them
+ *                 from Philox
+ * For every user the forward covers l_m + 1 query slots: the root token at
+ * position i_m followed by the drafts at i_m+1 .. i_m+l_m; their keys and
+ * values are written into the user's pages (reserved here).  Device inputs
+ * must stay valid until sd_accept(batch) returns.  The call does not wait for
+ * the GPU and allocates nothing; the launch shapes depend only on the batch
+ * composition (users, l_m, i_m), so a captured graph of it can be replayed
+ * while those are unchanged.
+ * Errors (nothing enqueued): SD_EINVAL (empty batch, l_m out of range, user
+ * not started, sum l_m+1 > max_batch_tokens, i_m+l_m+1 > max_ctx),
+ * SD_ESTATE (the batch's workspace slot batch % max_pending is busy, or a
+ * user is already pending), SD_ENOMEM (no pages left).
+ */
+sd_status sd_verify_batch(sd_ctx* ctx, int32_t batch, int32_t n_users, const int32_t* assign,
+                          const int32_t* draft_len, const int32_t* draft_tokens, const float* q,
+                          int32_t mode, uint64_t seed, uint64_t round, const float* accept_u,
+                          sd_stream stream);
+
+/*
+ * Wait for batch `batch` and return its decisions (Sec. II-A steps 2-3):
+ *   n_accepted: host [M] (M of the sd_verify_batch call); entry m of every
+ *               batch user receives a_m, the number of leading drafts accepted
+ *   out_token:  host [M]; entry m receives the resampled token (a_m < l_m) or
+ *               the bonus token (a_m == l_m)
+ *   commit:     1 = advance each user (Sec. II-A step 4): i_m += 1 + a_m, root
+ *               := out_token, pages trimmed to the new length; 0 = leave the
+ *               user state unchanged (repeatable measurements)
+ * Entries of users outside the batch are not touched.  Returns SD_EDEVICE,
+ * without committing, if the GPU saw a token id >= vocab.
+ */
+sd_status sd_accept(sd_ctx* ctx, int32_t batch, int32_t* n_accepted, int32_t* out_token,
+                    int32_t commit);
+
+/* Diagnostic: run only the accept/resample step of sd_verify_batch on
+ * caller-supplied logits (device fp32 [sum(l_m+1)][vocab], slot rows of the
+ * batch users in order).  Same arguments and rules otherwise; the batch is
+ * then completed with sd_accept(batch, ..., commit = 0). */
+sd_status sd_sample_logits(sd_ctx* ctx, int32_t batch, int32_t n_users, const int32_t* assign,
+                           const int32_t* draft_len, const int32_t* draft_tokens, const float* q,
+                           const float* logits, int32_t mode, uint64_t seed, uint64_t round,
+                           const float* accept_u, sd_stream stream);
+
+/* Diagnostic: copy the logits of pending batch `batch` (device fp32
+ * [sum(l_m+1)][vocab]) into dst (device), ordered after the batch on
+ * `stream`.  SD_ESTATE if the batch is not pending. */
+sd_status sd_debug_logits(sd_ctx* ctx, int32_t batch, float* dst, sd_stream stream);
+
+/* Static description of a status code. */
+const char* sd_status_str(sd_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SD_VERIFY_H */

@@ -1,0 +1,225 @@
+// Accept/reject and resampling over the full vocabulary (DiP-SD Sec. II-A,
+// step 2: stop at the first rejected draft, emit one bonus or corrected
+// token).  Two kernels, both split over vocab chunks so that every row is
+// read by many workgroups at once:
+//   phase A, per query slot: row max, sum of exp(z - max) and argmax (lowest
+//     index on ties); the last chunk workgroup of a slot merges the chunk
+//     partials in chunk order and takes the slot's accept decision:
+//     greedy: draft == argmax; stochastic: u < p(d)/q(d) as an fp32
+//     division, u from the caller or from Philox;
+//   phase B, per user: a = number of leading accepts; greedy/force emit the
+//     argmax of slot a (force: slot l); stochastic runs an exponential race
+//     argmax_k w_k / E_k with w = max(0, p - q) at slot a (p itself when all
+//     drafts passed, or when the residual is empty), E_k unit exponentials
+//     from Philox keyed by (round, user, slot, k).  Chunk winners are merged
+//     in chunk order (ties to the lowest index).
+#include "sdv_device.h"
+#include "sdv_internal.h"
+
+namespace sdv {
+
+struct SampP {
+    BatchView bv;
+    const float* logits;  // [T][V]
+    int V, cw;            // vocab, chunk width (multiple of 4)
+    float* sstat;         // [T][4]
+    float* spartA;        // [T][kVocabChunks][4]
+    float* spartB;        // [B][kVocabChunks][4]
+    int32_t* cntA;        // [T]
+    int32_t* cntB;        // [B]
+    int32_t* result;      // n_acc [Bmax], token [Bmax], flags
+    int bmax;
+};
+
+__device__ __forceinline__ void merge_ms(float& m, float& s, float m2, float s2) {
+    if (m2 == -INFINITY) return;
+    if (m == -INFINITY) { m = m2; s = s2; return; }
+    if (m2 > m) { s = s * expf(m - m2) + s2; m = m2; }
+    else s += s2 * expf(m2 - m);
+}
+
+__global__ __launch_bounds__(256) void k_sample_a(SampP p) {
+    __shared__ float sm[4], ss[4], sv[4];
+    __shared__ int si[4];
+    __shared__ int last;
+    const int t = blockIdx.x, c = blockIdx.y;
+    const float* z = p.logits + (size_t)t * p.V;
+    const int k0 = c * p.cw, k1 = min(p.V, k0 + p.cw);
+    float m = -INFINITY, s = 0.f, bv = -INFINITY;
+    int bi = 0x7fffffff;
+    for (int k = k0 + threadIdx.x; k < k1; k += 256) {
+        const float v = z[k];
+        if (v > bv) { bv = v; bi = k; }  // increasing k per thread: first max kept
+        if (v > m) { s = (m == -INFINITY ? 0.f : s * expf(m - v)) + 1.f; m = v; }
+        else if (v != -INFINITY) s += expf(v - m);
+    }
+    // wave reduce (max, sum) and (value, index)
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const float m2 = __shfl_xor(m, o, 64), s2 = __shfl_xor(s, o, 64);
+        merge_ms(m, s, m2, s2);
+        const float v2 = __shfl_xor(bv, o, 64);
+        const int i2 = __shfl_xor(bi, o, 64);
+        if (v2 > bv || (v2 == bv && i2 < bi)) { bv = v2; bi = i2; }
+    }
+    const int w = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) { sm[w] = m; ss[w] = s; sv[w] = bv; si[w] = bi; }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int i = 1; i < 4; ++i) {
+            merge_ms(m, s, sm[i], ss[i]);
+            if (sv[i] > bv || (sv[i] == bv && si[i] < bi)) { bv = sv[i]; bi = si[i]; }
+        }
+        float* dst = p.spartA + ((size_t)t * kVocabChunks + c) * 4;
+        dst[0] = m; dst[1] = s; dst[2] = bv; dst[3] = __int_as_float(bi);
+        __threadfence();
+        last = (atomicAdd(p.cntA + t, 1) == (int)gridDim.y - 1);
+    }
+    __syncthreads();
+    if (!last || threadIdx.x != 0) return;
+    __threadfence();
+    float M = -INFINITY, S = 0.f, BV = -INFINITY;
+    int BI = 0;
+    for (int i = 0; i < (int)gridDim.y; ++i) {
+        const float* e = p.spartA + ((size_t)t * kVocabChunks + i) * 4;
+        merge_ms(M, S, e[0], e[1]);
+        if (e[2] > BV) { BV = e[2]; BI = __float_as_int(e[3]); }
+    }
+    p.cntA[t] = 0;
+    const BatchView& bv2 = p.bv;
+    const int b = bv2.slot_b[t], j = bv2.slot_j[t];
+    float acc = 0.f;
+    if (j < bv2.L[b]) {
+        const int di = bv2.draft_off[b] + j;
+        int d = bv2.drafts[di];
+        if (d < 0 || d >= p.V) d = 0;  // flagged by the prepare kernel
+        if (bv2.mode == 0) acc = (d == BI) ? 1.f : 0.f;
+        else if (bv2.mode == 2) acc = 1.f;
+        else {
+            const float pd = expf(z[d] - M) / S;
+            const float qd = bv2.q[(size_t)di * p.V + d];
+            const float r = pd / qd;
+            float u;
+            if (bv2.accept_u) u = bv2.accept_u[di];
+            else {
+                const u64x4 ctr = {bv2.round, (uint64_t)bv2.user_id[b],
+                                   ((uint64_t)PURPOSE_ACCEPT << 32) | (uint64_t)j, 0ull};
+                u = accept_uniform(philox4x64_10(ctr, bv2.seed, 0ull).x);
+            }
+            acc = (u < r) ? 1.f : 0.f;
+        }
+    }
+    float* st4 = p.sstat + (size_t)t * 4;
+    st4[0] = M; st4[1] = S; st4[2] = __int_as_float(BI); st4[3] = acc;
+}
+
+__global__ __launch_bounds__(256) void k_sample_b(SampP p) {
+    __shared__ float sk[2][4];
+    __shared__ int sidx[2][4];
+    __shared__ int last;
+    const int b = blockIdx.x, c = blockIdx.y;
+    const BatchView& bv = p.bv;
+    const int Lb = bv.L[b];
+    const int so = bv.slot_off[b];
+    int a = 0;
+    if (bv.mode == 2) a = Lb;
+    else
+        while (a < Lb && p.sstat[(size_t)(so + a) * 4 + 3] != 0.f) ++a;
+    const float* st4 = p.sstat + (size_t)(so + a) * 4;
+    if (bv.mode != 1) {
+        if (c == 0 && threadIdx.x == 0) {
+            p.result[b] = a;
+            p.result[p.bmax + b] = __float_as_int(st4[2]);
+            if (b == 0) p.result[2 * p.bmax] = *bv.flags;
+        }
+        return;
+    }
+    const float M = st4[0], S = st4[1];
+    const float* z = p.logits + (size_t)(so + a) * p.V;
+    const bool resid = a < Lb;
+    const float* qr = resid ? bv.q + (size_t)(bv.draft_off[b] + a) * p.V : nullptr;
+    const uint64_t user = (uint64_t)bv.user_id[b];
+    const int k0 = c * p.cw, k1 = min(p.V, k0 + p.cw);
+    float br = -1.f, bp = -1.f;  // best residual / target keys
+    int ir = 0x7fffffff, ip = 0x7fffffff;
+    for (int k4 = k0 + 4 * threadIdx.x; k4 < k1; k4 += 4 * 256) {
+        const u64x4 ctr = {bv.round, user, ((uint64_t)PURPOSE_RACE << 32) | (uint64_t)a,
+                           (uint64_t)(k4 >> 2)};
+        const u64x4 rnd = philox4x64_10(ctr, bv.seed, 0ull);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int k = k4 + e;
+            if (k >= k1) break;
+            const float pk = expf(z[k] - M) / S;
+            const float E = race_exponential(word_of(rnd, e));
+            if (pk > 0.f) {
+                const float kp = pk / E;
+                if (kp > bp) { bp = kp; ip = k; }
+            }
+            if (resid) {
+                const float wk = fmaxf(pk - qr[k], 0.f);
+                if (wk > 0.f) {
+                    const float kr = wk / E;
+                    if (kr > br) { br = kr; ir = k; }
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const float b2 = __shfl_xor(br, o, 64);
+        const int i2 = __shfl_xor(ir, o, 64);
+        if (b2 > br || (b2 == br && i2 < ir)) { br = b2; ir = i2; }
+        const float p2 = __shfl_xor(bp, o, 64);
+        const int j2 = __shfl_xor(ip, o, 64);
+        if (p2 > bp || (p2 == bp && j2 < ip)) { bp = p2; ip = j2; }
+    }
+    const int w = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) { sk[0][w] = br; sidx[0][w] = ir; sk[1][w] = bp; sidx[1][w] = ip; }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int i = 1; i < 4; ++i) {
+            if (sk[0][i] > br || (sk[0][i] == br && sidx[0][i] < ir)) { br = sk[0][i]; ir = sidx[0][i]; }
+            if (sk[1][i] > bp || (sk[1][i] == bp && sidx[1][i] < ip)) { bp = sk[1][i]; ip = sidx[1][i]; }
+        }
+        float* dst = p.spartB + ((size_t)b * kVocabChunks + c) * 4;
+        dst[0] = br; dst[1] = __int_as_float(ir); dst[2] = bp; dst[3] = __int_as_float(ip);
+        __threadfence();
+        last = (atomicAdd(p.cntB + b, 1) == (int)gridDim.y - 1);
+    }
+    __syncthreads();
+    if (!last || threadIdx.x != 0) return;
+    __threadfence();
+    float BR = -1.f, BP = -1.f;
+    int IR = 0, IP = 0;
+    for (int i = 0; i < (int)gridDim.y; ++i) {
+        const float* e = p.spartB + ((size_t)b * kVocabChunks + i) * 4;
+        if (e[0] > BR) { BR = e[0]; IR = __float_as_int(e[1]); }
+        if (e[2] > BP) { BP = e[2]; IP = __float_as_int(e[3]); }
+    }
+    p.cntB[b] = 0;
+    p.result[b] = a;
+    p.result[p.bmax + b] = (resid && BR > 0.f) ? IR : IP;
+    if (b == 0) p.result[2 * p.bmax] = *bv.flags;
+}
+
+void launch_sampler(const Dims& D, const BatchView& bv, const SlotBufs& sb, const float* logits,
+                    hipStream_t s) {
+    SampP p;
+    p.bv = bv;
+    p.logits = logits;
+    p.V = D.V;
+    p.cw = ((D.V + kVocabChunks - 1) / kVocabChunks + 3) & ~3;
+    p.sstat = sb.sstat;
+    p.spartA = sb.spart;
+    p.spartB = sb.spartB;
+    p.cntA = sb.scount;
+    p.cntB = sb.scountB;
+    p.result = sb.result;
+    p.bmax = sb.bmax;
+    const int chunks = (D.V + p.cw - 1) / p.cw;
+    hipLaunchKernelGGL(k_sample_a, dim3(bv.T, chunks), dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_sample_b, dim3(bv.B, chunks), dim3(256), 0, s, p);
+}
+
+}  // namespace sdv

@@ -1,0 +1,747 @@
+// Host runtime and C ABI of the batched speculative-verify library.
+//
+// The host side owns user state (cached length i_m, root token, KV pages),
+// the page free list, per-batch staging and the launch sequence of one verify
+// pass.  All device memory (weights, KV pool, workspace) belongs to the
+// caller; this file never allocates device memory.  Batches are validated and
+// planned on the host before anything is enqueued, so an error return leaves
+// every state untouched.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/sd_verify.h"
+#include "sdv_internal.h"
+
+using namespace sdv;
+
+namespace sdv {
+bool gemm_shape_ok(const Dims& D, int T, int K, int N, int epi);
+}
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+int ceil_div(long a, long b) { return (int)((a + b - 1) / b); }
+
+// Byte layout of one workspace slot and of the staging block inside it.
+struct Layout {
+    // staging block (int32 offsets within the block)
+    size_t st_user, st_prefix, st_L, st_root, st_soff, st_doff, st_sb, st_sj, st_pt, st_items,
+        st_ioff, st_flags, st_bytes;
+    // slot buffers (byte offsets within the slot)
+    size_t stage, tok, cs, x, h, ffn, qkv, qbuf, attn, apart, aml, gpart, gcount, logits, sstat, spart,
+        spartB, scount, scountB, result, slot_bytes;
+    size_t gpart_floats;
+    int gcount_n;
+    // global region after the slots
+    size_t kvw_pages, total;
+    int max_pages, max_items, rows_max, Tmax, Bmax;
+};
+
+Dims dims_of(const sd_config& c) {
+    Dims D;
+    D.L = c.n_layers;
+    D.d = c.d_model;
+    D.hq = c.n_q_heads;
+    D.hkv = c.n_kv_heads;
+    D.hd = c.head_dim;
+    D.F = c.d_ffn;
+    D.V = c.vocab;
+    D.qk_norm = c.qk_norm;
+    D.bf16 = c.dtype == SD_BF16;
+    D.rope_base = c.rope_base;
+    D.eps = c.rms_eps;
+    return D;
+}
+
+sd_status validate_config(const sd_config* c) {
+    if (!c) return SD_EINVAL;
+    if (c->n_layers < 1 || c->d_model < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1 ||
+        c->head_dim < 2 || c->d_ffn < 1 || c->vocab < 2)
+        return SD_EINVAL;
+    if (c->n_q_heads % c->n_kv_heads) return SD_EINVAL;
+    if (c->head_dim % 2 || c->head_dim > 128) return SD_EINVAL;
+    if (c->dtype != SD_F32 && c->dtype != SD_BF16) return SD_EINVAL;
+    if (c->page_tokens != kPageTokens) return SD_EINVAL;
+    if (c->n_pages < 1 || c->max_users < 1 || c->max_draft < 1 || c->max_draft > 64) return SD_EINVAL;
+    if (c->max_batch_users < 1 || c->max_batch_tokens < 2 || c->max_ctx < 2) return SD_EINVAL;
+    if (c->max_pending < 1 || c->max_pending > kMaxPending) return SD_EINVAL;
+    if (!(c->rope_base > 1.0f) || !(c->rms_eps >= 0.0f)) return SD_EINVAL;
+    if (c->qk_norm != 0 && c->qk_norm != 1) return SD_EINVAL;
+    if (c->dtype == SD_BF16) {
+        // MFMA kernels: 128-wide heads, k dimensions in whole LDS chunks and
+        // output widths in whole 128-column tiles
+        if (c->head_dim != 128) return SD_ENOTIMPL;
+        const Dims D = dims_of(*c);
+        if (D.d % 256 || D.nq() % 256 || D.F % 256) return SD_ENOTIMPL;
+        if (D.nqkv() % 128 || D.d % 128 || (2 * D.F) % 128 || D.V % 128) return SD_ENOTIMPL;
+        if (D.hq * D.hd % 16 || D.hkv * D.hd % 16) return SD_ENOTIMPL;
+        if (c->max_batch_tokens > 416) return SD_ENOTIMPL;
+    } else {
+        if (c->head_dim > 128) return SD_ENOTIMPL;
+    }
+    return SD_OK;
+}
+
+Layout plan(const sd_config& c) {
+    const Dims D = dims_of(c);
+    Layout L;
+    L.Tmax = c.max_batch_tokens;
+    L.Bmax = c.max_batch_users;
+    L.max_pages = ceil_div(c.max_ctx, kPageTokens);
+    L.max_items = L.Bmax * D.hkv * ceil_div(c.max_ctx, kAttnChunk);
+    L.rows_max = (c.max_draft + 1) * D.G();
+    const size_t es = D.bf16 ? 2 : 4;
+    // staging block
+    size_t o = 0;
+    auto take_i = [&](size_t n) { size_t r = o; o = align_up(o + n * 4); return r; };
+    L.st_user = take_i(L.Bmax);
+    L.st_prefix = take_i(L.Bmax);
+    L.st_L = take_i(L.Bmax);
+    L.st_root = take_i(L.Bmax);
+    L.st_soff = take_i(L.Bmax + 1);
+    L.st_doff = take_i(L.Bmax + 1);
+    L.st_sb = take_i(L.Tmax);
+    L.st_sj = take_i(L.Tmax);
+    L.st_pt = take_i((size_t)L.Bmax * L.max_pages);
+    L.st_items = take_i((size_t)L.max_items * 4);
+    L.st_ioff = take_i(L.Bmax + 1);
+    L.st_flags = take_i(4);
+    L.st_bytes = o;
+    // slot
+    size_t s = 0;
+    auto take = [&](size_t bytes) { size_t r = s; s = align_up(s + bytes); return r; };
+    L.stage = take(L.st_bytes);
+    L.tok = take((size_t)L.Tmax * 4);
+    L.cs = take((size_t)L.Tmax * (D.hd / 2) * 2 * 4);
+    L.x = take((size_t)L.Tmax * D.d * 4);
+    L.h = take((size_t)L.Tmax * D.d * es);
+    L.ffn = take((size_t)L.Tmax * D.F * es);
+    L.qkv = take((size_t)L.Tmax * D.nqkv() * 4);
+    L.qbuf = take((size_t)L.Tmax * D.nq() * es);
+    L.attn = take((size_t)L.Tmax * D.nq() * es);
+    const size_t nparts = D.bf16 ? (size_t)L.max_items * 4 * L.rows_max : 1;
+    L.apart = take(nparts * D.hd * 4);
+    L.aml = take(nparts * 2 * 4);
+    L.gpart_floats = gemm_partial_floats(D, L.Tmax);
+    L.gpart = take(std::max<size_t>(L.gpart_floats, 1) * 4);
+    L.gcount_n = gemm_counter_count(D);
+    L.gcount = take((size_t)L.gcount_n * 4);
+    L.logits = take((size_t)L.Tmax * D.V * 4);
+    L.sstat = take((size_t)L.Tmax * 4 * 4);
+    L.spart = take((size_t)L.Tmax * kVocabChunks * 4 * 4);
+    L.spartB = take((size_t)L.Bmax * kVocabChunks * 4 * 4);
+    L.scount = take((size_t)L.Tmax * 4);
+    L.scountB = take((size_t)L.Bmax * 4);
+    L.result = take((size_t)(2 * L.Bmax + 4) * 4);
+    L.slot_bytes = s;
+    L.kvw_pages = L.slot_bytes * (size_t)c.max_pending;
+    L.total = align_up(L.kvw_pages + (size_t)L.max_pages * 4);
+    return L;
+}
+
+struct User {
+    bool active = false;
+    int prefix = 0;
+    int root = 0;
+    std::vector<int> pages;
+    int pending_slot = -1;
+};
+
+struct Slot {
+    bool pending = false;
+    bool sample_only = false;
+    int batch = -1;
+    int B = 0, T = 0, nd = 0;
+    std::vector<int> users;  // global ids in batch order
+    std::vector<int> L;
+    hipEvent_t done = nullptr;
+    char* stage_host = nullptr;  // pinned
+    int32_t* result_host = nullptr;  // pinned
+    char* base = nullptr;        // device slot base
+    SlotBufs bufs{};
+};
+
+}  // namespace
+
+struct sd_ctx {
+    sd_config cfg{};
+    Dims D{};
+    Layout lay{};
+    sd_weights w{};
+    std::vector<sd_layer_weights> layers;
+    KVPool kv{};
+    char* ws = nullptr;
+    std::vector<User> users;
+    std::vector<int> free_pages;  // stack: back is allocated first
+    Slot slots[kMaxPending];
+    int32_t* kvw_host = nullptr;  // pinned page list for kv copies
+    int device = 0;
+};
+
+namespace {
+
+sd_status hip_status(hipError_t e) { return e == hipSuccess ? SD_OK : SD_EHIP; }
+
+#define SD_HIP(expr)                                            \
+    do {                                                        \
+        hipError_t _e = (expr);                                 \
+        if (_e != hipSuccess) return SD_EHIP;                   \
+    } while (0)
+
+int pages_for(int tokens) { return ceil_div(tokens, kPageTokens); }
+
+void release_to(sd_ctx* c, User& u, int keep) {
+    while ((int)u.pages.size() > keep) {
+        c->free_pages.push_back(u.pages.back());
+        u.pages.pop_back();
+    }
+}
+
+bool reserve_to(sd_ctx* c, User& u, int want) {
+    const int need = want - (int)u.pages.size();
+    if (need <= 0) return true;
+    if ((int)c->free_pages.size() < need) return false;
+    for (int i = 0; i < need; ++i) {
+        u.pages.push_back(c->free_pages.back());
+        c->free_pages.pop_back();
+    }
+    return true;
+}
+
+BatchView make_view(sd_ctx* c, Slot& s) {
+    const Layout& L = c->lay;
+    char* st = s.base + L.stage;
+    BatchView v{};
+    v.user_id = (const int32_t*)(st + L.st_user);
+    v.prefix = (const int32_t*)(st + L.st_prefix);
+    v.L = (const int32_t*)(st + L.st_L);
+    v.root = (const int32_t*)(st + L.st_root);
+    v.slot_off = (const int32_t*)(st + L.st_soff);
+    v.draft_off = (const int32_t*)(st + L.st_doff);
+    v.slot_b = (const int32_t*)(st + L.st_sb);
+    v.slot_j = (const int32_t*)(st + L.st_sj);
+    v.page_table = (const int32_t*)(st + L.st_pt);
+    v.items = (const int4*)(st + L.st_items);
+    v.item_off = (const int32_t*)(st + L.st_ioff);
+    v.flags = (int32_t*)(st + L.st_flags);
+    v.max_pages = L.max_pages;
+    return v;
+}
+
+// Collect the users of batch `batch` and validate every argument that does
+// not need the device.  Fills users / Ls / T / nd.
+sd_status collect_batch(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t* assign,
+                        const int32_t* draft_len, bool need_active, std::vector<int>& users,
+                        std::vector<int>& Ls, int& T, int& nd) {
+    if (batch < 0 || n_users < 1 || n_users > c->cfg.max_users || !assign || !draft_len)
+        return SD_EINVAL;
+    users.clear();
+    Ls.clear();
+    T = 0;
+    nd = 0;
+    for (int m = 0; m < n_users; ++m) {
+        if (assign[m] != batch) continue;
+        const int L = draft_len[m];
+        if (L < 1 || L > c->cfg.max_draft) return SD_EINVAL;
+        const User& u = c->users[m];
+        if (need_active) {
+            if (!u.active) return SD_EINVAL;
+            if (u.prefix + L + 1 > c->cfg.max_ctx) return SD_EINVAL;
+        }
+        if (u.pending_slot >= 0) return SD_ESTATE;
+        users.push_back(m);
+        Ls.push_back(L);
+        T += L + 1;
+        nd += L;
+    }
+    if (users.empty()) return SD_EINVAL;  // eq. (10): a declared batch is active
+    if ((int)users.size() > c->cfg.max_batch_users || T > c->cfg.max_batch_tokens) return SD_EINVAL;
+    return SD_OK;
+}
+
+// Write the staging block for the batch into the slot's pinned buffer.
+void build_stage(sd_ctx* c, Slot& s, int mode, bool with_items, int* n_items, int* rows_max) {
+    const Layout& L = c->lay;
+    char* st = s.stage_host;
+    int32_t* user = (int32_t*)(st + L.st_user);
+    int32_t* prefix = (int32_t*)(st + L.st_prefix);
+    int32_t* Lb = (int32_t*)(st + L.st_L);
+    int32_t* root = (int32_t*)(st + L.st_root);
+    int32_t* soff = (int32_t*)(st + L.st_soff);
+    int32_t* doff = (int32_t*)(st + L.st_doff);
+    int32_t* sb = (int32_t*)(st + L.st_sb);
+    int32_t* sj = (int32_t*)(st + L.st_sj);
+    int32_t* pt = (int32_t*)(st + L.st_pt);
+    int32_t* items = (int32_t*)(st + L.st_items);
+    int32_t* ioff = (int32_t*)(st + L.st_ioff);
+    int32_t* flags = (int32_t*)(st + L.st_flags);
+    (void)mode;
+    soff[0] = 0;
+    doff[0] = 0;
+    int maxL = 0, ni = 0;
+    ioff[0] = 0;
+    for (int b = 0; b < s.B; ++b) {
+        const User& u = c->users[s.users[b]];
+        user[b] = s.users[b];
+        prefix[b] = u.prefix;
+        Lb[b] = s.L[b];
+        root[b] = u.root;
+        soff[b + 1] = soff[b] + s.L[b] + 1;
+        doff[b + 1] = doff[b] + s.L[b];
+        for (int j = 0; j <= s.L[b]; ++j) {
+            sb[soff[b] + j] = b;
+            sj[soff[b] + j] = j;
+        }
+        for (int i = 0; i < L.max_pages; ++i)
+            pt[(size_t)b * L.max_pages + i] = i < (int)u.pages.size() ? u.pages[i] : 0;
+        maxL = std::max(maxL, s.L[b]);
+        if (with_items) {
+            const int ctx = u.prefix + s.L[b] + 1;
+            const int nch = ceil_div(ctx, kAttnChunk);
+            for (int g = 0; g < c->D.hkv; ++g)
+                for (int ch = 0; ch < nch; ++ch) {
+                    items[ni * 4 + 0] = b;
+                    items[ni * 4 + 1] = g;
+                    items[ni * 4 + 2] = ch * kAttnChunk;
+                    items[ni * 4 + 3] = std::min(ctx, (ch + 1) * kAttnChunk);
+                    ++ni;
+                }
+        }
+        ioff[b + 1] = ni;
+    }
+    flags[0] = flags[1] = flags[2] = flags[3] = 0;
+    *n_items = ni;
+    *rows_max = (maxL + 1) * c->D.G();
+}
+
+sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t st) {
+    const Dims& D = c->D;
+    const SlotBufs& sb = s.bufs;
+    launch_prepare(D, bv, sb, st);
+    launch_embed(D, bv, c->w.embed, sb, st);
+    const int T = bv.T;
+    for (int l = 0; l < D.L; ++l) {
+        const sd_layer_weights& w = c->layers[l];
+        launch_rmsnorm(D, T, sb.x, w.norm1, sb.h, st);
+        GemmCall g{};
+        g.X = sb.h;
+        g.W[0] = w.wq; g.W[1] = w.wk; g.W[2] = w.wv;
+        g.seg[0] = 0; g.seg[1] = D.nq(); g.seg[2] = D.nq() + D.nkv();
+        g.nseg = 3;
+        g.N = D.nqkv();
+        g.K = D.d;
+        g.T = T;
+        g.epi = EPI_STORE;
+        g.out = sb.qkv;
+        g.ldo = D.nqkv();
+        launch_gemm(D, g, sb, st);
+        launch_qkrope(D, bv, sb, c->kv, l, w.qnorm, w.knorm, st);
+        launch_attention(D, bv, sb, c->kv, l, st);
+        GemmCall o{};
+        o.X = sb.attn;
+        o.W[0] = w.wo;
+        o.nseg = 1;
+        o.N = D.d;
+        o.K = D.nq();
+        o.T = T;
+        o.epi = EPI_RESID;
+        o.out = sb.x;
+        o.ldo = D.d;
+        launch_gemm(D, o, sb, st);
+        launch_rmsnorm(D, T, sb.x, w.norm2, sb.h, st);
+        GemmCall gu{};
+        gu.X = sb.h;
+        gu.W[0] = w.wg; gu.W[1] = w.wu;
+        gu.nseg = 2;
+        gu.seg[1] = D.F;
+        gu.N = D.F;
+        gu.K = D.d;
+        gu.T = T;
+        gu.epi = EPI_SWIGLU;
+        gu.out = sb.ffn;
+        gu.ldo = D.F;
+        launch_gemm(D, gu, sb, st);
+        GemmCall dn{};
+        dn.X = sb.ffn;
+        dn.W[0] = w.wd;
+        dn.nseg = 1;
+        dn.N = D.d;
+        dn.K = D.F;
+        dn.T = T;
+        dn.epi = EPI_RESID;
+        dn.out = sb.x;
+        dn.ldo = D.d;
+        launch_gemm(D, dn, sb, st);
+    }
+    launch_rmsnorm(D, T, sb.x, c->w.norm_f, sb.h, st);
+    GemmCall lm{};
+    lm.X = sb.h;
+    lm.W[0] = c->w.lm_head;
+    lm.nseg = 1;
+    lm.N = D.V;
+    lm.K = D.d;
+    lm.T = T;
+    lm.epi = EPI_STORE;
+    lm.out = sb.logits;
+    lm.ldo = D.V;
+    launch_gemm(D, lm, sb, st);
+    return hip_status(hipGetLastError());
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sd_status_str(sd_status s) {
+    switch (s) {
+        case SD_OK: return "ok";
+        case SD_EINVAL: return "invalid argument";
+        case SD_ENOMEM: return "out of KV pages or workspace";
+        case SD_EHIP: return "HIP runtime error";
+        case SD_ESTATE: return "call out of order";
+        case SD_EDEVICE: return "device reported bad input data";
+        case SD_ENOTIMPL: return "configuration not supported";
+        case SD_ENODEV: return "no gfx950 device";
+    }
+    return "unknown status";
+}
+
+sd_status sd_verify_query_sizes(const sd_config* cfg, uint64_t* kv_pool_bytes,
+                                uint64_t* workspace_bytes) {
+    sd_status r = validate_config(cfg);
+    if (r != SD_OK) return r;
+    if (!kv_pool_bytes || !workspace_bytes) return SD_EINVAL;
+    const Dims D = dims_of(*cfg);
+    const size_t es = D.bf16 ? 2 : 4;
+    *kv_pool_bytes = (uint64_t)D.L * cfg->n_pages * 2 * D.hkv * kPageTokens * D.hd * es;
+    *workspace_bytes = plan(*cfg).total;
+    return SD_OK;
+}
+
+sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_pool, void* workspace,
+                         sd_ctx** out) {
+    if (!out) return SD_EINVAL;
+    *out = nullptr;
+    sd_status r = validate_config(cfg);
+    if (r != SD_OK) return r;
+    if (!w || !w->embed || !w->lm_head || !w->norm_f || !w->layers || !kv_pool || !workspace)
+        return SD_EINVAL;
+    if (((uintptr_t)kv_pool | (uintptr_t)workspace) & (kAlign - 1)) return SD_EINVAL;
+    for (int l = 0; l < cfg->n_layers; ++l) {
+        const sd_layer_weights& lw = w->layers[l];
+        if (!lw.wq || !lw.wk || !lw.wv || !lw.wo || !lw.wg || !lw.wu || !lw.wd || !lw.norm1 ||
+            !lw.norm2)
+            return SD_EINVAL;
+        if (cfg->qk_norm && (!lw.qnorm || !lw.knorm)) return SD_EINVAL;
+    }
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return SD_ENODEV;
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return SD_ENODEV;
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0) return SD_ENODEV;
+
+    sd_ctx* c = new (std::nothrow) sd_ctx();
+    if (!c) return SD_ENOMEM;
+    c->cfg = *cfg;
+    c->D = dims_of(*cfg);
+    c->lay = plan(*cfg);
+    c->w = *w;
+    c->layers.assign(w->layers, w->layers + cfg->n_layers);
+    c->w.layers = nullptr;
+    c->device = dev;
+    c->kv.base = kv_pool;
+    c->kv.n_pages = cfg->n_pages;
+    c->kv.hkv = c->D.hkv;
+    c->kv.hd = c->D.hd;
+    c->kv.esize = c->D.bf16 ? 2 : 4;
+    c->ws = (char*)workspace;
+    c->users.resize(cfg->max_users);
+    c->free_pages.reserve(cfg->n_pages);
+    for (int p = cfg->n_pages - 1; p >= 0; --p) c->free_pages.push_back(p);
+    const Layout& L = c->lay;
+    bool ok = true;
+    for (int i = 0; i < cfg->max_pending && ok; ++i) {
+        Slot& s = c->slots[i];
+        s.base = c->ws + (size_t)i * L.slot_bytes;
+        ok &= hipHostMalloc((void**)&s.stage_host, L.st_bytes, hipHostMallocDefault) == hipSuccess;
+        ok &= hipHostMalloc((void**)&s.result_host, (size_t)(2 * L.Bmax + 4) * 4,
+                            hipHostMallocDefault) == hipSuccess;
+        ok &= hipEventCreateWithFlags(&s.done, hipEventDisableTiming) == hipSuccess;
+        SlotBufs& b = s.bufs;
+        b.tok = (int32_t*)(s.base + L.tok);
+        b.cs = (float*)(s.base + L.cs);
+        b.x = (float*)(s.base + L.x);
+        b.h = s.base + L.h;
+        b.ffn = s.base + L.ffn;
+        b.qkv = (float*)(s.base + L.qkv);
+        b.qbuf = s.base + L.qbuf;
+        b.attn = s.base + L.attn;
+        b.apart = (float*)(s.base + L.apart);
+        b.aml = (float*)(s.base + L.aml);
+        b.gpart = (float*)(s.base + L.gpart);
+        b.gpart_floats = L.gpart_floats;
+        b.gcount = (int32_t*)(s.base + L.gcount);
+        b.gcount_n = L.gcount_n;
+        b.logits = (float*)(s.base + L.logits);
+        b.sstat = (float*)(s.base + L.sstat);
+        b.spart = (float*)(s.base + L.spart);
+        b.spartB = (float*)(s.base + L.spartB);
+        b.scount = (int32_t*)(s.base + L.scount);
+        b.scountB = (int32_t*)(s.base + L.scountB);
+        b.result = (int32_t*)(s.base + L.result);
+        b.bmax = L.Bmax;
+        if (ok) {
+            // arrival counters start at zero and are reset by their last user
+            ok &= hipMemset(b.gcount, 0, (size_t)L.gcount_n * 4) == hipSuccess;
+            ok &= hipMemset(b.scount, 0, (size_t)L.Tmax * 4) == hipSuccess;
+            ok &= hipMemset(b.scountB, 0, (size_t)L.Bmax * 4) == hipSuccess;
+        }
+    }
+    ok = ok && hipHostMalloc((void**)&c->kvw_host, (size_t)L.max_pages * 4, hipHostMallocDefault) ==
+                   hipSuccess;
+    ok = ok && hipDeviceSynchronize() == hipSuccess;
+    if (!ok) {
+        sd_verify_destroy(c);
+        return SD_EHIP;
+    }
+    *out = c;
+    return SD_OK;
+}
+
+sd_status sd_verify_destroy(sd_ctx* c) {
+    if (!c) return SD_EINVAL;
+    for (int i = 0; i < kMaxPending; ++i) {
+        Slot& s = c->slots[i];
+        if (s.done) {
+            (void)hipEventSynchronize(s.done);
+            (void)hipEventDestroy(s.done);
+        }
+        if (s.stage_host) (void)hipHostFree(s.stage_host);
+        if (s.result_host) (void)hipHostFree(s.result_host);
+    }
+    if (c->kvw_host) (void)hipHostFree(c->kvw_host);
+    delete c;
+    return SD_OK;
+}
+
+sd_status sd_user_reset(sd_ctx* c, int32_t user, int32_t prefix_len, int32_t root_token) {
+    if (!c || user < 0 || user >= c->cfg.max_users) return SD_EINVAL;
+    if (prefix_len < 0 || prefix_len + 2 > c->cfg.max_ctx) return SD_EINVAL;
+    if (root_token < 0 || root_token >= c->cfg.vocab) return SD_EINVAL;
+    User& u = c->users[user];
+    if (u.pending_slot >= 0) return SD_ESTATE;
+    const int want = pages_for(prefix_len);
+    if (want > (int)u.pages.size() &&
+        want - (int)u.pages.size() > (int)c->free_pages.size())
+        return SD_ENOMEM;
+    release_to(c, u, std::max(want, 0));
+    reserve_to(c, u, want);
+    u.active = true;
+    u.prefix = prefix_len;
+    u.root = root_token;
+    return SD_OK;
+}
+
+sd_status sd_user_release(sd_ctx* c, int32_t user) {
+    if (!c || user < 0 || user >= c->cfg.max_users) return SD_EINVAL;
+    User& u = c->users[user];
+    if (u.pending_slot >= 0) return SD_ESTATE;
+    release_to(c, u, 0);
+    u.active = false;
+    u.prefix = 0;
+    u.root = 0;
+    return SD_OK;
+}
+
+sd_status sd_user_state(sd_ctx* c, int32_t user, int32_t* prefix_len, int32_t* root_token) {
+    if (!c || user < 0 || user >= c->cfg.max_users || !prefix_len || !root_token) return SD_EINVAL;
+    const User& u = c->users[user];
+    if (!u.active) return SD_EINVAL;
+    *prefix_len = u.prefix;
+    *root_token = u.root;
+    return SD_OK;
+}
+
+static sd_status kv_copy(sd_ctx* c, int32_t user, int32_t layer, int32_t pos0, int32_t n,
+                         const void* k, const void* v, sd_stream stream, int to_pool) {
+    if (!c || user < 0 || user >= c->cfg.max_users || layer < 0 || layer >= c->cfg.n_layers ||
+        pos0 < 0 || n < 0 || (n > 0 && (!k || !v)))
+        return SD_EINVAL;
+    User& u = c->users[user];
+    if (!u.active) return SD_EINVAL;
+    const int limit = to_pool ? u.prefix : (int)u.pages.size() * kPageTokens;
+    if (pos0 + n > limit) return SD_EINVAL;
+    if (n == 0) return SD_OK;
+    if (to_pool && u.pending_slot >= 0) return SD_ESTATE;
+    hipStream_t st = (hipStream_t)stream;
+    const int np = (int)u.pages.size();
+    std::memcpy(c->kvw_host, u.pages.data(), (size_t)np * 4);
+    int32_t* dev_pages = (int32_t*)(c->ws + c->lay.kvw_pages);
+    SD_HIP(hipMemcpyAsync(dev_pages, c->kvw_host, (size_t)np * 4, hipMemcpyHostToDevice, st));
+    launch_kv_copy(c->D, c->kv, dev_pages, layer, pos0, n, k, v, to_pool, st);
+    SD_HIP(hipGetLastError());
+    // the page list buffers are reused by the next call
+    SD_HIP(hipStreamSynchronize(st));
+    return SD_OK;
+}
+
+sd_status sd_kv_write(sd_ctx* c, int32_t user, int32_t layer, int32_t pos0, int32_t n,
+                      const void* k, const void* v, sd_stream stream) {
+    return kv_copy(c, user, layer, pos0, n, k, v, stream, 1);
+}
+
+sd_status sd_kv_read(sd_ctx* c, int32_t user, int32_t layer, int32_t pos0, int32_t n, void* k,
+                     void* v, sd_stream stream) {
+    return kv_copy(c, user, layer, pos0, n, k, v, stream, 0);
+}
+
+static sd_status submit(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t* assign,
+                        const int32_t* draft_len, const int32_t* draft_tokens, const float* q,
+                        const float* logits, int32_t mode, uint64_t seed, uint64_t round,
+                        const float* accept_u, sd_stream stream) {
+    if (!c) return SD_EINVAL;
+    if (mode != SD_GREEDY && mode != SD_STOCHASTIC && mode != SD_FORCE) return SD_EINVAL;
+    if (!draft_tokens || (mode == SD_STOCHASTIC && !q)) return SD_EINVAL;
+    const bool sample_only = logits != nullptr;
+    if (batch < 0) return SD_EINVAL;
+    Slot& s = c->slots[batch % c->cfg.max_pending];
+    if (s.pending) return SD_ESTATE;
+    std::vector<int> users, Ls;
+    int T = 0, nd = 0;
+    sd_status r = collect_batch(c, batch, n_users, assign, draft_len, !sample_only, users, Ls, T, nd);
+    if (r != SD_OK) return r;
+    if (!sample_only) {
+        // page reservation for i_m + l_m + 1 tokens per user, all or nothing
+        int need = 0;
+        for (size_t b = 0; b < users.size(); ++b) {
+            const User& u = c->users[users[b]];
+            need += std::max(0, pages_for(u.prefix + Ls[b] + 1) - (int)u.pages.size());
+        }
+        if (need > (int)c->free_pages.size()) return SD_ENOMEM;
+        for (size_t b = 0; b < users.size(); ++b) {
+            User& u = c->users[users[b]];
+            reserve_to(c, u, pages_for(u.prefix + Ls[b] + 1));
+        }
+    }
+    s.users = users;
+    s.L = Ls;
+    s.B = (int)users.size();
+    s.T = T;
+    s.nd = nd;
+    s.batch = batch;
+    s.sample_only = sample_only;
+    int n_items = 0, rows_max = 0;
+    build_stage(c, s, mode, !sample_only, &n_items, &rows_max);
+    BatchView bv = make_view(c, s);
+    bv.B = s.B;
+    bv.T = T;
+    bv.nd = nd;
+    bv.mode = mode;
+    bv.seed = seed;
+    bv.round = round;
+    bv.n_items = n_items;
+    bv.rows_max = rows_max;
+    bv.drafts = draft_tokens;
+    bv.q = q;
+    bv.accept_u = accept_u;
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e = hipMemcpyAsync(s.base + c->lay.stage, s.stage_host, c->lay.st_bytes,
+                                  hipMemcpyHostToDevice, st);
+    sd_status rs = hip_status(e);
+    if (rs == SD_OK) {
+        if (sample_only) {
+            launch_prepare(c->D, bv, s.bufs, st);
+            launch_sampler(c->D, bv, s.bufs, logits, st);
+            rs = hip_status(hipGetLastError());
+        } else {
+            rs = enqueue_forward(c, s, bv, st);
+            if (rs == SD_OK) {
+                launch_sampler(c->D, bv, s.bufs, s.bufs.logits, st);
+                rs = hip_status(hipGetLastError());
+            }
+        }
+    }
+    if (rs == SD_OK)
+        rs = hip_status(hipMemcpyAsync(s.result_host, s.bufs.result,
+                                       (size_t)(2 * c->lay.Bmax + 4) * 4, hipMemcpyDeviceToHost, st));
+    if (rs == SD_OK) rs = hip_status(hipEventRecord(s.done, st));
+    if (rs != SD_OK) {
+        if (!sample_only)
+            for (size_t b = 0; b < users.size(); ++b) {
+                User& u = c->users[users[b]];
+                release_to(c, u, pages_for(u.prefix));
+            }
+        return rs;
+    }
+    s.pending = true;
+    const int slot_index = (int)(&s - c->slots);
+    for (int m : users) c->users[m].pending_slot = slot_index;
+    return SD_OK;
+}
+
+sd_status sd_verify_batch(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t* assign,
+                          const int32_t* draft_len, const int32_t* draft_tokens, const float* q,
+                          int32_t mode, uint64_t seed, uint64_t round, const float* accept_u,
+                          sd_stream stream) {
+    return submit(c, batch, n_users, assign, draft_len, draft_tokens, q, nullptr, mode, seed, round,
+                  accept_u, stream);
+}
+
+sd_status sd_sample_logits(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t* assign,
+                           const int32_t* draft_len, const int32_t* draft_tokens, const float* q,
+                           const float* logits, int32_t mode, uint64_t seed, uint64_t round,
+                           const float* accept_u, sd_stream stream) {
+    if (!logits) return SD_EINVAL;
+    return submit(c, batch, n_users, assign, draft_len, draft_tokens, q, logits, mode, seed, round,
+                  accept_u, stream);
+}
+
+sd_status sd_accept(sd_ctx* c, int32_t batch, int32_t* n_accepted, int32_t* out_token,
+                    int32_t commit) {
+    if (!c || batch < 0 || !n_accepted || !out_token) return SD_EINVAL;
+    Slot& s = c->slots[batch % c->cfg.max_pending];
+    if (!s.pending || s.batch != batch) return SD_ESTATE;
+    if (hipEventSynchronize(s.done) != hipSuccess) return SD_EHIP;
+    const int Bmax = c->lay.Bmax;
+    const int flags = s.result_host[2 * Bmax];
+    const bool ok = flags == 0;
+    for (int b = 0; b < s.B; ++b) {
+        User& u = c->users[s.users[b]];
+        if (ok) {
+            n_accepted[s.users[b]] = s.result_host[b];
+            out_token[s.users[b]] = s.result_host[Bmax + b];
+        }
+        if (!s.sample_only) {
+            if (ok && commit) {
+                u.prefix += 1 + s.result_host[b];
+                u.root = s.result_host[Bmax + b];
+            }
+            release_to(c, u, pages_for(u.prefix));
+        }
+        u.pending_slot = -1;
+    }
+    s.pending = false;
+    return ok ? SD_OK : SD_EDEVICE;
+}
+
+sd_status sd_debug_logits(sd_ctx* c, int32_t batch, float* dst, sd_stream stream) {
+    if (!c || batch < 0 || !dst) return SD_EINVAL;
+    Slot& s = c->slots[batch % c->cfg.max_pending];
+    if (!s.pending || s.batch != batch || s.sample_only) return SD_ESTATE;
+    hipStream_t st = (hipStream_t)stream;
+    SD_HIP(hipStreamWaitEvent(st, s.done, 0));
+    SD_HIP(hipMemcpyAsync(dst, s.bufs.logits, (size_t)s.T * c->D.V * 4, hipMemcpyDeviceToDevice, st));
+    return SD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,124 @@
+// Internal interfaces between the host runtime and the gfx950 kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+namespace sdv {
+
+constexpr int kPageTokens = 16;   // tokens per KV page
+constexpr int kAttnChunk = 256;   // context tokens per attention work item
+constexpr int kVocabChunks = 16;  // vocab split of the sampler kernels
+constexpr int kMaxPending = 8;
+
+// Model dimensions as the kernels see them.
+struct Dims {
+    int L, d, hq, hkv, hd, F, V, qk_norm, bf16;
+    float rope_base, eps;
+    int nq() const { return hq * hd; }
+    int nkv() const { return hkv * hd; }
+    int nqkv() const { return (hq + 2 * hkv) * hd; }
+    int G() const { return hq / hkv; }
+};
+
+// Paged KV pool: [layer][page][K | V][kv_head] blocks; a K block is
+// [page_tokens][head_dim] (token-major), a V block is [head_dim][page_tokens]
+// (dim-major, so attention reads V^T fragments contiguously).
+struct KVPool {
+    void* base;
+    int n_pages;
+    int hkv, hd, esize;  // esize: bytes per element
+    __host__ __device__ size_t block_elems() const { return (size_t)kPageTokens * hd; }
+    __host__ __device__ size_t page_elems() const { return 2 * (size_t)hkv * block_elems(); }
+    __host__ __device__ size_t k_off(int layer, int page, int g) const {
+        return ((size_t)layer * n_pages + page) * page_elems() + (size_t)g * block_elems();
+    }
+    __host__ __device__ size_t v_off(int layer, int page, int g) const {
+        return k_off(layer, page, g) + (size_t)hkv * block_elems();
+    }
+};
+
+// Device view of one staged batch (all pointers into the workspace slot).
+struct BatchView {
+    int B, T, nd, mode;
+    uint64_t seed, round;
+    int max_pages;     // page-table row length
+    int n_items;       // attention work items
+    int rows_max;      // (max l_m + 1) * G, rows of an attention partial
+    const int32_t* user_id;    // [B] global user id
+    const int32_t* prefix;     // [B] i_m
+    const int32_t* L;          // [B] l_m
+    const int32_t* root;       // [B] root token
+    const int32_t* slot_off;   // [B+1]
+    const int32_t* draft_off;  // [B+1]
+    const int32_t* slot_b;     // [T] user index of slot
+    const int32_t* slot_j;     // [T] slot index within the user
+    const int32_t* page_table; // [B][max_pages]
+    const int4* items;         // [n_items] (b, g, c0, c1)
+    const int32_t* item_off;   // [B+1]
+    const int32_t* drafts;     // device input [nd]
+    const float* q;            // device input [nd][V]
+    const float* accept_u;     // device input [nd] or null
+    int32_t* flags;            // [1] device error bits, zeroed by the staging copy
+};
+
+// Workspace buffers of one batch slot.
+struct SlotBufs {
+    int32_t* tok;     // [Tmax]
+    float* cs;        // [Tmax][hd/2][2]
+    float* x;         // [Tmax][d]
+    void* h;          // [Tmax][d] normed GEMM input (act type)
+    void* ffn;        // [Tmax][F] SwiGLU output (act type)
+    float* qkv;       // [Tmax][nqkv]
+    void* qbuf;       // [Tmax][nq] act type
+    void* attn;       // [Tmax][nq] act type
+    float* apart;     // [max_items][rows_max][hd]
+    float* aml;       // [max_items][rows_max][2]
+    float* gpart;     // GEMM split-K partials
+    size_t gpart_floats;
+    int32_t* gcount;  // GEMM tile counters
+    int gcount_n;
+    float* logits;    // [Tmax][V]
+    float* sstat;     // [Tmax][4] per-slot max, sum, argmax, accept
+    float* spart;     // [Tmax * kVocabChunks][4] phase-A vocab-chunk partials
+    float* spartB;    // [Bmax * kVocabChunks][4] phase-B partials
+    int32_t* scount;  // [Tmax] phase-A arrival counters
+    int32_t* scountB; // [Bmax] phase-B arrival counters
+    int32_t* result;  // [2*Bmax + 4]: n_acc, token, flags
+    int bmax;
+};
+
+// ---- launchers (all enqueue on `s`, no synchronisation) ----
+void launch_prepare(const Dims& D, const BatchView& bv, const SlotBufs& sb, hipStream_t s);
+void launch_embed(const Dims& D, const BatchView& bv, const void* embed, const SlotBufs& sb,
+                  hipStream_t s);
+void launch_rmsnorm(const Dims& D, int T, const float* x, const void* gamma, void* out,
+                    hipStream_t s);
+void launch_qkrope(const Dims& D, const BatchView& bv, const SlotBufs& sb, const KVPool& kv,
+                   int layer, const void* qn, const void* kn, hipStream_t s);
+void launch_attention(const Dims& D, const BatchView& bv, const SlotBufs& sb, const KVPool& kv,
+                      int layer, hipStream_t s);
+
+enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+struct GemmCall {
+    const void* X;    // [T][K] act type
+    const void* W[3]; // weight segments, rows [out][K]
+    int seg[3];       // first virtual column of each segment (seg[0] = 0)
+    int nseg;
+    int N;            // output columns (real); SWIGLU: F, with W[0]=gate, W[1]=up
+    int K, T;
+    int epi;
+    void* out;        // EPI_STORE: float [T][ldo]; EPI_RESID: float x [T][ldo]; SWIGLU: act [T][ldo]
+    int ldo;
+};
+void launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_t s);
+size_t gemm_partial_floats(const Dims& D, int Tmax);
+int gemm_counter_count(const Dims& D);
+
+void launch_sampler(const Dims& D, const BatchView& bv, const SlotBufs& sb, const float* logits,
+                    hipStream_t s);
+
+void launch_kv_copy(const Dims& D, const KVPool& kv, const int32_t* pages_dev, int layer,
+                    int pos0, int n, const void* k, const void* v, int to_pool, hipStream_t s);
+
+}  // namespace sdv

@@ -1,0 +1,199 @@
+"""Python binding of libsdverify.so (the C ABI in include/sd_verify.h).
+
+Argument marshalling only: every step of the verify pass runs in the HIP
+kernels of the library.  torch tensors are accepted where the C ABI takes a
+device pointer; torch supplies device memory and streams, nothing else.  If
+the library has not been built, loading raises -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsdverify.so")
+
+SD_OK, SD_EINVAL, SD_ENOMEM, SD_EHIP, SD_ESTATE, SD_EDEVICE, SD_ENOTIMPL, SD_ENODEV = (
+    0, -1, -2, -3, -4, -5, -6, -7)
+SD_F32, SD_BF16 = 0, 1
+SD_GREEDY, SD_STOCHASTIC, SD_FORCE = 0, 1, 2
+MODES = {"greedy": SD_GREEDY, "stochastic": SD_STOCHASTIC, "force": SD_FORCE}
+
+EXPORTS = ("sd_verify_query_sizes", "sd_verify_init", "sd_verify_destroy", "sd_user_reset",
+           "sd_user_release", "sd_user_state", "sd_kv_write", "sd_kv_read", "sd_verify_batch",
+           "sd_accept", "sd_sample_logits", "sd_debug_logits", "sd_status_str")
+
+
+class sd_config(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "n_layers", "d_model", "n_q_heads", "n_kv_heads", "head_dim", "d_ffn", "vocab", "qk_norm",
+        "dtype", "page_tokens", "n_pages", "max_users", "max_draft", "max_batch_users",
+        "max_batch_tokens", "max_ctx", "max_pending")] + [("rope_base", ctypes.c_float),
+                                                          ("rms_eps", ctypes.c_float)]
+
+
+class sd_layer_weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in (
+        "wq", "wk", "wv", "wo", "wg", "wu", "wd", "norm1", "norm2", "qnorm", "knorm")]
+
+
+class sd_weights(ctypes.Structure):
+    _fields_ = [("embed", ctypes.c_void_p), ("lm_head", ctypes.c_void_p),
+                ("norm_f", ctypes.c_void_p), ("layers", ctypes.POINTER(sd_layer_weights))]
+
+
+class SdError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn}: {status_str(status)} ({status})")
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, u64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint64
+        P = ctypes.POINTER
+        L.sd_status_str.restype = ctypes.c_char_p
+        L.sd_status_str.argtypes = [i32]
+        L.sd_verify_query_sizes.argtypes = [P(sd_config), P(u64), P(u64)]
+        L.sd_verify_init.argtypes = [P(sd_config), P(sd_weights), vp, vp, P(vp)]
+        L.sd_verify_destroy.argtypes = [vp]
+        L.sd_user_reset.argtypes = [vp, i32, i32, i32]
+        L.sd_user_release.argtypes = [vp, i32]
+        L.sd_user_state.argtypes = [vp, i32, P(i32), P(i32)]
+        L.sd_kv_write.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp]
+        L.sd_kv_read.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp]
+        L.sd_verify_batch.argtypes = [vp, i32, i32, vp, vp, vp, vp, i32, u64, u64, vp, vp]
+        L.sd_accept.argtypes = [vp, i32, vp, vp, i32]
+        L.sd_sample_logits.argtypes = [vp, i32, i32, vp, vp, vp, vp, vp, i32, u64, u64, vp, vp]
+        L.sd_debug_logits.argtypes = [vp, i32, vp, vp]
+        for name in EXPORTS:
+            if name != "sd_status_str":
+                getattr(L, name).restype = i32
+        _lib = L
+    return _lib
+
+
+def status_str(s: int) -> str:
+    return lib().sd_status_str(int(s)).decode()
+
+
+def _check(fn: str, s: int) -> int:
+    if s != SD_OK:
+        raise SdError(fn, s)
+    return s
+
+
+def _dev(t) -> Optional[int]:
+    """Device pointer of a torch tensor (or an int / None)."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    assert t.is_cuda and t.is_contiguous(), "device arguments must be contiguous GPU tensors"
+    return t.data_ptr()
+
+
+def _host_i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _stream(s) -> Optional[int]:
+    if s is None:
+        return None
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+# ---------------------------------------------------------------------------
+# thin wrappers with the C names (raise SdError on a nonzero status)
+# ---------------------------------------------------------------------------
+
+def sd_verify_query_sizes(cfg: sd_config):
+    kv, ws = ctypes.c_uint64(), ctypes.c_uint64()
+    _check("sd_verify_query_sizes", lib().sd_verify_query_sizes(ctypes.byref(cfg), ctypes.byref(kv),
+                                                                ctypes.byref(ws)))
+    return kv.value, ws.value
+
+
+def sd_verify_init(cfg: sd_config, weights: sd_weights, kv_pool, workspace) -> int:
+    out = ctypes.c_void_p()
+    _check("sd_verify_init", lib().sd_verify_init(ctypes.byref(cfg), ctypes.byref(weights),
+                                                  _dev(kv_pool), _dev(workspace), ctypes.byref(out)))
+    return out.value
+
+
+def sd_verify_destroy(ctx: int) -> None:
+    _check("sd_verify_destroy", lib().sd_verify_destroy(ctx))
+
+
+def sd_user_reset(ctx: int, user: int, prefix_len: int, root_token: int) -> None:
+    _check("sd_user_reset", lib().sd_user_reset(ctx, user, prefix_len, root_token))
+
+
+def sd_user_release(ctx: int, user: int) -> None:
+    _check("sd_user_release", lib().sd_user_release(ctx, user))
+
+
+def sd_user_state(ctx: int, user: int):
+    p, r = ctypes.c_int32(), ctypes.c_int32()
+    _check("sd_user_state", lib().sd_user_state(ctx, user, ctypes.byref(p), ctypes.byref(r)))
+    return p.value, r.value
+
+
+def sd_kv_write(ctx: int, user: int, layer: int, pos0: int, n: int, k, v, stream=None) -> None:
+    _check("sd_kv_write", lib().sd_kv_write(ctx, user, layer, pos0, n, _dev(k), _dev(v), _stream(stream)))
+
+
+def sd_kv_read(ctx: int, user: int, layer: int, pos0: int, n: int, k, v, stream=None) -> None:
+    _check("sd_kv_read", lib().sd_kv_read(ctx, user, layer, pos0, n, _dev(k), _dev(v), _stream(stream)))
+
+
+def sd_verify_batch(ctx: int, batch: int, assign: Sequence[int], draft_len: Sequence[int],
+                    draft_tokens, q, mode, seed: int = 0, round_: int = 0, accept_u=None,
+                    stream=None) -> None:
+    a, L = _host_i32(assign), _host_i32(draft_len)
+    mode = MODES[mode] if isinstance(mode, str) else int(mode)
+    _check("sd_verify_batch", lib().sd_verify_batch(
+        ctx, batch, a.size, a.ctypes.data, L.ctypes.data, _dev(draft_tokens), _dev(q), mode,
+        int(seed), int(round_), _dev(accept_u), _stream(stream)))
+
+
+def sd_sample_logits(ctx: int, batch: int, assign, draft_len, draft_tokens, q, logits, mode,
+                     seed: int = 0, round_: int = 0, accept_u=None, stream=None) -> None:
+    a, L = _host_i32(assign), _host_i32(draft_len)
+    mode = MODES[mode] if isinstance(mode, str) else int(mode)
+    _check("sd_sample_logits", lib().sd_sample_logits(
+        ctx, batch, a.size, a.ctypes.data, L.ctypes.data, _dev(draft_tokens), _dev(q), _dev(logits),
+        mode, int(seed), int(round_), _dev(accept_u), _stream(stream)))
+
+
+def sd_accept(ctx: int, batch: int, n_users: int, commit: bool = False):
+    """Returns (n_accepted[M], out_token[M]); entries of users outside the
+    batch are -1."""
+    n_acc = np.full(n_users, -1, np.int32)
+    tok = np.full(n_users, -1, np.int32)
+    _check("sd_accept", lib().sd_accept(ctx, batch, n_acc.ctypes.data, tok.ctypes.data, int(commit)))
+    return n_acc, tok
+
+
+def sd_debug_logits(ctx: int, batch: int, dst, stream=None) -> None:
+    _check("sd_debug_logits", lib().sd_debug_logits(ctx, batch, _dev(dst), _stream(stream)))
+
+
+def make_config(n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, vocab, qk_norm, dtype,
+                n_pages, max_users, max_draft, max_batch_users, max_batch_tokens, max_ctx,
+                max_pending=2, rope_base=1e6, rms_eps=1e-6) -> sd_config:
+    return sd_config(n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, vocab, int(qk_norm),
+                     int(dtype), 16, n_pages, max_users, max_draft, max_batch_users, max_batch_tokens,
+                     max_ctx, max_pending, float(rope_base), float(rms_eps))

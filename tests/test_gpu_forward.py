@@ -1,0 +1,196 @@
+"""End-to-end parity of the GPU verify pass with the oracle on small models:
+logits within tolerance, decisions bit-exact outside the window that the
+logit tolerance admits, KV append and commit semantics."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workload as wl
+from gpu_harness import (compare_decisions, load_synthetic_kv, logit_rel_err, make_verifier,
+                         run_gpu, run_oracle)
+from workload.device import DeviceWeights, batch_to_device
+
+pytestmark = pytest.mark.gpu
+
+
+def _extra_window(err_abs_per_user):
+    # |d log(p/q)| <= 2 max|dz|, so p/q may move by a factor exp(2 eps)
+    return np.expm1(2.0 * np.asarray(err_abs_per_user))
+
+
+def _per_user_abs_err(gl, rl, n_slots):
+    out, o = [], 0
+    for n in n_slots:
+        out.append(float(np.max(np.abs(gl[o:o + n] - rl[o:o + n]))))
+        o += int(n)
+    return np.array(out)
+
+
+def _check(w, b, gpu, ref_logits, ref, tol, label):
+    err = logit_rel_err(gpu.logits, ref_logits)
+    print(f"{label}: logit rel err max {err.max():.3e} mean {err.mean():.3e}")
+    assert err.max() < tol, f"{label}: logit error {err.max()}"
+    extra = _extra_window(_per_user_abs_err(gpu.logits, ref_logits, b.n_slots))
+    bad, border = compare_decisions(gpu.n_acc, gpu.token, ref, b.draft_len, extra=extra)
+    print(f"{label}: decision mismatches {bad}, borderline {border}")
+    assert bad == 0
+
+
+@pytest.mark.parametrize("model", ["tiny", "tiny-qknorm"])
+def test_fp32_model_synthetic_kv(model):
+    w = wl.custom_workload(model, [64, 96, 112, 128, 0, 300], [1, 2, 3, 4, 2, 6], seed=31,
+                           accept_u_input=True)
+    dw = DeviceWeights(w.model, w.seed, gamma="uniform")
+    v = make_verifier(w, dw)
+    load_synthetic_kv(v, w)
+    b = w.batch(0)
+    ws = oracle.WeightSource(w.model, w.seed, "uniform")
+    for mode in ("stochastic", "greedy"):
+        gpu = run_gpu(v, w, 0, b, mode, seed=3, round_=1)
+        rl, ref = run_oracle(w, b, mode, seed=3, round_=1, weights=ws)
+        _check(w, b, gpu, rl, ref, 1e-4, f"{model}/{mode}")
+    v.close()
+
+
+@pytest.mark.parametrize("gamma", ["ones", "uniform"])
+def test_bf16_model_synthetic_kv(gamma):
+    # 8 query heads per KV head and 128-wide heads (the 32B head layout);
+    # prefixes span several attention chunks, include an empty prefix, and
+    # draft lengths give up to 104 query rows per KV head (two row passes)
+    w = wl.custom_workload("tiny-bf16", [40, 700, 0, 17, 1030, 255], [1, 7, 3, 12, 4, 2], seed=32,
+                           q_sigma=1.0)
+    dw = DeviceWeights(w.model, w.seed, gamma=gamma)
+    v = make_verifier(w, dw)
+    load_synthetic_kv(v, w)
+    b = w.batch(0)
+    ws = oracle.WeightSource(w.model, w.seed, gamma)
+    for mode in ("stochastic", "greedy", "force"):
+        gpu = run_gpu(v, w, 0, b, mode, seed=9, round_=2)
+        rl, ref = run_oracle(w, b, mode, seed=9, round_=2, weights=ws)
+        _check(w, b, gpu, rl, ref, 2e-2, f"tiny-bf16/{gamma}/{mode}")
+    v.close()
+
+
+def test_fp32_prefill_via_force_mode_matches_oracle_prefill():
+    """Build the cache on the GPU by teacher-forced verify calls with commit
+    (chunks of up to 16 tokens), then verify drafts on top; the oracle builds
+    its cache with one causal forward.  Logits and KV must agree."""
+    m = wl.MODELS["tiny-qknorm"]
+    w = wl.custom_workload("tiny-qknorm", [0, 0], [16, 16], seed=33)
+    dw = DeviceWeights(m, w.seed, gamma="uniform")
+    v = make_verifier(w, dw, extra_ctx=80)
+    rng = np.random.default_rng(7)
+    P = [45, 70]
+    toks = [rng.integers(0, m.vocab, size=P[u] + 1).astype(np.int32) for u in range(2)]
+    for u in range(2):
+        v.reset_user(u, 0, int(toks[u][0]))
+        pos, remaining = 0, P[u]
+        while remaining > 0:
+            c = min(17, remaining)  # slots in this call: root + c-1 drafts
+            if remaining - c == 1:
+                c -= 1
+            n = c - 1
+            assign = np.array([0 if i == u else -1 for i in range(2)], np.int32)
+            dl = np.array([n if i == u else 1 for i in range(2)], np.int32)
+            d = torch.from_numpy(toks[u][pos + 1:pos + 1 + n].copy()).cuda()
+            v.verify(0, assign, dl, d, None, "force")
+            acc, _ = v.accept(0, 2, commit=True)
+            assert acc[u] == n
+            pos += c
+            remaining -= c
+            assert v.user_state(u)[0] == pos
+            v.reset_user(u, pos, int(toks[u][pos]))  # teacher forcing: next prefix token
+    ws = oracle.WeightSource(m, w.seed, "uniform")
+    explicit = {u: oracle.prefill(m, ws, toks[u][:P[u]]) for u in range(2)}
+    # compare cached K/V
+    for u in range(2):
+        K, V = explicit[u]
+        for l in range(m.n_layers):
+            kd = torch.empty((P[u], m.n_kv_heads, m.head_dim), dtype=torch.float32, device="cuda")
+            vd = torch.empty_like(kd)
+            v.read_kv(u, l, 0, kd, vd)
+            ek = np.abs(kd.cpu().numpy().reshape(P[u], -1) - K[l]).max() / np.abs(K[l]).max()
+            ev = np.abs(vd.cpu().numpy().reshape(P[u], -1) - V[l]).max() / np.abs(V[l]).max()
+            assert ek < 1e-4 and ev < 1e-4, (u, l, ek, ev)
+    # verify drafts on top of the prefilled caches
+    w2 = wl.custom_workload("tiny-qknorm", P, [3, 5], seed=34)
+    b = w2.batch(0)
+    b.root[:] = [toks[0][P[0]], toks[1][P[1]]]
+    drafts, q, _ = batch_to_device(b)
+    v.verify(0, w2.assign, w2.draft_len, drafts, q, "stochastic", 5, 0)
+    gl = v.logits(0, b.T).cpu().numpy()
+    n_acc, tok = v.accept(0, 2)
+    kvs = oracle.KVSource(m, 0, [0, 1], P, explicit=explicit)
+    rl, ref = run_oracle(w2, b, "stochastic", 5, 0, kv=kvs, weights=ws)
+    err = logit_rel_err(gl, rl)
+    assert err.max() < 1e-4, err.max()
+    bad, _ = compare_decisions(n_acc, tok, ref, b.draft_len, extra=_extra_window(
+        _per_user_abs_err(gl, rl, b.n_slots)))
+    assert bad == 0
+    v.close()
+
+
+def test_commit_advances_users_and_rounds_compose():
+    """Two rounds with commit: round 2 of the GPU path equals the oracle's
+    round 2 computed on the oracle's own round-1 result."""
+    m = wl.MODELS["tiny"]
+    w = wl.custom_workload("tiny", [20, 33, 5], [3, 2, 4], seed=35)
+    dw = DeviceWeights(m, w.seed, gamma="uniform")
+    v = make_verifier(w, dw, extra_ctx=16)
+    load_synthetic_kv(v, w)
+    b = w.batch(0)
+    ws = oracle.WeightSource(m, w.seed, "uniform")
+    gpu = run_gpu(v, w, 0, b, "greedy", commit=True)
+    rl, ref = run_oracle(w, b, "greedy", weights=ws)
+    assert np.array_equal(gpu.n_acc, ref["n_acc"]) and np.array_equal(gpu.token, ref["token"])
+    for i, u in enumerate(b.users):
+        P, root = v.user_state(int(u))
+        assert P == b.prefix_len[i] + 1 + ref["n_acc"][i] and root == ref["token"][i]
+    # the oracle's cache after round 1: synthetic prefix + the committed slots
+    _, K1, V1 = oracle.forward(m, ws, oracle.KVSource(m, w.seed, b.users, b.prefix_len),
+                               b.prefix_len, b.n_slots, b.slot_tokens(), want_kv=True)
+    explicit = {}
+    off = 0
+    for i, u in enumerate(b.users):
+        P0 = int(b.prefix_len[i])
+        keep = 1 + int(ref["n_acc"][i])
+        Kp = np.zeros((m.n_layers, P0 + keep, m.n_kv_heads * m.head_dim), np.float32)
+        Vp = np.zeros_like(Kp)
+        for l in range(m.n_layers):
+            kk = np.empty((P0, m.n_kv_heads, m.head_dim), np.float32)
+            vv = np.empty_like(kk)
+            wl.fill_kv(m, w.seed, l, int(u), 0, kk)
+            wl.fill_kv(m, w.seed, l, int(u), 1, vv)
+            Kp[l, :P0] = kk.reshape(P0, -1)
+            Vp[l, :P0] = vv.reshape(P0, -1)
+            Kp[l, P0:] = K1[l, off:off + keep]
+            Vp[l, P0:] = V1[l, off:off + keep]
+        explicit[int(u)] = (Kp, Vp)
+        off += int(b.n_slots[i])
+    P2 = [int(b.prefix_len[i]) + 1 + int(ref["n_acc"][i]) for i in range(len(b.users))]
+    w2 = wl.custom_workload("tiny", P2, [2, 4, 1], seed=36)
+    b2 = w2.batch(0)
+    b2.root[:] = ref["token"]
+    drafts, q, _ = batch_to_device(b2)
+    v.verify(0, w2.assign, w2.draft_len, drafts, q, "greedy")
+    gl = v.logits(0, b2.T).cpu().numpy()
+    n2, t2 = v.accept(0, 3)
+    rl2, ref2 = run_oracle(w2, b2, "greedy", kv=oracle.KVSource(m, 0, b2.users, P2, explicit=explicit),
+                           weights=ws)
+    assert logit_rel_err(gl, rl2).max() < 1e-4
+    assert np.array_equal(n2, ref2["n_acc"]) and np.array_equal(t2, ref2["token"])
+    v.close()
+
+
+def test_determinism_two_runs_bit_identical():
+    w = wl.custom_workload("tiny-bf16", [300, 12, 77], [4, 9, 2], seed=37)
+    dw = DeviceWeights(w.model, w.seed)
+    v = make_verifier(w, dw)
+    load_synthetic_kv(v, w)
+    b = w.batch(0)
+    a = run_gpu(v, w, 0, b, "stochastic", seed=1)
+    c = run_gpu(v, w, 0, b, "stochastic", seed=1)
+    assert np.array_equal(a.logits, c.logits)
+    assert np.array_equal(a.n_acc, c.n_acc) and np.array_equal(a.token, c.token)
+    v.close()
