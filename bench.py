@@ -1,0 +1,273 @@
+#!/usr/bin/env python
+"""Throughput of the batched speculative-verify pass on one MI355X.
+
+One step = the whole verify pass (sd_verify_batch: embedding, 64 decoder
+layers, lm_head, accept/resample) plus sd_accept, for every batch of the
+workload, with all inputs resident in HBM.  Users are not committed between
+steps, so every step verifies the same batch.  Reported value: accepted
+tokens per second, sum over users of (a_m + 1) per step / seconds per step
+(the numerator of DiP-SD's throughput, eq. 2 and eq. 22).
+
+Prints one JSON line (rank 0, one GPU).  Inputs are seeded synthetic stand-ins:
+random-init Qwen3-shaped weights, synthetic cached KV, synthetic draft
+distributions; no trained weights or prompts are used.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, vendor figure
+BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, vendor figure
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="qwen3-32b-b16")
+    ap.add_argument("--mode", default="stochastic", choices=["stochastic", "greedy"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-layers", type=int, default=6,
+                    help="decoder layers the CPU-baseline sample runs (extrapolated to all)")
+    ap.add_argument("--breakdown", action="store_true", help="time every kernel class")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    import workload as wl
+    from workload.device import DeviceWeights, batch_to_device, kv_rows
+    from paper_2604_20919_amd import sdverify as sv
+    from paper_2604_20919_amd.verifier import Verifier
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    sv.lib()  # fails loudly if the HIP library is not built
+    torch.cuda.set_device(0)
+
+    w = wl.workload(args.workload)
+    m = w.model
+    t0 = time.time()
+    dw = DeviceWeights(m, w.seed)
+    log(f"weights {dw.nbytes() / 1e9:.1f} GB generated on GPU in {time.time() - t0:.1f}s")
+
+    names = {"wq": wl.W_Q, "wk": wl.W_K, "wv": wl.W_V, "wo": wl.W_O, "wg": wl.W_G, "wu": wl.W_U,
+             "wd": wl.W_D, "norm1": wl.N_1, "norm2": wl.N_2, "qnorm": wl.N_Q, "knorm": wl.N_K}
+    ptrs = {"embed": dw.ptr(wl.EMBED), "lm_head": dw.ptr(wl.LM_HEAD), "norm_f": dw.ptr(wl.NORM_F),
+            "layers": [{f: dw.ptr(k, l) for f, k in names.items()} for l in range(m.n_layers)]}
+    nb = w.n_batches
+    batches = [w.batch(n) for n in range(nb)]
+    max_ctx = int((w.prefix_len + w.draft_len).max()) + 1
+    pages = sum((int(p) + int(l) + 1 + 15) // 16 for p, l in zip(w.prefix_len, w.draft_len)) + 16
+    v = Verifier(m, ptrs, n_pages=pages, max_users=w.n_users, max_draft=int(w.draft_len.max()),
+                 max_batch_users=max(len(b.users) for b in batches),
+                 max_batch_tokens=max(b.T for b in batches), max_ctx=max_ctx,
+                 max_pending=min(nb, 8))
+    log(f"KV pool {v.kv_bytes / 1e9:.1f} GB, workspace {v.ws_bytes / 1e9:.2f} GB")
+
+    t0 = time.time()
+    dt = torch.int16 if m.dtype == "bf16" else torch.float32
+    pmax = int(w.prefix_len.max())
+    buf = (torch.empty((pmax, m.n_kv_heads, m.head_dim), dtype=dt, device="cuda"),
+           torch.empty((pmax, m.n_kv_heads, m.head_dim), dtype=dt, device="cuda"))
+    for b in batches:
+        for i, u in enumerate(b.users):
+            P = int(b.prefix_len[i])
+            v.reset_user(int(u), P, int(b.root[i]))
+            for l in range(m.n_layers):
+                k, vv = kv_rows(m, w.seed, l, int(u), P, out=buf)
+                v.write_kv(int(u), l, 0, k, vv)
+    torch.cuda.synchronize()
+    del buf
+    kv_tokens = int(w.prefix_len.sum())
+    log(f"cached KV of {kv_tokens} tokens written in {time.time() - t0:.1f}s")
+
+    dev_in = [batch_to_device(b) for b in batches]
+    if args.mode == "greedy":
+        plant_greedy_drafts(v, w, batches, dev_in, torch)
+    streams = [torch.cuda.Stream() for _ in range(min(nb, 2))]
+
+    def step():
+        for n in range(nb):
+            d, q, au = dev_in[n]
+            v.verify(n, w.assign, w.draft_len, d, q, args.mode, seed=w.seed, round_=0,
+                     accept_u=au, stream=streams[n % len(streams)])
+        acc = 0
+        for n in range(nb):
+            n_acc, _ = v.accept(n, w.n_users)
+            acc += int((n_acc[batches[n].users] + 1).sum())
+        return acc
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    accepted = 0
+    for _ in range(args.steps):
+        accepted += step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_step = 1e3 * elapsed / args.steps
+    acc_step = accepted / args.steps
+    verified_step = sum(b.T for b in batches)
+    value = acc_step / (ms_step / 1e3)
+    log(f"{ms_step:.3f} ms/step, {acc_step:.1f} accepted / {verified_step} verified tokens per step")
+
+    # ---- roofline of the dominant kernel (gate/up GEMM + SwiGLU), timed live ----
+    T = batches[0].T
+    per_layer_w = 2 * m.d_ffn * m.d_model * 2
+    gu_bytes = per_layer_w + T * m.d_model * 2 + T * m.d_ffn * 2
+    prof_steps = max(3, args.steps // 2)
+    sv.sd_profile_begin(v.ctx, sv.SD_K_GATEUP, prof_steps * nb * m.n_layers + 8)
+    for _ in range(prof_steps):
+        step()
+    gu_ms, gu_n = sv.sd_profile_end(v.ctx)
+    gu_avg_s = gu_ms / 1e3 / max(gu_n, 1)
+    achieved = gu_bytes / gu_avg_s / 1e9
+    roofline = {"bound": "hbm", "kernel": "k_gemm_bf16 (gate/up + SwiGLU epilogue)",
+                "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "bytes_per_launch": gu_bytes, "avg_launch_us": round(gu_avg_s * 1e6, 2),
+                "launches": gu_n}
+
+    breakdown = None
+    if args.breakdown:
+        breakdown = {}
+        for name, k in (("qkv", sv.SD_K_QKV), ("attention", sv.SD_K_ATTN), ("o_proj", sv.SD_K_O),
+                        ("gate_up", sv.SD_K_GATEUP), ("down", sv.SD_K_DOWN), ("lm_head", sv.SD_K_LMHEAD),
+                        ("sampler", sv.SD_K_SAMPLER), ("small", sv.SD_K_SMALL)):
+            sv.sd_profile_begin(v.ctx, k, 3 * nb * (4 * m.n_layers + 8))
+            for _ in range(3):
+                step()
+            ms, n = sv.sd_profile_end(v.ctx)
+            breakdown[name] = round(ms / 3, 4)
+        log(f"per-step ms by kernel class: {breakdown}")
+
+    # algorithmic bytes of one step: weights once per batch, each user's KV
+    # once, logits and q rows once
+    wbytes = (m.n_layers * m.layer_params() + 2 * m.vocab * m.d_model) * m.wbytes
+    wbytes -= m.vocab * m.d_model * m.wbytes  # embedding: only T rows are read
+    kv_read = sum(int(p + l + 1) for p, l in zip(w.prefix_len, w.draft_len)) * m.kv_bytes_per_token()
+    step_bytes = nb * wbytes + kv_read
+    result = {
+        "metric": "accepted tokens/s, Qwen3-32B-shaped batch verify; MFMA util + HBM GB/s",
+        "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": m.dtype,
+        "data": "synthetic (random-init weights N(0,0.02), synthetic KV N(0,1), synthetic draft q)",
+        "config": {"workload": args.workload, "model": m.name, "mode": args.mode,
+                   "users": int(w.n_users), "batches": nb, "verified_tokens_per_step": verified_step,
+                   "prefix_tokens": kv_tokens},
+        "verified_tokens_per_s": round(verified_step / (ms_step / 1e3), 1),
+        "accepted_per_step": acc_step,
+        "step_hbm_floor_ms": round(step_bytes / (HBM_PEAK_GBS * 1e9) * 1e3, 3),
+        "step_algorithmic_gb": round(step_bytes / 1e9, 2),
+        "step_effective_gbs": round(step_bytes / (ms_step / 1e3) / 1e9, 1),
+        "roofline": roofline,
+    }
+    if breakdown is not None:
+        result["breakdown_ms"] = breakdown
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, batches[0], args.cpu_layers, acc_step / verified_step)
+    v.close()
+    print(json.dumps(result), flush=True)
+
+
+def plant_greedy_drafts(v, w, batches, dev_in, torch):
+    """Greedy workload: user m's first k_m drafts follow the target's own
+    argmax continuation (k_m uniform in 0..l_m, seeded), then one random
+    token; found with l_max teacher-forced passes on the GPU."""
+    import workload as wl
+    for n, b in enumerate(batches):
+        d, q, au = dev_in[n]
+        k = wl._ints(len(b.users), w.seed, wl.S_LEN << 8, 0, int(b.draft_len.max()))
+        k = np.minimum(k, b.draft_len)
+        drafts = b.drafts.copy()
+        for j in range(int(b.draft_len.max())):
+            d.copy_(torch.from_numpy(drafts))
+            v.verify(n, w.assign, w.draft_len, d, q, "force")
+            lg = v.logits(n, b.T)
+            v.accept(n, w.n_users)
+            am = lg.argmax(dim=1).cpu().numpy()
+            so, do = 0, 0
+            for i, L in enumerate(b.draft_len):
+                if j < L and j < k[i]:
+                    drafts[do + j] = am[so + j]
+                so += int(L) + 1
+                do += int(L)
+        d.copy_(torch.from_numpy(drafts))
+        b.drafts = drafts
+
+
+def cpu_baseline(w, b, n_layers_sample, acc_per_verified):
+    """The oracle on the host cores: one user of the batch through
+    n_layers_sample decoder layers, plus lm_head and the sampler, timed with
+    weight generation excluded; per-user time extrapolated to all layers."""
+    import oracle
+    import workload as wl
+    m = w.model
+    threads = int(os.environ.get("OMP_NUM_THREADS") or os.cpu_count() or 1)
+    i = 0
+    u = int(b.users[i])
+    sub = [b.draft_len[:i].sum(), b.draft_len[:i + 1].sum()]
+    ws = oracle.WeightSource(m, w.seed)
+    layers = {l: ws.layer(l) for l in range(n_layers_sample)}
+
+    class Cached(oracle.WeightSource):
+        def __init__(self):
+            self.m, self.seed, self.gamma, self._glob = m, w.seed, "ones", ws._glob
+
+        def layer(self, l):
+            return layers[l]
+
+    import dataclasses
+    ms = dataclasses.replace(m, n_layers=n_layers_sample)
+    kv = oracle.KVSource(ms, w.seed, [u], [int(b.prefix_len[i])])
+    toks = b.slot_tokens()[int(b.n_slots[:i].sum()):int(b.n_slots[:i + 1].sum())]
+    t0 = time.perf_counter()
+    logits = oracle.forward(ms, Cached(), kv, [int(b.prefix_len[i])], [int(b.n_slots[i])], toks)
+    t_fwd = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.sample("stochastic", [u], [int(b.draft_len[i])], logits, b.drafts[sub[0]:sub[1]],
+                  b.q[sub[0]:sub[1]], None, w.seed, 0)
+    t_samp = time.perf_counter() - t0
+    # split the measured forward into per-layer and lm_head parts: time the
+    # lm_head alone with a zero-layer model
+    m0 = dataclasses.replace(m, n_layers=0)
+    t0 = time.perf_counter()
+    oracle.forward(m0, Cached(), oracle.KVSource(m0, w.seed, [u], [int(b.prefix_len[i])]),
+                   [int(b.prefix_len[i])], [int(b.n_slots[i])], toks)
+    t_head = time.perf_counter() - t0
+    t_layer = max(t_fwd - t_head, 0.0) / n_layers_sample
+    per_user = t_layer * m.n_layers + t_head + t_samp
+    slots = int(b.n_slots[i])
+    cpu_tok_s = slots * acc_per_verified / per_user
+    return {"value": round(cpu_tok_s, 4), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": (f"user {u} of the batch ({slots} query slots, prefix {int(b.prefix_len[i])}): "
+                       f"{n_layers_sample} of {m.n_layers} decoder layers timed ({t_layer:.2f} s/layer), "
+                       f"lm_head {t_head:.2f} s and sampler {t_samp:.2f} s timed, extrapolated to "
+                       f"{per_user:.1f} s per user; accepted = verified x {acc_per_verified:.3f} "
+                       f"(the GPU run's ratio); weight generation excluded")}
+
+
+if __name__ == "__main__":
+    main()

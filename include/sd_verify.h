@@ -222,6 +222,28 @@ sd_status sd_sample_logits(sd_ctx* ctx, int32_t batch, int32_t n_users, const in
  * `stream`.  SD_ESTATE if the batch is not pending. */
 sd_status sd_debug_logits(sd_ctx* ctx, int32_t batch, float* dst, sd_stream stream);
 
+/* Kernel classes for sd_profile_begin. */
+enum {
+    SD_K_QKV = 1,      /* QKV projection GEMM */
+    SD_K_ATTN = 2,     /* paged attention + chunk combine */
+    SD_K_O = 3,        /* output projection GEMM + residual */
+    SD_K_GATEUP = 4,   /* gate/up GEMM + SwiGLU */
+    SD_K_DOWN = 5,     /* down projection GEMM + residual */
+    SD_K_LMHEAD = 6,   /* final norm + lm_head GEMM */
+    SD_K_SAMPLER = 7,  /* accept/resample kernels */
+    SD_K_SMALL = 8     /* embedding, RMSNorm, QK-norm/RoPE/KV append */
+};
+
+/* Diagnostic timing: until sd_profile_end, every sd_verify_batch records a
+ * pair of HIP events around each launch of kernel class `kclass`, on the
+ * stream the kernels run on (up to max_launches pairs; later launches are
+ * not timed).  Host-side event creation happens here, not per batch. */
+sd_status sd_profile_begin(sd_ctx* ctx, int32_t kclass, int32_t max_launches);
+
+/* Wait for the recorded launches and return their summed duration in
+ * milliseconds and their count; stops profiling.  SD_ESTATE if not active. */
+sd_status sd_profile_end(sd_ctx* ctx, double* total_ms, int32_t* launches);
+
 /* Static description of a status code. */
 const char* sd_status_str(sd_status s);
 

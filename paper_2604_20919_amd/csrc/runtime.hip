@@ -186,6 +186,10 @@ struct sd_ctx {
     Slot slots[kMaxPending];
     int32_t* kvw_host = nullptr;  // pinned page list for kv copies
     int device = 0;
+    // diagnostic timing of one kernel class
+    int prof_class = 0;
+    int prof_used = 0;
+    std::vector<hipEvent_t> prof_ev;  // pairs (start, end)
 };
 
 namespace {
@@ -324,15 +328,38 @@ void build_stage(sd_ctx* c, Slot& s, int mode, bool with_items, int* n_items, in
     *rows_max = (maxL + 1) * c->D.G();
 }
 
+// Records a start event before a launch group of class k and an end event
+// after it when that class is being profiled.
+struct ProfScope {
+    sd_ctx* c;
+    hipStream_t st;
+    int idx = -1;
+    ProfScope(sd_ctx* c_, int k, hipStream_t s) : c(c_), st(s) {
+        if (c->prof_class == k && 2 * (c->prof_used + 1) <= (int)c->prof_ev.size()) {
+            idx = c->prof_used++;
+            (void)hipEventRecord(c->prof_ev[2 * idx], st);
+        }
+    }
+    ~ProfScope() {
+        if (idx >= 0) (void)hipEventRecord(c->prof_ev[2 * idx + 1], st);
+    }
+};
+
 sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t st) {
     const Dims& D = c->D;
     const SlotBufs& sb = s.bufs;
-    launch_prepare(D, bv, sb, st);
-    launch_embed(D, bv, c->w.embed, sb, st);
+    {
+        ProfScope ps(c, SD_K_SMALL, st);
+        launch_prepare(D, bv, sb, st);
+        launch_embed(D, bv, c->w.embed, sb, st);
+    }
     const int T = bv.T;
     for (int l = 0; l < D.L; ++l) {
         const sd_layer_weights& w = c->layers[l];
-        launch_rmsnorm(D, T, sb.x, w.norm1, sb.h, st);
+        {
+            ProfScope ps(c, SD_K_SMALL, st);
+            launch_rmsnorm(D, T, sb.x, w.norm1, sb.h, st);
+        }
         GemmCall g{};
         g.X = sb.h;
         g.W[0] = w.wq; g.W[1] = w.wk; g.W[2] = w.wv;
@@ -344,9 +371,18 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
         g.epi = EPI_STORE;
         g.out = sb.qkv;
         g.ldo = D.nqkv();
-        launch_gemm(D, g, sb, st);
-        launch_qkrope(D, bv, sb, c->kv, l, w.qnorm, w.knorm, st);
-        launch_attention(D, bv, sb, c->kv, l, st);
+        {
+            ProfScope ps(c, SD_K_QKV, st);
+            launch_gemm(D, g, sb, st);
+        }
+        {
+            ProfScope ps(c, SD_K_SMALL, st);
+            launch_qkrope(D, bv, sb, c->kv, l, w.qnorm, w.knorm, st);
+        }
+        {
+            ProfScope ps(c, SD_K_ATTN, st);
+            launch_attention(D, bv, sb, c->kv, l, st);
+        }
         GemmCall o{};
         o.X = sb.attn;
         o.W[0] = w.wo;
@@ -357,8 +393,14 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
         o.epi = EPI_RESID;
         o.out = sb.x;
         o.ldo = D.d;
-        launch_gemm(D, o, sb, st);
-        launch_rmsnorm(D, T, sb.x, w.norm2, sb.h, st);
+        {
+            ProfScope ps(c, SD_K_O, st);
+            launch_gemm(D, o, sb, st);
+        }
+        {
+            ProfScope ps(c, SD_K_SMALL, st);
+            launch_rmsnorm(D, T, sb.x, w.norm2, sb.h, st);
+        }
         GemmCall gu{};
         gu.X = sb.h;
         gu.W[0] = w.wg; gu.W[1] = w.wu;
@@ -370,7 +412,10 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
         gu.epi = EPI_SWIGLU;
         gu.out = sb.ffn;
         gu.ldo = D.F;
-        launch_gemm(D, gu, sb, st);
+        {
+            ProfScope ps(c, SD_K_GATEUP, st);
+            launch_gemm(D, gu, sb, st);
+        }
         GemmCall dn{};
         dn.X = sb.ffn;
         dn.W[0] = w.wd;
@@ -381,8 +426,12 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
         dn.epi = EPI_RESID;
         dn.out = sb.x;
         dn.ldo = D.d;
-        launch_gemm(D, dn, sb, st);
+        {
+            ProfScope ps(c, SD_K_DOWN, st);
+            launch_gemm(D, dn, sb, st);
+        }
     }
+    ProfScope ps_lm(c, SD_K_LMHEAD, st);
     launch_rmsnorm(D, T, sb.x, c->w.norm_f, sb.h, st);
     GemmCall lm{};
     lm.X = sb.h;
@@ -530,6 +579,7 @@ sd_status sd_verify_destroy(sd_ctx* c) {
         if (s.result_host) (void)hipHostFree(s.result_host);
     }
     if (c->kvw_host) (void)hipHostFree(c->kvw_host);
+    for (hipEvent_t e : c->prof_ev) (void)hipEventDestroy(e);
     delete c;
     return SD_OK;
 }
@@ -666,6 +716,7 @@ static sd_status submit(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t
         } else {
             rs = enqueue_forward(c, s, bv, st);
             if (rs == SD_OK) {
+                ProfScope ps(c, SD_K_SAMPLER, st);
                 launch_sampler(c->D, bv, s.bufs, s.bufs.logits, st);
                 rs = hip_status(hipGetLastError());
             }
@@ -741,6 +792,37 @@ sd_status sd_debug_logits(sd_ctx* c, int32_t batch, float* dst, sd_stream stream
     hipStream_t st = (hipStream_t)stream;
     SD_HIP(hipStreamWaitEvent(st, s.done, 0));
     SD_HIP(hipMemcpyAsync(dst, s.bufs.logits, (size_t)s.T * c->D.V * 4, hipMemcpyDeviceToDevice, st));
+    return SD_OK;
+}
+
+sd_status sd_profile_begin(sd_ctx* c, int32_t kclass, int32_t max_launches) {
+    if (!c || kclass < SD_K_QKV || kclass > SD_K_SMALL || max_launches < 1 || max_launches > 65536)
+        return SD_EINVAL;
+    if (c->prof_class) return SD_ESTATE;
+    while ((int)c->prof_ev.size() < 2 * max_launches) {
+        hipEvent_t e;
+        SD_HIP(hipEventCreate(&e));
+        c->prof_ev.push_back(e);
+    }
+    c->prof_used = 0;
+    c->prof_class = kclass;
+    return SD_OK;
+}
+
+sd_status sd_profile_end(sd_ctx* c, double* total_ms, int32_t* launches) {
+    if (!c || !total_ms || !launches) return SD_EINVAL;
+    if (!c->prof_class) return SD_ESTATE;
+    double tot = 0.0;
+    for (int i = 0; i < c->prof_used; ++i) {
+        SD_HIP(hipEventSynchronize(c->prof_ev[2 * i + 1]));
+        float ms = 0.f;
+        SD_HIP(hipEventElapsedTime(&ms, c->prof_ev[2 * i], c->prof_ev[2 * i + 1]));
+        tot += ms;
+    }
+    *total_ms = tot;
+    *launches = c->prof_used;
+    c->prof_class = 0;
+    c->prof_used = 0;
     return SD_OK;
 }
 

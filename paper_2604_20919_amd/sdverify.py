@@ -24,7 +24,9 @@ MODES = {"greedy": SD_GREEDY, "stochastic": SD_STOCHASTIC, "force": SD_FORCE}
 
 EXPORTS = ("sd_verify_query_sizes", "sd_verify_init", "sd_verify_destroy", "sd_user_reset",
            "sd_user_release", "sd_user_state", "sd_kv_write", "sd_kv_read", "sd_verify_batch",
-           "sd_accept", "sd_sample_logits", "sd_debug_logits", "sd_status_str")
+           "sd_accept", "sd_sample_logits", "sd_debug_logits", "sd_profile_begin", "sd_profile_end",
+           "sd_status_str")
+SD_K_QKV, SD_K_ATTN, SD_K_O, SD_K_GATEUP, SD_K_DOWN, SD_K_LMHEAD, SD_K_SAMPLER, SD_K_SMALL = range(1, 9)
 
 
 class sd_config(ctypes.Structure):
@@ -76,6 +78,8 @@ def lib() -> ctypes.CDLL:
         L.sd_accept.argtypes = [vp, i32, vp, vp, i32]
         L.sd_sample_logits.argtypes = [vp, i32, i32, vp, vp, vp, vp, vp, i32, u64, u64, vp, vp]
         L.sd_debug_logits.argtypes = [vp, i32, vp, vp]
+        L.sd_profile_begin.argtypes = [vp, i32, i32]
+        L.sd_profile_end.argtypes = [vp, P(ctypes.c_double), P(i32)]
         for name in EXPORTS:
             if name != "sd_status_str":
                 getattr(L, name).restype = i32
@@ -189,6 +193,17 @@ def sd_accept(ctx: int, batch: int, n_users: int, commit: bool = False):
 
 def sd_debug_logits(ctx: int, batch: int, dst, stream=None) -> None:
     _check("sd_debug_logits", lib().sd_debug_logits(ctx, batch, _dev(dst), _stream(stream)))
+
+
+def sd_profile_begin(ctx: int, kclass: int, max_launches: int = 4096) -> None:
+    _check("sd_profile_begin", lib().sd_profile_begin(ctx, kclass, max_launches))
+
+
+def sd_profile_end(ctx: int):
+    """Returns (total_ms, launches) of the profiled kernel class."""
+    ms, n = ctypes.c_double(), ctypes.c_int32()
+    _check("sd_profile_end", lib().sd_profile_end(ctx, ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
 
 
 def make_config(n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, vocab, qk_norm, dtype,

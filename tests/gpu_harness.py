@@ -37,12 +37,17 @@ def make_verifier(w: wl.Workload, dw: DeviceWeights, max_pending: int = 2, extra
 def load_synthetic_kv(v: Verifier, w: wl.Workload, users=None):
     m = w.model
     users = range(w.n_users) if users is None else users
+    pmax = max([int(w.prefix_len[u]) for u in users] + [1])
+    dt = torch.float32 if m.dtype == "f32" else torch.int16
+    buf = (torch.empty((pmax, m.n_kv_heads, m.head_dim), dtype=dt, device="cuda"),
+           torch.empty((pmax, m.n_kv_heads, m.head_dim), dtype=dt, device="cuda"))
     for u in users:
         P = int(w.prefix_len[u])
         v.reset_user(u, P, 0)
         for l in range(m.n_layers):
-            k, vv = kv_rows(m, w.seed, l, u, P)
-            v.write_kv(u, l, 0, k, vv)
+            if P:
+                k, vv = kv_rows(m, w.seed, l, u, P, out=buf)
+                v.write_kv(u, l, 0, k, vv)
     torch.cuda.synchronize()
 
 

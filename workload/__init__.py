@@ -28,10 +28,41 @@ def build(force: bool = True) -> str:
     """Compile gen.c into libworkload.so (plain gcc, OpenMP)."""
     if force or not os.path.exists(_SO):
         tmp = _SO + ".tmp"
-        subprocess.check_call(["gcc", "-O3", "-fopenmp", "-fPIC", "-shared", "-o", tmp,
-                               os.path.join(_HERE, "gen.c"), "-lm"])
+        subprocess.check_call(["gcc", "-O3", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared",
+                               "-o", tmp, os.path.join(_HERE, "gen.c"), "-lm"])
         os.replace(tmp, _SO)
     return _SO
+
+
+_GPU_SO = os.path.join(_HERE, "libworkload_gpu.so")
+
+
+def build_gpu(force: bool = True) -> str:
+    """Compile the bit-identical GPU fill kernels (gen_gpu.hip) for gfx950."""
+    if force or not os.path.exists(_GPU_SO):
+        tmp = _GPU_SO + ".tmp"
+        subprocess.check_call(["hipcc", "--offload-arch=gfx950", "-O3", "-fPIC", "-shared",
+                               "-ffp-contract=off", "-Xclang", "-target-feature", "-Xclang",
+                               "-packed-fp32-ops", "-o", tmp, os.path.join(_HERE, "gen_gpu.hip")],
+                              stderr=subprocess.DEVNULL)
+        os.replace(tmp, _GPU_SO)
+    return _GPU_SO
+
+
+_glib = None
+
+
+def glib():
+    global _glib
+    if _glib is None:
+        if not os.path.exists(_GPU_SO):
+            raise RuntimeError(f"{_GPU_SO} is not built; run __graft_entry__.build()")
+        L = ctypes.CDLL(_GPU_SO)
+        i64, u64, f32, vp, i32 = ctypes.c_int64, ctypes.c_uint64, ctypes.c_float, ctypes.c_void_p, ctypes.c_int
+        L.wlg_fill_normal.argtypes = [vp, i64, u64, u64, i64, f32, i32, vp]
+        L.wlg_fill_uniform.argtypes = [vp, i64, u64, u64, i64, f32, f32, i32, vp]
+        _glib = L
+    return _glib
 
 
 _lib = None

@@ -1,7 +1,8 @@
 """Device copies of the seeded synthetic inputs (weights, cached KV, batch
-inputs) as torch tensors.  Values come from the generator in gen.c, so the
-GPU path sees exactly what the oracle sees.  torch is used for device memory
-only."""
+inputs) as torch tensors.  Weights and cached keys/values are written on the
+GPU by the fill kernels of gen_gpu.hip, which produce the same bits as the
+host generator in gen.c (pinned by a GPU test), so the GPU path sees exactly
+what the oracle sees.  torch is used for device memory only."""
 from __future__ import annotations
 
 import numpy as np
@@ -11,6 +12,7 @@ import workload as wl
 
 LAYER_KINDS = (wl.W_Q, wl.W_K, wl.W_V, wl.W_O, wl.W_G, wl.W_U, wl.W_D,
                wl.N_1, wl.N_2, wl.N_Q, wl.N_K)
+NORM_KINDS = (wl.N_1, wl.N_2, wl.N_Q, wl.N_K, wl.NORM_F)
 
 
 def _tdtype(m: wl.ModelShape):
@@ -18,10 +20,37 @@ def _tdtype(m: wl.ModelShape):
     return torch.float32 if m.dtype == "f32" else torch.int16
 
 
-def _to_dev(a: np.ndarray, dev) -> torch.Tensor:
-    if a.dtype == np.uint16:
-        a = a.view(np.int16)
-    return torch.from_numpy(a).to(dev)
+def _stream_ptr():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def gpu_fill_normal(out: torch.Tensor, seed: int, stream: int, offset: int, std: float):
+    bf16 = out.dtype == torch.int16
+    rc = wl.glib().wlg_fill_normal(out.data_ptr(), out.numel(), seed, stream, offset, std, int(bf16),
+                                   _stream_ptr())
+    if rc != 0:
+        raise RuntimeError("GPU generator launch failed")
+
+
+def gpu_fill_uniform(out: torch.Tensor, seed: int, stream: int, offset: int, lo: float, hi: float):
+    bf16 = out.dtype == torch.int16
+    rc = wl.glib().wlg_fill_uniform(out.data_ptr(), out.numel(), seed, stream, offset, lo, hi,
+                                    int(bf16), _stream_ptr())
+    if rc != 0:
+        raise RuntimeError("GPU generator launch failed")
+
+
+def fill_weight_gpu(m: wl.ModelShape, seed: int, layer: int, kind: int, out: torch.Tensor,
+                    gamma: str = "ones"):
+    """GPU twin of workload.fill_weight."""
+    s = wl._wstream(layer, kind)
+    if kind in NORM_KINDS:
+        if gamma == "ones":
+            out.fill_(0x3F80 if out.dtype == torch.int16 else 1.0)
+        else:
+            gpu_fill_uniform(out, seed, s, 0, 0.5, 1.5)
+    else:
+        gpu_fill_normal(out, seed, s, 0, wl.WEIGHT_STD)
 
 
 class DeviceWeights:
@@ -31,24 +60,27 @@ class DeviceWeights:
     def __init__(self, m: wl.ModelShape, seed: int, gamma: str = "ones", device="cuda"):
         self.m = m
         dt = _tdtype(m)
-        self.glob = {k: _to_dev(wl.new_weight(m, seed, -1, k, gamma), device)
-                     for k in (wl.EMBED, wl.LM_HEAD, wl.NORM_F)}
+        self.glob = {}
+        for k in (wl.EMBED, wl.LM_HEAD, wl.NORM_F):
+            t = torch.empty(wl.weight_shape(m, k), dtype=dt, device=device)
+            fill_weight_gpu(m, seed, -1, k, t, gamma)
+            self.glob[k] = t
         self.layer = {}
         for k in LAYER_KINDS:
-            shape = wl.weight_shape(m, k)
-            self.layer[k] = torch.empty((m.n_layers,) + shape, dtype=dt, device=device)
-        np_dt = np.float32 if m.dtype == "f32" else np.uint16
-        for l in range(m.n_layers):
-            for k in LAYER_KINDS:
-                host = np.empty(wl.weight_shape(m, k), dtype=np_dt)
-                wl.fill_weight(m, seed, l, k, host, gamma)
-                self.layer[k][l].copy_(torch.from_numpy(host.view(np.int16) if np_dt == np.uint16 else host))
+            t = torch.empty((m.n_layers,) + wl.weight_shape(m, k), dtype=dt, device=device)
+            for l in range(m.n_layers):
+                fill_weight_gpu(m, seed, l, k, t[l], gamma)
+            self.layer[k] = t
+        torch.cuda.synchronize()
 
     def ptr(self, kind: int, layer: int = -1) -> int:
         if layer < 0:
             return self.glob[kind].data_ptr()
         t = self.layer[kind]
         return t.data_ptr() + layer * t[0].numel() * t.element_size()
+
+    def nbytes(self) -> int:
+        return sum(t.numel() * t.element_size() for t in list(self.glob.values()) + list(self.layer.values()))
 
 
 def batch_to_device(b: wl.Batch, device="cuda"):
@@ -59,13 +91,15 @@ def batch_to_device(b: wl.Batch, device="cuda"):
     return drafts, q, au
 
 
-def kv_rows(m: wl.ModelShape, seed: int, layer: int, user: int, n: int, device="cuda"):
+def kv_rows(m: wl.ModelShape, seed: int, layer: int, user: int, n: int, device="cuda", out=None):
     """Synthetic cached K and V of positions 0..n-1 as device tensors
-    [n][hkv][hd] in the model dtype."""
-    np_dt = np.float32 if m.dtype == "f32" else np.uint16
+    [n][hkv][hd] in the model dtype (GPU twin of workload.fill_kv)."""
     shape = (n, m.n_kv_heads, m.head_dim)
-    k = np.empty(shape, np_dt)
-    v = np.empty(shape, np_dt)
-    wl.fill_kv(m, seed, layer, user, 0, k)
-    wl.fill_kv(m, seed, layer, user, 1, v)
-    return _to_dev(k, device), _to_dev(v, device)
+    if out is None:
+        k = torch.empty(shape, dtype=_tdtype(m), device=device)
+        v = torch.empty(shape, dtype=_tdtype(m), device=device)
+    else:
+        k, v = out[0][:n], out[1][:n]
+    gpu_fill_normal(k, seed, wl._kvstream(layer, user, 0), 0, wl.KV_STD)
+    gpu_fill_normal(v, seed, wl._kvstream(layer, user, 1), 0, wl.KV_STD)
+    return k, v
