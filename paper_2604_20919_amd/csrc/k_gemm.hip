@@ -6,19 +6,22 @@
 //   * weights are read in place, row-major [out][in]; each lane loads 16
 //     contiguous bytes (8 bf16 along k) straight into the A operand of
 //     v_mfma_f32_16x16x32_bf16 (16 weight rows x 32 k);
-//   * the activation chunk X[0:T][k0:k0+KC] is staged once per workgroup in
-//     LDS and read by the 4 waves as the B operand (32 k x 16 slots);
+//   * the activation chunk X[0:T][k0:k0+KC] is staged in LDS (double
+//     buffered) and read by the 4 waves of the workgroup as the B operand
+//     (32 k x 16 slots);
+//   * software pipeline per chunk: the loads of X(c+1) are issued before the
+//     weight loads of chunk c+1, so storing X(c+1) to LDS after computing
+//     chunk c waits for X only and the weight prefetch stays in flight;
 //   * each wave owns NSUB groups of 16 weight rows and all T slots, so every
-//     weight byte is read exactly once per call;
-//   * the k range is split over S workgroups when there are too few column
-//     tiles to fill the GPU; partial sums go to a workspace and the last
-//     workgroup of a tile (atomic arrival counter) adds them in split order,
-//     so results are bit-identical from run to run;
-//   * the epilogue is fused: plain fp32 store, residual add into the fp32
-//     stream, or SwiGLU silu(g) * u with gate/up rows interleaved per wave.
+//     weight byte is read once per call;
+//   * when there are too few column tiles to fill the GPU the k range is
+//     split over S workgroups; partial sums are written to a workspace and a
+//     second kernel adds them in split order and applies the epilogue (no
+//     device-wide fences, deterministic results);
+//   * epilogues: fp32 store, residual add into the fp32 stream, or SwiGLU
+//     silu(g) * u with gate/up rows interleaved per wave.
 // An fp32 fallback (plain FMA loop) serves the fp32 model configuration.
-#include <map>
-#include <tuple>
+#include <algorithm>
 
 #include "sdv_device.h"
 #include "sdv_internal.h"
@@ -30,45 +33,85 @@ struct GemmP {
     const bf16_t* W0;
     const bf16_t* W1;
     const bf16_t* W2;
+    int rows0, rows1, rows2;  // weight rows of each segment (buffer ranges)
     int seg1, seg2;  // first virtual column of segments 1 and 2
     int K, T, S, kchunks, tiles;
-    float* part;
-    int32_t* cnt;
+    float* part;     // [S][T][vcols] when S > 1
+    int vcols;
     void* out;
     int ldo;
 };
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + expf(-g)); }
 
-template <int MT, int NSUB, int KC, int EPI>
-__global__ __launch_bounds__(256) void k_gemm_bf16(GemmP p) {
+template <int EPI>
+__device__ __forceinline__ void epi_store4(const GemmP& p, int t, int col, f32x4 v) {
+    float* o = (float*)p.out + (size_t)t * p.ldo + col;
+    if (EPI == EPI_RESID) {
+        f32x4 x = *(f32x4*)o;
+        x += v;
+        *(f32x4*)o = x;
+    } else {
+        *(f32x4*)o = v;
+    }
+}
+
+__device__ __forceinline__ void swiglu_store4(const GemmP& p, int t, int col, f32x4 g, f32x4 u) {
+    bf16_t* o = (bf16_t*)p.out + (size_t)t * p.ldo + col;
+    uint2 pk;
+    pk.x = (uint32_t)f32_to_bf16(silu(g[0]) * u[0]) | ((uint32_t)f32_to_bf16(silu(g[1]) * u[1]) << 16);
+    pk.y = (uint32_t)f32_to_bf16(silu(g[2]) * u[2]) | ((uint32_t)f32_to_bf16(silu(g[3]) * u[3]) << 16);
+    *(uint2*)o = pk;
+}
+
+template <int MT, int NSUB, int KC, int EPI, bool SPLIT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2)))
+void k_gemm_bf16(GemmP p) {
     constexpr int NT = 4 * NSUB * 16;  // virtual columns per tile
     constexpr int KS = KC / 32;        // MFMA k-steps per chunk
     constexpr int LDX = KC + 8;        // padded LDS row (bf16 elements)
-    __shared__ __attribute__((aligned(16))) bf16_t xs[MT * 16 * LDX];
-    __shared__ int last_flag;
+    constexpr int PPR = KC / 8;        // 16-byte pieces per staged row
+    constexpr int XPT = (MT * 16 * PPR) / 256;  // X pieces per thread
+    static_assert((MT * 16 * PPR) % 256 == 0, "X chunk must split evenly over 256 threads");
+    static_assert(EPI != EPI_SWIGLU || NSUB % 2 == 0, "SwiGLU pairs gate/up sub-tiles");
+    __shared__ __attribute__((aligned(16))) bf16_t xs[2][MT * 16 * LDX];
 
-    const int tile = blockIdx.x / p.S, split = blockIdx.x % p.S;
+    const int tile = SPLIT ? blockIdx.x / p.S : blockIdx.x;
+    const int split = SPLIT ? blockIdx.x % p.S : 0;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int lr = lane & 15, lg = lane >> 4;
     const int mt_act = (p.T + 15) >> 4;
 
-    // weight row of this lane for each sub-tile
-    const bf16_t* wrow[NSUB];
+    // Buffer resources: the weight segment of each sub-tile is uniform over
+    // the wave (segment boundaries are multiples of 16 rows), so every load
+    // is a uniform resource + a fixed 32-bit per-lane offset + a uniform
+    // chunk offset.  Out-of-range reads return zero.
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    __amdgpu_buffer_rsrc_t wres[NSUB];
+    uint32_t woff[NSUB];
 #pragma unroll
     for (int s = 0; s < NSUB; ++s) {
+        const bf16_t* base;
+        int rows, row;
         if (EPI == EPI_SWIGLU) {
-            const int col = tile * (NT / 2) + (wave * (NSUB / 2) + s / 2) * 16 + lr;
-            wrow[s] = ((s & 1) ? p.W1 : p.W0) + (size_t)col * p.K;
+            const int col = tile * (NT / 2) + (wv * (NSUB / 2) + s / 2) * 16;
+            base = (s & 1) ? p.W1 : p.W0;
+            rows = (s & 1) ? p.rows1 : p.rows0;
+            row = col;
         } else {
-            const int v = tile * NT + (wave * NSUB + s) * 16 + lr;
-            const bf16_t* w = v < p.seg1 ? p.W0 + (size_t)v * p.K
-                              : v < p.seg2 ? p.W1 + (size_t)(v - p.seg1) * p.K
-                                           : p.W2 + (size_t)(v - p.seg2) * p.K;
-            wrow[s] = w;
+            const int v = tile * NT + (wv * NSUB + s) * 16;
+            if (v < p.seg1) { base = p.W0; rows = p.rows0; row = v; }
+            else if (v < p.seg2) { base = p.W1; rows = p.rows1; row = v - p.seg1; }
+            else { base = p.W2; rows = p.rows2; row = v - p.seg2; }
         }
-        wrow[s] += 8 * lg;
+        const uint64_t bytes = (uint64_t)rows * (uint64_t)p.K * 2u;
+        wres[s] = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0,
+                                                    (int)(bytes > 0x7fffffffu ? 0x7fffffffu : bytes),
+                                                    0x00020000);
+        woff[s] = ((uint32_t)(row + lr) * (uint32_t)p.K + 8u * lg) * 2u;
     }
+    const __amdgpu_buffer_rsrc_t xres =
+        __builtin_amdgcn_make_buffer_rsrc((void*)p.X, (short)0, p.T * p.K * 2, 0x00020000);
 
     f32x4 acc[NSUB][MT];
 #pragma unroll
@@ -79,119 +122,141 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(GemmP p) {
     const int c_begin = split * p.kchunks / p.S;
     const int c_end = (split + 1) * p.kchunks / p.S;
 
-    bf16x8 wcur[KS][NSUB], wnxt[KS][NSUB];
+    // Ping-pong pipeline: while chunk c is multiplied out of (LDS buffer
+    // c&1, weight registers A or B), X(c+1) and W(c+1) are requested into the
+    // other set.  The loop is unrolled by two so the two register sets swap
+    // roles statically, and scheduling barriers keep the order issue loads ->
+    // multiply -> store X(c+1) to LDS.  X rows >= T are read as row T-1: they
+    // only feed output slots >= T, which are never stored.
+    uint4 xr[XPT];
+    bf16x8 wa[KS][NSUB], wb[KS][NSUB];
+    uint32_t xoff[XPT];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
+    for (int i = 0; i < XPT; ++i) {
+        const int idx = threadIdx.x + i * 256;
+        const int r = min(idx / PPR, p.T - 1), cc = idx % PPR;
+        xoff[i] = ((uint32_t)r * (uint32_t)p.K + (uint32_t)cc * 8u) * 2u;
+    }
+    auto load_x = [&](int c) {
+        const int so = c * KC * 2;
 #pragma unroll
-        for (int s = 0; s < NSUB; ++s)
-            wcur[ks][s] = *(const bf16x8*)(wrow[s] + (size_t)c_begin * KC + ks * 32);
-
-    constexpr int PIECES = MT * 16 * (KC / 8);
-    for (int c = c_begin; c < c_end; ++c) {
-        if (c + 1 < c_end) {
+        for (int i = 0; i < XPT; ++i)
+            xr[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xres, xoff[i], so, 0));
+    };
+    auto store_x = [&](int buf) {
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-                for (int s = 0; s < NSUB; ++s)
-                    wnxt[ks][s] = *(const bf16x8*)(wrow[s] + (size_t)(c + 1) * KC + ks * 32);
+        for (int i = 0; i < XPT; ++i) {
+            const int idx = threadIdx.x + i * 256;
+            *(uint4*)(&xs[buf][(idx / PPR) * LDX + (idx % PPR) * 8]) = xr[i];
         }
-        // stage X[0:16*mt_act][c*KC : (c+1)*KC] (rows >= T are zero)
-        for (int i = threadIdx.x; i < mt_act * 16 * (KC / 8); i += 256) {
-            const int r = i / (KC / 8), cc = i % (KC / 8);
-            uint4 v = {0u, 0u, 0u, 0u};
-            if (r < p.T) v = *(const uint4*)(p.X + (size_t)r * p.K + (size_t)c * KC + cc * 8);
-            *(uint4*)(xs + r * LDX + cc * 8) = v;
-        }
-        (void)PIECES;
-        __syncthreads();
+    };
+    auto load_w = [&](bf16x8 (&w)[KS][NSUB], int c) {
+        const int so = c * KC * 2;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+            for (int s = 0; s < NSUB; ++s)
+                w[ks][s] = __builtin_bit_cast(
+                    bf16x8, __builtin_amdgcn_raw_buffer_load_b128(wres[s], woff[s] + ks * 64, so, 0));
+    };
+    auto compute = [&](int buf, const bf16x8 (&w)[KS][NSUB]) {
+        const bf16_t* xb = xs[buf];
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
             for (int m = 0; m < MT; ++m) {
                 if (m < mt_act) {
-                    const bf16x8 xf = *(const bf16x8*)(xs + (m * 16 + lr) * LDX + ks * 32 + 8 * lg);
+                    const bf16x8 xf = *(const bf16x8*)(xb + (m * 16 + lr) * LDX + ks * 32 + 8 * lg);
 #pragma unroll
                     for (int s = 0; s < NSUB; ++s)
-                        acc[s][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wcur[ks][s], xf,
-                                                                             acc[s][m], 0, 0, 0);
+                        acc[s][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[ks][s], xf, acc[s][m],
+                                                                             0, 0, 0);
                 }
             }
         }
+    };
+
+    load_x(c_begin);
+    load_w(wa, c_begin);
+    store_x(0);
+    __syncthreads();
+    // The prefetch is unconditional (the chunk index is clamped, so the last
+    // step re-reads the current chunk from cache): conditional loads would
+    // make the compiler's wait-count analysis merge states pessimistically
+    // and wait for the prefetch inside the multiply.
+    const int c_last = c_end - 1;
+    for (int c = c_begin; c < c_end; c += 2) {
+        // even step: compute c from (LDS 0, wa), prefetch c+1 into (xr, wb)
+        load_x(min(c + 1, c_last));
+        load_w(wb, min(c + 1, c_last));
+        __builtin_amdgcn_sched_barrier(0);
+        compute(0, wa);
+        __builtin_amdgcn_sched_barrier(0);
+        store_x(1);
         __syncthreads();
-        if (c + 1 < c_end) {
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-                for (int s = 0; s < NSUB; ++s) wcur[ks][s] = wnxt[ks][s];
-        }
+        if (c + 1 >= c_end) break;
+        // odd step: compute c+1 from (LDS 1, wb), prefetch c+2 into (xr, wa)
+        load_x(min(c + 2, c_last));
+        load_w(wa, min(c + 2, c_last));
+        __builtin_amdgcn_sched_barrier(0);
+        compute(1, wb);
+        __builtin_amdgcn_sched_barrier(0);
+        store_x(0);
+        __syncthreads();
     }
 
     // lane holds D[n = 4*lg + r][t = lr] of each (sub-tile, slot tile)
-    if (p.S > 1) {
-#pragma unroll
-        for (int s = 0; s < NSUB; ++s)
-#pragma unroll
-            for (int m = 0; m < MT; ++m) {
-                const int t = m * 16 + lr;
-                if (m < mt_act && t < p.T) {
-                    float* dst = p.part + ((size_t)(tile * p.S + split) * p.T + t) * NT +
-                                 (wave * NSUB + s) * 16 + 4 * lg;
-                    *(f32x4*)dst = acc[s][m];
-                }
-            }
-        __threadfence();
-        __syncthreads();
-        if (threadIdx.x == 0) last_flag = (atomicAdd(p.cnt + tile, 1) == p.S - 1);
-        __syncthreads();
-        if (!last_flag) return;
-        __threadfence();
-#pragma unroll
-        for (int s = 0; s < NSUB; ++s)
-#pragma unroll
-            for (int m = 0; m < MT; ++m) {
-                const int t = m * 16 + lr;
-                if (m < mt_act && t < p.T) {
-                    f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
-                    for (int sp = 0; sp < p.S; ++sp)
-                        sum += *(const f32x4*)(p.part + ((size_t)(tile * p.S + sp) * p.T + t) * NT +
-                                               (wave * NSUB + s) * 16 + 4 * lg);
-                    acc[s][m] = sum;
-                }
-            }
-        if (threadIdx.x == 0) p.cnt[tile] = 0;
-    }
-
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
         const int t = m * 16 + lr;
         if (!(m < mt_act && t < p.T)) continue;
-        if (EPI == EPI_SWIGLU) {
-#pragma unroll
-            for (int s = 0; s < NSUB; s += 2) {
-                const int col = tile * (NT / 2) + (wave * (NSUB / 2) + s / 2) * 16 + 4 * lg;
-                bf16_t* o = (bf16_t*)p.out + (size_t)t * p.ldo + col;
-                const f32x4 g = acc[s][m], u = acc[s + 1][m];
-                uint2 pk;
-                pk.x = (uint32_t)f32_to_bf16(silu(g[0]) * u[0]) |
-                       ((uint32_t)f32_to_bf16(silu(g[1]) * u[1]) << 16);
-                pk.y = (uint32_t)f32_to_bf16(silu(g[2]) * u[2]) |
-                       ((uint32_t)f32_to_bf16(silu(g[3]) * u[3]) << 16);
-                *(uint2*)o = pk;
-            }
-        } else {
+        if (SPLIT) {
 #pragma unroll
             for (int s = 0; s < NSUB; ++s) {
-                const int col = tile * NT + (wave * NSUB + s) * 16 + 4 * lg;
-                float* o = (float*)p.out + (size_t)t * p.ldo + col;
-                if (EPI == EPI_RESID) {
-                    f32x4 v = *(f32x4*)o;
-                    v += acc[s][m];
-                    *(f32x4*)o = v;
-                } else {
-                    *(f32x4*)o = acc[s][m];
-                }
+                const int v = tile * NT + (wave * NSUB + s) * 16 + 4 * lg;
+                *(f32x4*)(p.part + ((size_t)split * p.T + t) * p.vcols + v) = acc[s][m];
             }
+        } else if (EPI == EPI_SWIGLU) {
+#pragma unroll
+            for (int s = 0; s < NSUB; s += 2)
+                swiglu_store4(p, t, tile * (NT / 2) + (wave * (NSUB / 2) + s / 2) * 16 + 4 * lg,
+                              acc[s][m], acc[s + 1][m]);
+        } else {
+#pragma unroll
+            for (int s = 0; s < NSUB; ++s)
+                epi_store4<EPI>(p, t, tile * NT + (wave * NSUB + s) * 16 + 4 * lg, acc[s][m]);
         }
+    }
+}
+
+// Sum of the S split-K partials (in split order) plus the epilogue; one
+// thread per 4 output columns of one slot.
+template <int EPI>
+__global__ __launch_bounds__(256) void k_splitk_reduce(GemmP p, int nsub) {
+    const int ncols = EPI == EPI_SWIGLU ? p.vcols / 2 : p.vcols;
+    const int per_row = ncols / 4;
+    const int idx = blockIdx.x * 256 + threadIdx.x;
+    if (idx >= p.T * per_row) return;
+    const int t = idx / per_row, c = (idx % per_row) * 4;
+    const size_t stride = (size_t)p.T * p.vcols;
+    const float* base = p.part + (size_t)t * p.vcols;
+    if (EPI == EPI_SWIGLU) {
+        // real column c -> virtual gate / up columns of its tile
+        const int nt = 64 * nsub, half = nt / 2;
+        const int tile = c / half, rem = c % half;
+        const int pair = rem / 16, lr = rem % 16;
+        const int wave = pair / (nsub / 2), sp = pair % (nsub / 2);
+        const int vg = tile * nt + (wave * nsub + 2 * sp) * 16 + lr;
+        f32x4 g = f32x4{0.f, 0.f, 0.f, 0.f}, u = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int s = 0; s < p.S; ++s) {
+            g += *(const f32x4*)(base + s * stride + vg);
+            u += *(const f32x4*)(base + s * stride + vg + 16);
+        }
+        swiglu_store4(p, t, c, g, u);
+    } else {
+        f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int s = 0; s < p.S; ++s) v += *(const f32x4*)(base + s * stride + c);
+        epi_store4<EPI>(p, t, c, v);
     }
 }
 
@@ -238,82 +303,102 @@ __global__ void k_gemm_f32(GemmF p) {
 // ---------------------------------------------------------------------------
 // host-side configuration
 // ---------------------------------------------------------------------------
-namespace {
 
-constexpr int kNSub = 2;
-constexpr int kNT = 4 * kNSub * 16;
+// Tile shape per slot-count class: MT slot tiles of 16, NSUB weight
+// sub-tiles of 16 rows per wave, KC k elements per pipeline chunk.
+struct GemmShape { int MT, NSUB, KC; };
 
-struct Shape { int MT, KC; };
-
-Shape shape_for(int T) {
+static GemmShape shape_for(int T, int epi) {
     const int mt = (T + 15) / 16;
-    static const int classes[] = {2, 4, 6, 8, 12, 16, 20, 26};
-    for (int c : classes)
-        if (mt <= c) return {c, c <= 8 ? 256 : (c <= 16 ? 128 : 64)};
-    return {0, 0};
+    const int n1 = epi == EPI_SWIGLU ? 2 : 1;  // SwiGLU pairs gate/up sub-tiles
+    if (mt <= 2) return {2, n1, 256};
+    if (mt <= 4) return {4, n1, 256};
+    if (mt <= 6) return {6, 2, 128};
+    if (mt <= 8) return {8, 2, 128};
+    if (mt <= 12) return {12, 2, 64};
+    if (mt <= 16) return {16, 2, 64};
+    if (mt <= 20) return {20, 2, 64};
+    if (mt <= 26) return {26, 2, 64};
+    return {0, 0, 0};
 }
 
 typedef void (*GemmFn)(GemmP);
+typedef void (*ReduceFn)(GemmP, int);
 
-template <int MT, int KC>
-GemmFn pick_epi(int epi) {
+template <int MT, int NSUB, int KC, bool SPLIT>
+static GemmFn pick_epi(int epi) {
     switch (epi) {
-        case EPI_RESID: return k_gemm_bf16<MT, kNSub, KC, EPI_RESID>;
-        case EPI_SWIGLU: return k_gemm_bf16<MT, kNSub, KC, EPI_SWIGLU>;
-        default: return k_gemm_bf16<MT, kNSub, KC, EPI_STORE>;
+        case EPI_RESID: return k_gemm_bf16<MT, NSUB, KC, EPI_RESID, SPLIT>;
+        case EPI_SWIGLU:
+            if constexpr (NSUB % 2 == 0) return k_gemm_bf16<MT, NSUB, KC, EPI_SWIGLU, SPLIT>;
+            return nullptr;
+        default: return k_gemm_bf16<MT, NSUB, KC, EPI_STORE, SPLIT>;
     }
 }
 
-GemmFn pick(const Shape& sh, int epi) {
+template <bool SPLIT>
+static GemmFn pick(const GemmShape& sh, int epi) {
+    if (epi == EPI_SWIGLU && sh.MT <= 4)
+        return sh.MT == 2 ? k_gemm_bf16<2, 2, 256, EPI_SWIGLU, SPLIT>
+                          : k_gemm_bf16<4, 2, 256, EPI_SWIGLU, SPLIT>;
     switch (sh.MT) {
-        case 2: return pick_epi<2, 256>(epi);
-        case 4: return pick_epi<4, 256>(epi);
-        case 6: return pick_epi<6, 256>(epi);
-        case 8: return pick_epi<8, 256>(epi);
-        case 12: return pick_epi<12, 128>(epi);
-        case 16: return pick_epi<16, 128>(epi);
-        case 20: return pick_epi<20, 64>(epi);
-        case 26: return pick_epi<26, 64>(epi);
+        case 2: return pick_epi<2, 1, 256, SPLIT>(epi == EPI_SWIGLU ? EPI_STORE : epi);
+        case 4: return pick_epi<4, 1, 256, SPLIT>(epi == EPI_SWIGLU ? EPI_STORE : epi);
+        case 6: return pick_epi<6, 2, 128, SPLIT>(epi);
+        case 8: return pick_epi<8, 2, 128, SPLIT>(epi);
+        case 12: return pick_epi<12, 2, 64, SPLIT>(epi);
+        case 16: return pick_epi<16, 2, 64, SPLIT>(epi);
+        case 20: return pick_epi<20, 2, 64, SPLIT>(epi);
+        case 26: return pick_epi<26, 2, 64, SPLIT>(epi);
     }
     return nullptr;
 }
 
-int resident_blocks(GemmFn fn) {
-    static std::map<GemmFn, int> cache;
-    auto it = cache.find(fn);
-    if (it != cache.end()) return it->second;
-    int per_cu = 1, cus = 256, dev = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)fn, 256, 0) != hipSuccess ||
-        per_cu < 1)
-        per_cu = 1;
-    if (hipGetDevice(&dev) == hipSuccess)
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    const int n = per_cu * cus;
-    cache[fn] = n;
+static ReduceFn pick_reduce(int epi) {
+    switch (epi) {
+        case EPI_RESID: return k_splitk_reduce<EPI_RESID>;
+        case EPI_SWIGLU: return k_splitk_reduce<EPI_SWIGLU>;
+        default: return k_splitk_reduce<EPI_STORE>;
+    }
+}
+
+static int cu_count() {
+    static int n = 0;
+    if (n == 0) {
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
+            n = 256;
+    }
     return n;
 }
 
-// number of k splits: the largest divisor of kchunks that keeps every
-// workgroup resident at once (so all of them stream weights concurrently)
-int choose_splits(int tiles, int kchunks, int capacity) {
-    int best = 1;
-    for (int s = 1; s <= kchunks; ++s)
-        if (kchunks % s == 0 && (long)tiles * s <= capacity) best = s;
-    return best;
+// k splits: the smallest divisor of kchunks that gives at least one
+// workgroup per CU (more splits only add partial traffic)
+static int choose_splits(int tiles, int kchunks) {
+    const int target = cu_count();
+    if (tiles >= target) return 1;
+    for (int s = 2; s <= kchunks; ++s)
+        if (kchunks % s == 0 && tiles * s >= target) return s;
+    return kchunks;
 }
-
-}  // namespace
 
 size_t gemm_partial_floats(const Dims& D, int Tmax) {
     if (!D.bf16) return 0;
-    // worst case: every call uses at most 32 splits of the widest non-SwiGLU output
-    const int nmax = D.nqkv() > D.d ? D.nqkv() : D.d;
-    return (size_t)32 * Tmax * nmax;
+    // the split count is bounded by the CU count over the tile count, so
+    // S * vcols <= ~2 * (CUs * NT) for every call; reserve generously
+    const size_t widest = (size_t)std::max(std::max(D.nqkv(), D.d), 2 * D.F);
+    return (size_t)Tmax * std::max<size_t>(widest * 2, (size_t)65536);
 }
 
-int gemm_counter_count(const Dims& D) {
-    const int v = 2 * D.F > D.nqkv() ? 2 * D.F : D.nqkv();
-    return (v > D.V ? v : D.V) / 16 + 64;
+int gemm_counter_count(const Dims&) { return 1; }
+
+bool gemm_shape_ok(const Dims& D, int T, int K, int N, int epi) {
+    if (!D.bf16) return true;
+    const GemmShape sh = shape_for(T, epi);
+    if (sh.MT == 0) return false;
+    const int vcols = epi == EPI_SWIGLU ? 2 * N : N;
+    return K % sh.KC == 0 && vcols % (64 * sh.NSUB) == 0;
 }
 
 void launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_t s) {
@@ -335,9 +420,8 @@ void launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream
         hipLaunchKernelGGL(k_gemm_f32, dim3((n + 255) / 256), dim3(256), 0, s, p);
         return;
     }
-    const Shape sh = shape_for(g.T);
-    GemmFn fn = pick(sh, g.epi);
-    const int vcols = g.epi == EPI_SWIGLU ? 2 * g.N : g.N;
+    const GemmShape sh = shape_for(g.T, g.epi);
+    const int nt = 64 * sh.NSUB;
     GemmP p;
     p.X = (const bf16_t*)g.X;
     p.W0 = (const bf16_t*)g.W[0];
@@ -345,33 +429,36 @@ void launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream
     p.W2 = (const bf16_t*)(g.nseg > 2 ? g.W[2] : g.W[0]);
     p.seg1 = g.nseg > 1 ? g.seg[1] : (1 << 30);
     p.seg2 = g.nseg > 2 ? g.seg[2] : (1 << 30);
+    if (g.epi == EPI_SWIGLU) {
+        p.rows0 = p.rows1 = p.rows2 = g.N;
+    } else {
+        p.rows0 = g.nseg > 1 ? g.seg[1] : g.N;
+        p.rows1 = g.nseg > 2 ? g.seg[2] - g.seg[1] : (g.nseg > 1 ? g.N - g.seg[1] : 0);
+        p.rows2 = g.nseg > 2 ? g.N - g.seg[2] : 0;
+    }
     p.K = g.K;
     p.T = g.T;
     p.kchunks = g.K / sh.KC;
-    p.tiles = vcols / kNT;
-    int S = 1;
-    if (g.epi != EPI_SWIGLU || true) S = choose_splits(p.tiles, p.kchunks, resident_blocks(fn));
-    // the partial buffer bounds the split count
-    while (S > 1 && (size_t)S * g.T * (size_t)p.tiles * kNT > sb.gpart_floats) {
+    p.vcols = g.epi == EPI_SWIGLU ? 2 * g.N : g.N;
+    p.tiles = p.vcols / nt;
+    int S = choose_splits(p.tiles, p.kchunks);
+    while (S > 1 && (size_t)S * g.T * p.vcols > sb.gpart_floats) {
         int t = S - 1;
         while (t > 1 && p.kchunks % t) --t;
         S = t;
     }
     p.S = S;
     p.part = sb.gpart;
-    p.cnt = sb.gcount;
     p.out = g.out;
     p.ldo = g.ldo;
-    hipLaunchKernelGGL(fn, dim3(p.tiles * S), dim3(256), 0, s, p);
-}
-
-// shape checks used by the runtime before anything is enqueued
-bool gemm_shape_ok(const Dims& D, int T, int K, int N, int epi) {
-    if (!D.bf16) return true;
-    const Shape sh = shape_for(T);
-    if (sh.MT == 0) return false;
-    const int vcols = epi == EPI_SWIGLU ? 2 * N : N;
-    return K % sh.KC == 0 && vcols % kNT == 0;
+    if (S == 1) {
+        hipLaunchKernelGGL(pick<false>(sh, g.epi), dim3(p.tiles), dim3(256), 0, s, p);
+    } else {
+        hipLaunchKernelGGL(pick<true>(sh, g.epi), dim3(p.tiles * S), dim3(256), 0, s, p);
+        const int ncols = g.epi == EPI_SWIGLU ? p.vcols / 2 : p.vcols;
+        const int n = g.T * (ncols / 4);
+        hipLaunchKernelGGL(pick_reduce(g.epi), dim3((n + 255) / 256), dim3(256), 0, s, p, sh.NSUB);
+    }
 }
 
 }  // namespace sdv
