@@ -114,19 +114,27 @@ typedef struct sd_ctx sd_ctx;
  *   every layer and KV head (K and V), in dtype.
  * workspace_bytes: activations, logits and per-batch staging for max_pending
  *   batches of up to max_batch_tokens slots.
+ * weight_pack_bytes: the library's copy of the projection matrices and the
+ *   lm_head in its streaming layout (SD_BF16; 0 for SD_F32).
  * Returns SD_EINVAL if cfg is inconsistent. Host-only; needs no device. */
 sd_status sd_verify_query_sizes(const sd_config* cfg, uint64_t* kv_pool_bytes,
-                                uint64_t* workspace_bytes);
+                                uint64_t* workspace_bytes, uint64_t* weight_pack_bytes);
 
 /* Create a context on the current HIP device.
- * w: weights as above (device pointers, kept until destroy).
- * kv_pool / workspace: device buffers of at least the queried sizes, 256-byte
- *   aligned, owned by the caller, kept until destroy.  The workspace is
- *   initialised here (stream-ordered on the null stream, then synchronised).
+ * w: weights as above (device pointers).  With SD_BF16 the projection
+ *   matrices (wq, wk, wv, wo, wg, wu, wd) and lm_head are copied here into
+ *   weight_pack in the order the GEMM kernels stream them (16-row x 32-column
+ *   fragments, each 1 KB contiguous); after this call returns they are no
+ *   longer read and the caller may free them.  embed and the norm gains are
+ *   read in place until destroy.  With SD_F32 every pointer is kept.
+ * kv_pool / workspace / weight_pack: device buffers of at least the queried
+ *   sizes, 256-byte aligned, owned by the caller, kept until destroy
+ *   (weight_pack may be NULL when its size is 0).  Initialisation work runs on
+ *   the null stream and is synchronised before returning.
  * out: receives the context.  Errors: SD_EINVAL (cfg, NULL pointer),
  * SD_ENODEV (current device is not gfx950), SD_EHIP. */
 sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_pool,
-                         void* workspace, sd_ctx** out);
+                         void* workspace, void* weight_pack, sd_ctx** out);
 
 /* Destroy a context (waits for pending work; frees host state only). */
 sd_status sd_verify_destroy(sd_ctx* ctx);

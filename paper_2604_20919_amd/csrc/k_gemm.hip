@@ -3,9 +3,10 @@
 // matrices of thousands of rows.  At these shapes the work is bound by
 // streaming the weights from HBM once, so the kernel is built around that
 // stream:
-//   * weights are read in place, row-major [out][in]; each lane loads 16
-//     contiguous bytes (8 bf16 along k) straight into the A operand of
-//     v_mfma_f32_16x16x32_bf16 (16 weight rows x 32 k);
+//   * weights are repacked once (at init) into fragment order: the A operand
+//     of v_mfma_f32_16x16x32_bf16 for 16 weight rows x 32 k is one 1 KB block
+//     laid out lane by lane, and the blocks of a 16-row group follow each
+//     other along k, so every wave-wide weight load reads 1 KB contiguously;
 //   * the activation chunk X[0:T][k0:k0+KC] is staged in LDS (double
 //     buffered) and read by the 4 waves of the workgroup as the B operand
 //     (32 k x 16 slots);
@@ -30,12 +31,8 @@ namespace sdv {
 
 struct GemmP {
     const bf16_t* X;
-    const bf16_t* W0;
-    const bf16_t* W1;
-    const bf16_t* W2;
-    int rows0, rows1, rows2;  // weight rows of each segment (buffer ranges)
-    int seg1, seg2;  // first virtual column of segments 1 and 2
-    int K, T, S, kchunks, tiles;
+    const bf16_t* Wp;  // packed weights: [vcols/16][K/32][64 lanes][8]
+    int K, KT, T, S, kchunks, tiles;
     float* part;     // [S][T][vcols] when S > 1
     int vcols;
     void* out;
@@ -82,33 +79,17 @@ void k_gemm_bf16(GemmP p) {
     const int lr = lane & 15, lg = lane >> 4;
     const int mt_act = (p.T + 15) >> 4;
 
-    // Buffer resources: the weight segment of each sub-tile is uniform over
-    // the wave (segment boundaries are multiples of 16 rows), so every load
-    // is a uniform resource + a fixed 32-bit per-lane offset + a uniform
-    // chunk offset.  Out-of-range reads return zero.
+    // Buffer resources: one uniform resource per operand, fixed 32-bit
+    // per-lane offsets, uniform chunk offsets.  Out-of-range reads return 0.
     const int wv = __builtin_amdgcn_readfirstlane(wave);
-    __amdgpu_buffer_rsrc_t wres[NSUB];
+    const uint64_t wbytes = (uint64_t)p.vcols * (uint64_t)p.K * 2u;
+    const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)p.Wp, (short)0, (int)(wbytes > 0x7fffffffu ? 0x7fffffffu : wbytes), 0x00020000);
     uint32_t woff[NSUB];
 #pragma unroll
     for (int s = 0; s < NSUB; ++s) {
-        const bf16_t* base;
-        int rows, row;
-        if (EPI == EPI_SWIGLU) {
-            const int col = tile * (NT / 2) + (wv * (NSUB / 2) + s / 2) * 16;
-            base = (s & 1) ? p.W1 : p.W0;
-            rows = (s & 1) ? p.rows1 : p.rows0;
-            row = col;
-        } else {
-            const int v = tile * NT + (wv * NSUB + s) * 16;
-            if (v < p.seg1) { base = p.W0; rows = p.rows0; row = v; }
-            else if (v < p.seg2) { base = p.W1; rows = p.rows1; row = v - p.seg1; }
-            else { base = p.W2; rows = p.rows2; row = v - p.seg2; }
-        }
-        const uint64_t bytes = (uint64_t)rows * (uint64_t)p.K * 2u;
-        wres[s] = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0,
-                                                    (int)(bytes > 0x7fffffffu ? 0x7fffffffu : bytes),
-                                                    0x00020000);
-        woff[s] = ((uint32_t)(row + lr) * (uint32_t)p.K + 8u * lg) * 2u;
+        const uint32_t vs = (uint32_t)((tile * 4 + wv) * NSUB + s);  // 16-row group
+        woff[s] = vs * (uint32_t)p.KT * 1024u + (uint32_t)lane * 16u;
     }
     const __amdgpu_buffer_rsrc_t xres =
         __builtin_amdgcn_make_buffer_rsrc((void*)p.X, (short)0, p.T * p.K * 2, 0x00020000);
@@ -151,13 +132,12 @@ void k_gemm_bf16(GemmP p) {
         }
     };
     auto load_w = [&](bf16x8 (&w)[KS][NSUB], int c) {
-        const int so = c * KC * 2;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
             for (int s = 0; s < NSUB; ++s)
                 w[ks][s] = __builtin_bit_cast(
-                    bf16x8, __builtin_amdgcn_raw_buffer_load_b128(wres[s], woff[s] + ks * 64, so, 0));
+                    bf16x8, __builtin_amdgcn_raw_buffer_load_b128(wres, woff[s], (c * KS + ks) * 1024, 0));
     };
     auto compute = [&](int buf, const bf16x8 (&w)[KS][NSUB]) {
         const bf16_t* xb = xs[buf];
@@ -217,10 +197,11 @@ void k_gemm_bf16(GemmP p) {
                 *(f32x4*)(p.part + ((size_t)split * p.T + t) * p.vcols + v) = acc[s][m];
             }
         } else if (EPI == EPI_SWIGLU) {
+            // groups 2j / 2j+1 hold gate / up rows 16j..16j+15
 #pragma unroll
             for (int s = 0; s < NSUB; s += 2)
-                swiglu_store4(p, t, tile * (NT / 2) + (wave * (NSUB / 2) + s / 2) * 16 + 4 * lg,
-                              acc[s][m], acc[s + 1][m]);
+                swiglu_store4(p, t, ((tile * 4 + wave) * NSUB + s) / 2 * 16 + 4 * lg, acc[s][m],
+                              acc[s + 1][m]);
         } else {
 #pragma unroll
             for (int s = 0; s < NSUB; ++s)
@@ -232,7 +213,7 @@ void k_gemm_bf16(GemmP p) {
 // Sum of the S split-K partials (in split order) plus the epilogue; one
 // thread per 4 output columns of one slot.
 template <int EPI>
-__global__ __launch_bounds__(256) void k_splitk_reduce(GemmP p, int nsub) {
+__global__ __launch_bounds__(256) void k_splitk_reduce(GemmP p) {
     const int ncols = EPI == EPI_SWIGLU ? p.vcols / 2 : p.vcols;
     const int per_row = ncols / 4;
     const int idx = blockIdx.x * 256 + threadIdx.x;
@@ -241,12 +222,7 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(GemmP p, int nsub) {
     const size_t stride = (size_t)p.T * p.vcols;
     const float* base = p.part + (size_t)t * p.vcols;
     if (EPI == EPI_SWIGLU) {
-        // real column c -> virtual gate / up columns of its tile
-        const int nt = 64 * nsub, half = nt / 2;
-        const int tile = c / half, rem = c % half;
-        const int pair = rem / 16, lr = rem % 16;
-        const int wave = pair / (nsub / 2), sp = pair % (nsub / 2);
-        const int vg = tile * nt + (wave * nsub + 2 * sp) * 16 + lr;
+        const int vg = (c / 16) * 32 + (c % 16);  // gate group 2j, up group 2j+1
         f32x4 g = f32x4{0.f, 0.f, 0.f, 0.f}, u = f32x4{0.f, 0.f, 0.f, 0.f};
         for (int s = 0; s < p.S; ++s) {
             g += *(const f32x4*)(base + s * stride + vg);
@@ -258,6 +234,39 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(GemmP p, int nsub) {
         for (int s = 0; s < p.S; ++s) v += *(const f32x4*)(base + s * stride + c);
         epi_store4<EPI>(p, t, c, v);
     }
+}
+
+// Weight repack into fragment order.  One wave per (16-row group, 32-k step)
+// fragment; lane (r, g) = (lane % 16, lane / 16) copies row r, k 8g..8g+7.
+// mode 0: virtual rows are the concatenation of up to three row-major
+// segments (QKV); mode 1: groups 2j / 2j+1 are rows 16j.. of src0 / src1
+// (SwiGLU gate / up).
+__global__ __launch_bounds__(256) void k_pack(const bf16_t* src0, const bf16_t* src1,
+                                              const bf16_t* src2, int seg1, int seg2, int mode,
+                                              int K, int groups, bf16_t* dst) {
+    const int KT = K / 32;
+    const long long f = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (f >= (long long)groups * KT) return;
+    const int lane = threadIdx.x & 63;
+    const int vs = (int)(f / KT), ks = (int)(f % KT);
+    const int r = lane & 15, g = lane >> 4;
+    const bf16_t* row;
+    if (mode == 1) {
+        row = ((vs & 1) ? src1 : src0) + (size_t)((vs >> 1) * 16 + r) * K;
+    } else {
+        const int v = vs * 16 + r;
+        row = v < seg1 ? src0 + (size_t)v * K
+              : v < seg2 ? src1 + (size_t)(v - seg1) * K : src2 + (size_t)(v - seg2) * K;
+    }
+    *(uint4*)(dst + ((size_t)f * 64 + lane) * 8) = *(const uint4*)(row + ks * 32 + 8 * g);
+}
+
+void launch_pack(const void* s0, const void* s1, const void* s2, int seg1, int seg2, int mode,
+                 int K, int vrows, void* dst, hipStream_t s) {
+    const long long frags = (long long)(vrows / 16) * (K / 32);
+    hipLaunchKernelGGL(k_pack, dim3((unsigned)((frags + 3) / 4)), dim3(256), 0, s,
+                       (const bf16_t*)s0, (const bf16_t*)s1, (const bf16_t*)s2, seg1, seg2, mode, K,
+                       vrows / 16, (bf16_t*)dst);
 }
 
 // ---------------------------------------------------------------------------
@@ -323,7 +332,7 @@ static GemmShape shape_for(int T, int epi) {
 }
 
 typedef void (*GemmFn)(GemmP);
-typedef void (*ReduceFn)(GemmP, int);
+typedef void (*ReduceFn)(GemmP);
 
 template <int MT, int NSUB, int KC, bool SPLIT>
 static GemmFn pick_epi(int epi) {
@@ -424,19 +433,9 @@ void launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream
     const int nt = 64 * sh.NSUB;
     GemmP p;
     p.X = (const bf16_t*)g.X;
-    p.W0 = (const bf16_t*)g.W[0];
-    p.W1 = (const bf16_t*)(g.nseg > 1 ? g.W[1] : g.W[0]);
-    p.W2 = (const bf16_t*)(g.nseg > 2 ? g.W[2] : g.W[0]);
-    p.seg1 = g.nseg > 1 ? g.seg[1] : (1 << 30);
-    p.seg2 = g.nseg > 2 ? g.seg[2] : (1 << 30);
-    if (g.epi == EPI_SWIGLU) {
-        p.rows0 = p.rows1 = p.rows2 = g.N;
-    } else {
-        p.rows0 = g.nseg > 1 ? g.seg[1] : g.N;
-        p.rows1 = g.nseg > 2 ? g.seg[2] - g.seg[1] : (g.nseg > 1 ? g.N - g.seg[1] : 0);
-        p.rows2 = g.nseg > 2 ? g.N - g.seg[2] : 0;
-    }
+    p.Wp = (const bf16_t*)g.Wp;
     p.K = g.K;
+    p.KT = g.K / 32;
     p.T = g.T;
     p.kchunks = g.K / sh.KC;
     p.vcols = g.epi == EPI_SWIGLU ? 2 * g.N : g.N;
@@ -457,7 +456,7 @@ void launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream
         hipLaunchKernelGGL(pick<true>(sh, g.epi), dim3(p.tiles * S), dim3(256), 0, s, p);
         const int ncols = g.epi == EPI_SWIGLU ? p.vcols / 2 : p.vcols;
         const int n = g.T * (ncols / 4);
-        hipLaunchKernelGGL(pick_reduce(g.epi), dim3((n + 255) / 256), dim3(256), 0, s, p, sh.NSUB);
+        hipLaunchKernelGGL(pick_reduce(g.epi), dim3((n + 255) / 256), dim3(256), 0, s, p);
     }
 }
 

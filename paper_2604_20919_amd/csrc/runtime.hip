@@ -149,6 +149,24 @@ Layout plan(const sd_config& c) {
     return L;
 }
 
+// Element offsets of the packed GEMM weights (bf16): per layer QKV, O,
+// gate/up (interleaved), down; then lm_head.
+struct PackLayout {
+    size_t qkv, o, gu, down, layer, lm, total;
+};
+
+PackLayout pack_layout(const Dims& D) {
+    PackLayout P;
+    P.qkv = 0;
+    P.o = P.qkv + (size_t)D.nqkv() * D.d;
+    P.gu = P.o + (size_t)D.d * D.nq();
+    P.down = P.gu + (size_t)2 * D.F * D.d;
+    P.layer = P.down + (size_t)D.d * D.F;
+    P.lm = P.layer * D.L;
+    P.total = P.lm + (size_t)D.V * D.d;
+    return P;
+}
+
 struct User {
     bool active = false;
     int prefix = 0;
@@ -181,6 +199,8 @@ struct sd_ctx {
     std::vector<sd_layer_weights> layers;
     KVPool kv{};
     char* ws = nullptr;
+    char* wpack = nullptr;  // packed GEMM weights (bf16 configurations)
+    PackLayout pl{};
     std::vector<User> users;
     std::vector<int> free_pages;  // stack: back is allocated first
     Slot slots[kMaxPending];
@@ -361,7 +381,9 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
             launch_rmsnorm(D, T, sb.x, w.norm1, sb.h, st);
         }
         GemmCall g{};
+        const size_t lbase = (size_t)l * c->pl.layer * 2;
         g.X = sb.h;
+        g.Wp = c->wpack + lbase + c->pl.qkv * 2;
         g.W[0] = w.wq; g.W[1] = w.wk; g.W[2] = w.wv;
         g.seg[0] = 0; g.seg[1] = D.nq(); g.seg[2] = D.nq() + D.nkv();
         g.nseg = 3;
@@ -385,6 +407,7 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
         }
         GemmCall o{};
         o.X = sb.attn;
+        o.Wp = c->wpack + lbase + c->pl.o * 2;
         o.W[0] = w.wo;
         o.nseg = 1;
         o.N = D.d;
@@ -403,6 +426,7 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
         }
         GemmCall gu{};
         gu.X = sb.h;
+        gu.Wp = c->wpack + lbase + c->pl.gu * 2;
         gu.W[0] = w.wg; gu.W[1] = w.wu;
         gu.nseg = 2;
         gu.seg[1] = D.F;
@@ -418,6 +442,7 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
         }
         GemmCall dn{};
         dn.X = sb.ffn;
+        dn.Wp = c->wpack + lbase + c->pl.down * 2;
         dn.W[0] = w.wd;
         dn.nseg = 1;
         dn.N = D.d;
@@ -435,6 +460,7 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
     launch_rmsnorm(D, T, sb.x, c->w.norm_f, sb.h, st);
     GemmCall lm{};
     lm.X = sb.h;
+    lm.Wp = c->wpack + c->pl.lm * 2;
     lm.W[0] = c->w.lm_head;
     lm.nseg = 1;
     lm.N = D.V;
@@ -466,26 +492,29 @@ const char* sd_status_str(sd_status s) {
 }
 
 sd_status sd_verify_query_sizes(const sd_config* cfg, uint64_t* kv_pool_bytes,
-                                uint64_t* workspace_bytes) {
+                                uint64_t* workspace_bytes, uint64_t* weight_pack_bytes) {
     sd_status r = validate_config(cfg);
     if (r != SD_OK) return r;
-    if (!kv_pool_bytes || !workspace_bytes) return SD_EINVAL;
+    if (!kv_pool_bytes || !workspace_bytes || !weight_pack_bytes) return SD_EINVAL;
     const Dims D = dims_of(*cfg);
     const size_t es = D.bf16 ? 2 : 4;
     *kv_pool_bytes = (uint64_t)D.L * cfg->n_pages * 2 * D.hkv * kPageTokens * D.hd * es;
     *workspace_bytes = plan(*cfg).total;
+    *weight_pack_bytes = D.bf16 ? (uint64_t)pack_layout(D).total * 2 : 0;
     return SD_OK;
 }
 
 sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_pool, void* workspace,
-                         sd_ctx** out) {
+                         void* weight_pack, sd_ctx** out) {
     if (!out) return SD_EINVAL;
     *out = nullptr;
     sd_status r = validate_config(cfg);
     if (r != SD_OK) return r;
     if (!w || !w->embed || !w->lm_head || !w->norm_f || !w->layers || !kv_pool || !workspace)
         return SD_EINVAL;
-    if (((uintptr_t)kv_pool | (uintptr_t)workspace) & (kAlign - 1)) return SD_EINVAL;
+    if (cfg->dtype == SD_BF16 && !weight_pack) return SD_EINVAL;
+    if (((uintptr_t)kv_pool | (uintptr_t)workspace | (uintptr_t)weight_pack) & (kAlign - 1))
+        return SD_EINVAL;
     for (int l = 0; l < cfg->n_layers; ++l) {
         const sd_layer_weights& lw = w->layers[l];
         if (!lw.wq || !lw.wk || !lw.wv || !lw.wo || !lw.wg || !lw.wu || !lw.wd || !lw.norm1 ||
@@ -514,6 +543,8 @@ sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_poo
     c->kv.hd = c->D.hd;
     c->kv.esize = c->D.bf16 ? 2 : 4;
     c->ws = (char*)workspace;
+    c->wpack = (char*)weight_pack;
+    c->pl = pack_layout(c->D);
     c->users.resize(cfg->max_users);
     c->free_pages.reserve(cfg->n_pages);
     for (int p = cfg->n_pages - 1; p >= 0; --p) c->free_pages.push_back(p);
@@ -558,6 +589,25 @@ sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_poo
     }
     ok = ok && hipHostMalloc((void**)&c->kvw_host, (size_t)L.max_pages * 4, hipHostMallocDefault) ==
                    hipSuccess;
+    if (ok && c->D.bf16) {
+        // repack the projection matrices and the lm_head into fragment order
+        const Dims& D = c->D;
+        const PackLayout& P = c->pl;
+        for (int l = 0; l < D.L; ++l) {
+            const sd_layer_weights& lw = c->layers[l];
+            char* base = c->wpack + (size_t)l * P.layer * 2;
+            launch_pack(lw.wq, lw.wk, lw.wv, D.nq(), D.nq() + D.nkv(), 0, D.d, D.nqkv(),
+                        base + P.qkv * 2, nullptr);
+            launch_pack(lw.wo, nullptr, nullptr, 1 << 30, 1 << 30, 0, D.nq(), D.d, base + P.o * 2,
+                        nullptr);
+            launch_pack(lw.wg, lw.wu, nullptr, 0, 0, 1, D.d, 2 * D.F, base + P.gu * 2, nullptr);
+            launch_pack(lw.wd, nullptr, nullptr, 1 << 30, 1 << 30, 0, D.F, D.d, base + P.down * 2,
+                        nullptr);
+        }
+        launch_pack(c->w.lm_head, nullptr, nullptr, 1 << 30, 1 << 30, 0, D.d, D.V,
+                    c->wpack + P.lm * 2, nullptr);
+        ok = hipGetLastError() == hipSuccess;
+    }
     ok = ok && hipDeviceSynchronize() == hipSuccess;
     if (!ok) {
         sd_verify_destroy(c);

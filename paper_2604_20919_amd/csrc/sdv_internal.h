@@ -102,7 +102,8 @@ void launch_attention(const Dims& D, const BatchView& bv, const SlotBufs& sb, co
 enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
 struct GemmCall {
     const void* X;    // [T][K] act type
-    const void* W[3]; // weight segments, rows [out][K]
+    const void* Wp;   // bf16: packed weights (fragment order, virtual rows)
+    const void* W[3]; // fp32: weight segments, rows [out][K]
     int seg[3];       // first virtual column of each segment (seg[0] = 0)
     int nseg;
     int N;            // output columns (real); SWIGLU: F, with W[0]=gate, W[1]=up
@@ -113,6 +114,8 @@ struct GemmCall {
 };
 void launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_t s);
 size_t gemm_partial_floats(const Dims& D, int Tmax);
+void launch_pack(const void* s0, const void* s1, const void* s2, int seg1, int seg2, int mode,
+                 int K, int vrows, void* dst, hipStream_t s);
 int gemm_counter_count(const Dims& D);
 
 void launch_sampler(const Dims& D, const BatchView& bv, const SlotBufs& sb, const float* logits,

@@ -66,8 +66,8 @@ def lib() -> ctypes.CDLL:
         P = ctypes.POINTER
         L.sd_status_str.restype = ctypes.c_char_p
         L.sd_status_str.argtypes = [i32]
-        L.sd_verify_query_sizes.argtypes = [P(sd_config), P(u64), P(u64)]
-        L.sd_verify_init.argtypes = [P(sd_config), P(sd_weights), vp, vp, P(vp)]
+        L.sd_verify_query_sizes.argtypes = [P(sd_config), P(u64), P(u64), P(u64)]
+        L.sd_verify_init.argtypes = [P(sd_config), P(sd_weights), vp, vp, vp, P(vp)]
         L.sd_verify_destroy.argtypes = [vp]
         L.sd_user_reset.argtypes = [vp, i32, i32, i32]
         L.sd_user_release.argtypes = [vp, i32]
@@ -124,16 +124,18 @@ def _stream(s) -> Optional[int]:
 # ---------------------------------------------------------------------------
 
 def sd_verify_query_sizes(cfg: sd_config):
-    kv, ws = ctypes.c_uint64(), ctypes.c_uint64()
-    _check("sd_verify_query_sizes", lib().sd_verify_query_sizes(ctypes.byref(cfg), ctypes.byref(kv),
-                                                                ctypes.byref(ws)))
-    return kv.value, ws.value
+    """Returns (kv_pool_bytes, workspace_bytes, weight_pack_bytes)."""
+    kv, ws, wp = ctypes.c_uint64(), ctypes.c_uint64(), ctypes.c_uint64()
+    _check("sd_verify_query_sizes", lib().sd_verify_query_sizes(
+        ctypes.byref(cfg), ctypes.byref(kv), ctypes.byref(ws), ctypes.byref(wp)))
+    return kv.value, ws.value, wp.value
 
 
-def sd_verify_init(cfg: sd_config, weights: sd_weights, kv_pool, workspace) -> int:
+def sd_verify_init(cfg: sd_config, weights: sd_weights, kv_pool, workspace, weight_pack=None) -> int:
     out = ctypes.c_void_p()
     _check("sd_verify_init", lib().sd_verify_init(ctypes.byref(cfg), ctypes.byref(weights),
-                                                  _dev(kv_pool), _dev(workspace), ctypes.byref(out)))
+                                                  _dev(kv_pool), _dev(workspace), _dev(weight_pack),
+                                                  ctypes.byref(out)))
     return out.value
 
 

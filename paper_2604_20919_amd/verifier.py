@@ -26,11 +26,12 @@ class Verifier:
                                   shape.head_dim, shape.d_ffn, shape.vocab, shape.qk_norm, dt,
                                   n_pages, max_users, max_draft, max_batch_users, max_batch_tokens,
                                   max_ctx, max_pending, shape.rope_base, shape.rms_eps)
-        kv_bytes, ws_bytes = sv.sd_verify_query_sizes(self.cfg)
-        self.kv_bytes, self.ws_bytes = kv_bytes, ws_bytes
+        kv_bytes, ws_bytes, wp_bytes = sv.sd_verify_query_sizes(self.cfg)
+        self.kv_bytes, self.ws_bytes, self.wp_bytes = kv_bytes, ws_bytes, wp_bytes
         # 256-byte aligned by the caching allocator
         self.kv_pool = torch.empty(kv_bytes, dtype=torch.uint8, device=device)
         self.workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=device)
+        self.weight_pack = torch.empty(max(wp_bytes, 256), dtype=torch.uint8, device=device)
         L = shape.n_layers
         self._layers = (sv.sd_layer_weights * L)()
         for l in range(L):
@@ -39,7 +40,8 @@ class Verifier:
         self._w = sv.sd_weights(int(weight_ptrs["embed"]), int(weight_ptrs["lm_head"]),
                                 int(weight_ptrs["norm_f"]), self._layers)
         torch.cuda.synchronize()
-        self.ctx = sv.sd_verify_init(self.cfg, self._w, self.kv_pool, self.workspace)
+        self.ctx = sv.sd_verify_init(self.cfg, self._w, self.kv_pool, self.workspace,
+                                     self.weight_pack if wp_bytes else None)
         self.max_users = max_users
         self.vocab = shape.vocab
 

@@ -52,7 +52,10 @@ def _cfg(**kw):
 
 
 def test_query_sizes_32b_shape():
-    kv, ws = sv.sd_verify_query_sizes(_cfg())
+    kv, ws, wp = sv.sd_verify_query_sizes(_cfg())
+    # projection matrices + lm_head of the 32B shape in bf16
+    per_layer = 10240 * 5120 + 5120 * 8192 + 2 * 25600 * 5120 + 5120 * 25600
+    assert wp == (64 * per_layer + 151936 * 5120) * 2
     # 64 layers x 4096 pages x (K + V) x 8 heads x 16 tokens x 128 x 2 bytes
     assert kv == 64 * 4096 * 2 * 8 * 16 * 128 * 2
     assert ws % 256 == 0 and ws > 0
@@ -84,9 +87,9 @@ def test_query_sizes_unsupported_bf16_shapes():
 
 def test_null_arguments_are_rejected_without_a_device():
     lib = sv.lib()
-    assert lib.sd_verify_query_sizes(None, None, None) == sv.SD_EINVAL
+    assert lib.sd_verify_query_sizes(None, None, None, None) == sv.SD_EINVAL
     out = ctypes.c_void_p()
-    assert lib.sd_verify_init(None, None, None, None, ctypes.byref(out)) == sv.SD_EINVAL
+    assert lib.sd_verify_init(None, None, None, None, None, ctypes.byref(out)) == sv.SD_EINVAL
     assert lib.sd_accept(None, 0, None, None, 0) == sv.SD_EINVAL
     assert lib.sd_verify_batch(None, 0, 1, None, None, None, None, 0, 0, 0, None, None) == sv.SD_EINVAL
     assert lib.sd_verify_destroy(None) == sv.SD_EINVAL
