@@ -5,19 +5,21 @@
 // positions 0 .. i_b + j (cached prefix plus the batch's own earlier slots,
 // whose keys the QK-norm/RoPE kernel has already appended to the pages).
 //
-// bf16 path (MFMA): a workgroup takes one work item (b, g, context chunk of
-// up to 256 tokens); its 4 waves take interleaved 32-token blocks.  Per
-// block, for up to 4 tiles of 16 query rows:
-//   S^T = K Q^T   with K as the A operand (16 tokens x 32 dims) and Q^T as
-//                 the B operand; the K rows are loaded in the token order
-//                 (0-3, 8-11, 16-19, 24-27 | 4-7, 12-15, 20-23, 28-31) so that
-//                 each lane ends up holding 8 consecutive tokens of one query
-//                 row -- exactly the B-operand layout of the next product;
-//   O^T += V^T P^T with V^T fragments read straight from the dim-major V
-//                 page blocks and P^T taken from registers (no LDS transpose).
-// The softmax is online in fp32 (exp2 domain).  Each wave writes its partial
+// bf16 path (MFMA).  A workgroup takes one work item (b, g, context chunk);
+// the host sizes chunks so that a batch has about 512 items of equal length.
+// The chunk is streamed in 32-token blocks (two KV pages, 16 KB of K and V)
+// through double-buffered LDS; the blocks are written to LDS in MFMA
+// fragment order, so every operand read is one contiguous 1 KB wave read.
+// Wave w owns query-row tiles w, w+4, ... (16 rows each) and, per block:
+//   S^T = K Q^T   K rows as the A operand (16 tokens x 32 dims), in the token
+//                 order (0-3, 8-11, 16-19, 24-27 | 4-7, 12-15, 20-23, 28-31)
+//                 so that each lane ends up with 8 consecutive tokens of one
+//                 query row -- the B-operand layout of the next product;
+//   O^T += V^T P^T with V^T fragments from the dim-major V page blocks and
+//                 P^T taken from registers (no transpose).
+// The softmax is online in fp32 (exp2 domain).  Each item writes one partial
 // (row max, row sum, unnormalised output); a combine kernel merges the
-// partials of all chunks in a fixed order, so results are deterministic.
+// partials of a row's chunks in chunk order, so results are deterministic.
 //
 // fp32 path: one wave per (slot, query head), plain loop over the context.
 #include "sdv_device.h"
@@ -32,160 +34,196 @@ struct AttnP {
     int layer;
     int hq, hkv, G;
     float scale_log2;  // log2(e) / sqrt(hd)
-    float* apart;      // [items*4][rows_max][hd]
-    float* aml;        // [items*4][rows_max][2]
+    float* apart;      // [items][rows_max][hd]
+    float* aml;        // [items][rows_max][2]
 };
 
 constexpr int HD = 128;
+constexpr int RT_MAX = 2;  // row tiles per wave and pass
 
-template <int RT>
+// LDS fragment index of K element (token t of the block, 16-byte dim piece j)
+__device__ __forceinline__ int k_frag_slot(int t, int j) {
+    const int tt = (t >> 2) & 1, lr = 4 * (t >> 3) + (t & 3);
+    const int ds = j >> 2, lg = j & 3;
+    return (tt * 4 + ds) * 64 + lr + 16 * lg;
+}
+// LDS fragment index of V^T piece (dim d, tokens 8h..8h+7 of page pg)
+__device__ __forceinline__ int v_frag_slot(int d, int pg, int h) {
+    return (d >> 4) * 64 + (d & 15) + 16 * (pg * 2 + h);
+}
+
 __global__ __launch_bounds__(256) void k_attn_bf16(AttnP p) {
+    __shared__ __attribute__((aligned(16))) uint4 kvs[2][1024];  // [buf][K 512 | V 512] x 16 B
     const int item = blockIdx.x;
     const int4 it = p.bv.items[item];
     const int b = it.x, g = it.y, c0 = it.z, c1 = it.w;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int lr = lane & 15, lg = lane >> 4;
     const int G = p.G;
-    const int nslot = p.bv.L[b] + 1;
-    const int R = nslot * G;
+    const int R = (p.bv.L[b] + 1) * G;
     const int prefix = p.bv.prefix[b];
     const int tbase = p.bv.slot_off[b];
     const int32_t* pt = p.bv.page_table + (size_t)b * p.bv.max_pages;
-    const bf16_t* kvb = (const bf16_t*)p.kv.base;
+    const char* kvb = (const char*)p.kv.base;
     const int nblk = (c1 - c0 + 31) >> 5;
-    const int pidx = item * 4 + wave;
-    // token order of the K rows this lane loads (A operand row lr)
-    const int pi0 = 8 * (lr >> 2) + (lr & 3);
-    const int pi1 = pi0 + 4;
 
-    for (int rp0 = 0; rp0 < R; rp0 += 16 * RT) {
-        bf16x8 qf[RT][4];
-        int lim[RT];
-        float m[RT], l[RT];
-        f32x4 o[RT][8];
+    // staging: thread i moves K piece (token i/16, dims 8*(i%16)) and V^T
+    // piece (dim i/2, tokens 8*(i%2)) of both pages of the block
+    const int tid = threadIdx.x;
+    const int kt = tid >> 4, kj = tid & 15;   // K: token 0..15 of a page, piece
+    const int vd = tid >> 1, vh = tid & 1;    // V: dim 0..127, token half
+    uint4 st[4];
+    auto load_blk = [&](int blk) {
+        const int t0 = c0 + blk * 32;
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt) {
-            const int row = rp0 + rt * 16 + lr;
-            const bool ok = row < R;
+        for (int pg = 0; pg < 2; ++pg) {
+            // clamp to the last valid token: masked tokens only need finite data
+            const int tok = min(t0 + pg * 16, c1 - 1);
+            const int page = pt[tok >> 4];
+            const char* kp = kvb + (p.kv.k_off(p.layer, page, g) * 2);
+            const char* vp = kvb + (p.kv.v_off(p.layer, page, g) * 2);
+            st[pg * 2 + 0] = *(const uint4*)(kp + (kt * HD + kj * 8) * 2);
+            uint4 v = *(const uint4*)(vp + (vd * kPageTokens + vh * 8) * 2);
+            // value slots past the chunk end may hold stale bits (even NaN):
+            // zero them so that p = 0 times v stays 0 (masked keys are
+            // handled by the score mask)
+            const int vt = t0 + pg * 16 + vh * 8;  // token of element 0
+            uint32_t* w = (uint32_t*)&v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t lo = vt + 2 * e < c1 ? 0x0000ffffu : 0u;
+                const uint32_t hi = vt + 2 * e + 1 < c1 ? 0xffff0000u : 0u;
+                w[e] &= lo | hi;
+            }
+            st[pg * 2 + 1] = v;
+        }
+    };
+    auto store_blk = [&](int buf) {
+#pragma unroll
+        for (int pg = 0; pg < 2; ++pg) {
+            kvs[buf][k_frag_slot(pg * 16 + kt, kj)] = st[pg * 2 + 0];
+            kvs[buf][512 + v_frag_slot(vd, pg, vh)] = st[pg * 2 + 1];
+        }
+    };
+
+    const int ntiles = (R + 15) >> 4;
+    for (int rp = 0; rp < ntiles; rp += 4 * RT_MAX) {
+        // this wave's row tiles in this pass: rp + wave + 4*i
+        bf16x8 qf[RT_MAX][4];
+        int lim[RT_MAX];
+        float m[RT_MAX], l[RT_MAX];
+        f32x4 o[RT_MAX][8];
+        bool act[RT_MAX];
+#pragma unroll
+        for (int i = 0; i < RT_MAX; ++i) {
+            const int tile = rp + wave + 4 * i;
+            act[i] = tile < ntiles;
+            const int row = tile * 16 + lr;
+            const bool ok = act[i] && row < R;
             const int j = ok ? row / G : 0, hh = ok ? row % G : 0;
             const bf16_t* qs = p.q + ((size_t)(tbase + j) * p.hq + g * G + hh) * HD + 8 * lg;
 #pragma unroll
-            for (int ds = 0; ds < 4; ++ds) {
-                if (ok)
-                    qf[rt][ds] = *(const bf16x8*)(qs + ds * 32);
-                else
-                    qf[rt][ds] = bf16x8{};
-            }
-            lim[rt] = prefix + j;
-            m[rt] = -INFINITY;
-            l[rt] = 0.f;
+            for (int ds = 0; ds < 4; ++ds) qf[i][ds] = ok ? *(const bf16x8*)(qs + ds * 32) : bf16x8{};
+            lim[i] = prefix + j;
+            m[i] = -INFINITY;
+            l[i] = 0.f;
 #pragma unroll
-            for (int dt = 0; dt < 8; ++dt) o[rt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int dt = 0; dt < 8; ++dt) o[i][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
-        const int rt_act = min(RT, (R - rp0 + 15) >> 4);
 
-        for (int blk = wave; blk < nblk; blk += 4) {
+        auto compute = [&](int buf, int blk) {
             const int t0 = c0 + blk * 32;
-            // K fragments of the two 16-token tiles
-            bf16x8 ka[4], kb[4];
-            {
-                const int ta = t0 + pi0, tb = t0 + pi1;
-                const bf16_t* pa = kvb + p.kv.k_off(p.layer, ta < c1 ? pt[ta >> 4] : 0, g) +
-                                   (size_t)(ta & 15) * HD + 8 * lg;
-                const bf16_t* pb = kvb + p.kv.k_off(p.layer, tb < c1 ? pt[tb >> 4] : 0, g) +
-                                   (size_t)(tb & 15) * HD + 8 * lg;
+            const uint4* kb = kvs[buf];
+            const uint4* vb = kvs[buf] + 512;
 #pragma unroll
-                for (int ds = 0; ds < 4; ++ds) {
-                    ka[ds] = ta < c1 ? *(const bf16x8*)(pa + ds * 32) : bf16x8{};
-                    kb[ds] = tb < c1 ? *(const bf16x8*)(pb + ds * 32) : bf16x8{};
-                }
-            }
-            // V^T fragments: dims dt*16 + lr, tokens t0 + 8*lg .. +7
-            bf16x8 vf[8];
-            {
-                const int tv = t0 + 8 * lg;
-                const int page = tv < c1 ? pt[tv >> 4] : 0;
-                const bf16_t* pv = kvb + p.kv.v_off(p.layer, page, g) + (tv & 15);
-                const int nvalid = c1 - tv;  // tokens of this group inside the chunk
-#pragma unroll
-                for (int dt = 0; dt < 8; ++dt) {
-                    if (nvalid >= 8) {
-                        vf[dt] = *(const bf16x8*)(pv + (size_t)(dt * 16 + lr) * kPageTokens);
-                    } else {
-                        bf16x8 v = bf16x8{};
-                        for (int e = 0; e < nvalid; ++e)
-                            v[e] = *(const __bf16*)(pv + (size_t)(dt * 16 + lr) * kPageTokens + e);
-                        vf[dt] = v;
-                    }
-                }
-            }
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt) {
-                if (rt >= rt_act) continue;
+            for (int i = 0; i < RT_MAX; ++i) {
+                if (!act[i]) continue;
                 f32x4 sa = f32x4{0.f, 0.f, 0.f, 0.f}, sb = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int ds = 0; ds < 4; ++ds) {
-                    sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[ds], qf[rt][ds], sa, 0, 0, 0);
-                    sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[ds], qf[rt][ds], sb, 0, 0, 0);
+                    const bf16x8 ka = __builtin_bit_cast(bf16x8, kb[(0 * 4 + ds) * 64 + lane]);
+                    const bf16x8 kk = __builtin_bit_cast(bf16x8, kb[(1 * 4 + ds) * 64 + lane]);
+                    sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[i][ds], sa, 0, 0, 0);
+                    sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qf[i][ds], sb, 0, 0, 0);
                 }
-                // lane holds scores of query row (rp0 + rt*16 + lr) at tokens
-                // t0 + 8*lg + e, e = 0..7 (sa: e < 4, sb: e >= 4)
-                float s[8];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    s[e] = sa[e];
-                    s[4 + e] = sb[e];
-                }
+                // lane holds the scores of its query row at tokens t0 + 8*lg + e
+                float sc[8];
                 float bm = -INFINITY;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     const int tok = t0 + 8 * lg + e;
-                    s[e] = (tok < c1 && tok <= lim[rt]) ? s[e] * p.scale_log2 : -INFINITY;
-                    bm = fmaxf(bm, s[e]);
+                    const float v = e < 4 ? sa[e] : sb[e - 4];
+                    sc[e] = (tok < c1 && tok <= lim[i]) ? v * p.scale_log2 : -INFINITY;
+                    bm = fmaxf(bm, sc[e]);
                 }
                 bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
                 bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
-                const float mn = fmaxf(m[rt], bm);
-                if (mn == -INFINITY) continue;  // nothing visible yet for this row
-                const float alpha = exp2f(m[rt] - mn);
+                const float mn = fmaxf(m[i], bm);
+                const bool live = mn != -INFINITY;  // something visible for this row
+                const float alpha = live ? exp2f(m[i] - mn) : 1.f;
                 float rs = 0.f;
-                bf16x8 pb8;
+                bf16x8 pb;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
-                    const float pe = exp2f(s[e] - mn);
+                    const float pe = live ? exp2f(sc[e] - mn) : 0.f;
                     rs += pe;
-                    pb8[e] = (__bf16)pe;
+                    pb[e] = (__bf16)pe;
                 }
                 rs += __shfl_xor(rs, 16, 64);
                 rs += __shfl_xor(rs, 32, 64);
-                l[rt] = l[rt] * alpha + rs;
-                m[rt] = mn;
+                l[i] = l[i] * alpha + rs;
+                m[i] = live ? mn : m[i];
 #pragma unroll
                 for (int dt = 0; dt < 8; ++dt) {
-                    o[rt][dt] *= alpha;
-                    o[rt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt], pb8, o[rt][dt], 0, 0, 0);
+                    const bf16x8 vf = __builtin_bit_cast(bf16x8, vb[dt * 64 + lane]);
+                    o[i][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb, o[i][dt] * alpha, 0, 0, 0);
                 }
             }
+        };
+
+        // ping-pong over blocks: prefetch block k+1 while computing block k;
+        // the prefetch index is clamped so the loads stay unconditional
+        const int last = nblk - 1;
+        load_blk(0);
+        store_blk(0);
+        __syncthreads();
+        for (int k = 0; k < nblk; k += 2) {
+            load_blk(min(k + 1, last));
+            __builtin_amdgcn_sched_barrier(0);
+            compute(0, k);
+            __builtin_amdgcn_sched_barrier(0);
+            store_blk(1);
+            __syncthreads();
+            if (k + 1 >= nblk) break;
+            load_blk(min(k + 2, last));
+            __builtin_amdgcn_sched_barrier(0);
+            compute(1, k + 1);
+            __builtin_amdgcn_sched_barrier(0);
+            store_blk(0);
+            __syncthreads();
         }
-        // partial of this wave: lane holds O^T[d = dt*16 + 4*lg + r][row lr]
+
+        // partial of this item: lane holds O^T[d = dt*16 + 4*lg + r][row lr]
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt) {
-            const int row = rp0 + rt * 16 + lr;
+        for (int i = 0; i < RT_MAX; ++i) {
+            if (!act[i]) continue;
+            const int row = (rp + wave + 4 * i) * 16 + lr;
             if (row >= R) continue;
-            const size_t pr = (size_t)pidx * p.bv.rows_max + row;
+            const size_t pr = (size_t)item * p.bv.rows_max + row;
             if (lg == 0) {
-                p.aml[pr * 2 + 0] = m[rt];
-                p.aml[pr * 2 + 1] = l[rt];
+                p.aml[pr * 2 + 0] = m[i];
+                p.aml[pr * 2 + 1] = l[i];
             }
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt)
-                *(f32x4*)(p.apart + pr * HD + dt * 16 + 4 * lg) = o[rt][dt];
+                *(f32x4*)(p.apart + pr * HD + dt * 16 + 4 * lg) = o[i][dt];
         }
+        __syncthreads();  // the LDS buffers are reused by the next row pass
     }
 }
 
-// Merge the partials of all chunks and waves of (b, g) for one query row in
-// a fixed order; one wave per (slot, query head).
+// Merge the partials of the chunks of (b, g) for one query row in chunk
+// order; one wave per (slot, query head).
 template <typename TA>
 __global__ __launch_bounds__(256) void k_attn_combine(BatchView bv, const float* apart,
                                                       const float* aml, TA* out, int hq, int hkv,
@@ -198,7 +236,7 @@ __global__ __launch_bounds__(256) void k_attn_combine(BatchView bv, const float*
     const int b = bv.slot_b[t], j = bv.slot_j[t];
     const int row = j * G + hh;
     const int i0 = bv.item_off[b], nch = (bv.item_off[b + 1] - i0) / hkv;
-    const int p0 = (i0 + g * nch) * 4, p1 = p0 + nch * 4;
+    const int p0 = i0 + g * nch, p1 = p0 + nch;
     float M = -INFINITY;
     for (int pi = p0; pi < p1; ++pi) M = fmaxf(M, aml[((size_t)pi * bv.rows_max + row) * 2]);
     float Ls = 0.f, acc0 = 0.f, acc1 = 0.f;
@@ -272,15 +310,7 @@ void launch_attention(const Dims& D, const BatchView& bv, const SlotBufs& sb, co
     p.scale_log2 = 1.4426950408889634f / sqrtf((float)D.hd);
     p.apart = sb.apart;
     p.aml = sb.aml;
-    const int rtiles = (bv.rows_max + 15) / 16;
-    if (rtiles <= 1)
-        hipLaunchKernelGGL(k_attn_bf16<1>, dim3(bv.n_items), dim3(256), 0, s, p);
-    else if (rtiles <= 2)
-        hipLaunchKernelGGL(k_attn_bf16<2>, dim3(bv.n_items), dim3(256), 0, s, p);
-    else if (rtiles <= 3)
-        hipLaunchKernelGGL(k_attn_bf16<3>, dim3(bv.n_items), dim3(256), 0, s, p);
-    else
-        hipLaunchKernelGGL(k_attn_bf16<4>, dim3(bv.n_items), dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_attn_bf16, dim3(bv.n_items), dim3(256), 0, s, p);
     hipLaunchKernelGGL(k_attn_combine<bf16_t>, dim3(blocks), dim3(256), 0, s, bv, sb.apart, sb.aml,
                        (bf16_t*)sb.attn, D.hq, D.hkv, D.hd);
 }

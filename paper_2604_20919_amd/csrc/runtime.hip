@@ -98,7 +98,9 @@ Layout plan(const sd_config& c) {
     L.Tmax = c.max_batch_tokens;
     L.Bmax = c.max_batch_users;
     L.max_pages = ceil_div(c.max_ctx, kPageTokens);
-    L.max_items = L.Bmax * D.hkv * ceil_div(c.max_ctx, kAttnChunk);
+    // the chunk length is chosen per batch so that there are at most
+    // kAttnItems + (users * kv heads) work items
+    L.max_items = kAttnItems + L.Bmax * D.hkv;
     L.rows_max = (c.max_draft + 1) * D.G();
     const size_t es = D.bf16 ? 2 : 4;
     // staging block
@@ -129,7 +131,7 @@ Layout plan(const sd_config& c) {
     L.qkv = take((size_t)L.Tmax * D.nqkv() * 4);
     L.qbuf = take((size_t)L.Tmax * D.nq() * es);
     L.attn = take((size_t)L.Tmax * D.nq() * es);
-    const size_t nparts = D.bf16 ? (size_t)L.max_items * 4 * L.rows_max : 1;
+    const size_t nparts = D.bf16 ? (size_t)L.max_items * L.rows_max : 1;
     L.apart = take(nparts * D.hd * 4);
     L.aml = take(nparts * 2 * 4);
     L.gpart_floats = gemm_partial_floats(D, L.Tmax);
@@ -314,6 +316,11 @@ void build_stage(sd_ctx* c, Slot& s, int mode, bool with_items, int* n_items, in
     doff[0] = 0;
     int maxL = 0, ni = 0;
     ioff[0] = 0;
+    // attention chunk: a multiple of 32 tokens giving about kAttnItems items
+    long total = 0;
+    for (int b = 0; b < s.B; ++b) total += (long)c->users[s.users[b]].prefix + s.L[b] + 1;
+    int chunk = (int)std::min<long>(1 << 20, std::max<long>(64, (total * c->D.hkv + kAttnItems - 1) / kAttnItems));
+    chunk = (chunk + 31) & ~31;
     for (int b = 0; b < s.B; ++b) {
         const User& u = c->users[s.users[b]];
         user[b] = s.users[b];
@@ -331,13 +338,13 @@ void build_stage(sd_ctx* c, Slot& s, int mode, bool with_items, int* n_items, in
         maxL = std::max(maxL, s.L[b]);
         if (with_items) {
             const int ctx = u.prefix + s.L[b] + 1;
-            const int nch = ceil_div(ctx, kAttnChunk);
+            const int nch = ceil_div(ctx, chunk);
             for (int g = 0; g < c->D.hkv; ++g)
                 for (int ch = 0; ch < nch; ++ch) {
                     items[ni * 4 + 0] = b;
                     items[ni * 4 + 1] = g;
-                    items[ni * 4 + 2] = ch * kAttnChunk;
-                    items[ni * 4 + 3] = std::min(ctx, (ch + 1) * kAttnChunk);
+                    items[ni * 4 + 2] = ch * chunk;
+                    items[ni * 4 + 3] = std::min(ctx, (ch + 1) * chunk);
                     ++ni;
                 }
         }

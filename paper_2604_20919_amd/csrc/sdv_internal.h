@@ -7,7 +7,7 @@
 namespace sdv {
 
 constexpr int kPageTokens = 16;   // tokens per KV page
-constexpr int kAttnChunk = 256;   // context tokens per attention work item
+constexpr int kAttnItems = 512;   // target attention work items per batch
 constexpr int kVocabChunks = 16;  // vocab split of the sampler kernels
 constexpr int kMaxPending = 8;
 
@@ -72,7 +72,7 @@ struct SlotBufs {
     float* qkv;       // [Tmax][nqkv]
     void* qbuf;       // [Tmax][nq] act type
     void* attn;       // [Tmax][nq] act type
-    float* apart;     // [max_items][rows_max][hd]
+    float* apart;     // [max_items][rows_max][hd] attention chunk partials
     float* aml;       // [max_items][rows_max][2]
     float* gpart;     // GEMM split-K partials
     size_t gpart_floats;
