@@ -318,12 +318,12 @@ __global__ void k_gemm_f32(GemmF p) {
 struct GemmShape { int MT, NSUB, KC; };
 
 static GemmShape shape_for(int T, int epi) {
+    (void)epi;
     const int mt = (T + 15) / 16;
-    const int n1 = epi == EPI_SWIGLU ? 2 : 1;  // SwiGLU pairs gate/up sub-tiles
-    if (mt <= 2) return {2, n1, 256};
-    if (mt <= 4) return {4, n1, 256};
-    if (mt <= 6) return {6, 2, 128};
-    if (mt <= 8) return {8, 2, 128};
+    if (mt <= 2) return {2, 2, 64};
+    if (mt <= 4) return {4, 2, 64};
+    if (mt <= 6) return {6, 2, 64};
+    if (mt <= 8) return {8, 2, 64};
     if (mt <= 12) return {12, 2, 64};
     if (mt <= 16) return {16, 2, 64};
     if (mt <= 20) return {20, 2, 64};
@@ -347,14 +347,11 @@ static GemmFn pick_epi(int epi) {
 
 template <bool SPLIT>
 static GemmFn pick(const GemmShape& sh, int epi) {
-    if (epi == EPI_SWIGLU && sh.MT <= 4)
-        return sh.MT == 2 ? k_gemm_bf16<2, 2, 256, EPI_SWIGLU, SPLIT>
-                          : k_gemm_bf16<4, 2, 256, EPI_SWIGLU, SPLIT>;
     switch (sh.MT) {
-        case 2: return pick_epi<2, 1, 256, SPLIT>(epi == EPI_SWIGLU ? EPI_STORE : epi);
-        case 4: return pick_epi<4, 1, 256, SPLIT>(epi == EPI_SWIGLU ? EPI_STORE : epi);
-        case 6: return pick_epi<6, 2, 128, SPLIT>(epi);
-        case 8: return pick_epi<8, 2, 128, SPLIT>(epi);
+        case 2: return pick_epi<2, 2, 64, SPLIT>(epi);
+        case 4: return pick_epi<4, 2, 64, SPLIT>(epi);
+        case 6: return pick_epi<6, 2, 64, SPLIT>(epi);
+        case 8: return pick_epi<8, 2, 64, SPLIT>(epi);
         case 12: return pick_epi<12, 2, 64, SPLIT>(epi);
         case 16: return pick_epi<16, 2, 64, SPLIT>(epi);
         case 20: return pick_epi<20, 2, 64, SPLIT>(epi);
@@ -382,13 +379,18 @@ static int cu_count() {
     return n;
 }
 
-// k splits: the smallest divisor of kchunks that gives at least one
-// workgroup per CU (more splits only add partial traffic)
+// k splits (a divisor of kchunks): the largest count giving 1.25 to 1.75
+// workgroups per CU, else the smallest giving at least 1.25 (measured on
+// the 32B shapes: fewer leave CUs idle, more add partial traffic)
 static int choose_splits(int tiles, int kchunks) {
-    const int target = cu_count();
-    if (tiles >= target) return 1;
+    const int lo = cu_count() * 5 / 4, hi = cu_count() * 7 / 4;
+    if (tiles >= lo) return 1;
+    int best = 0;
     for (int s = 2; s <= kchunks; ++s)
-        if (kchunks % s == 0 && tiles * s >= target) return s;
+        if (kchunks % s == 0 && tiles * s >= lo && tiles * s <= hi) best = s;
+    if (best) return best;
+    for (int s = 2; s <= kchunks; ++s)
+        if (kchunks % s == 0 && tiles * s >= lo) return s;
     return kchunks;
 }
 

@@ -60,30 +60,56 @@ void launch_embed(const Dims& D, const BatchView& bv, const void* embed, const S
 }
 
 // ---------------------------------------------------------------------------
-// RMSNorm of one fp32 row, output in the GEMM input type
+// RMSNorm of one fp32 row, output in the GEMM input type.  The row is read
+// once into registers (float4 loads, all issued before the reduction).
 // ---------------------------------------------------------------------------
-template <typename TA>
+template <typename TA, int PER>  // PER: float4 loads per thread
 __global__ __launch_bounds__(256) void k_rmsnorm(const float* x, const TA* gamma, TA* out, int d,
                                                  float eps) {
     __shared__ float red[4];
     const int t = blockIdx.x;
-    const float* xr = x + (size_t)t * d;
+    const float4* xr = (const float4*)(x + (size_t)t * d);
+    const int n4 = d >> 2;
+    float4 v[PER];
     float ss = 0.f;
-    for (int i = threadIdx.x; i < d; i += 256) ss += xr[i] * xr[i];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+        const int k = threadIdx.x + i * 256;
+        v[i] = k < n4 ? xr[k] : float4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int i = 0; i < PER; ++i) ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
     ss = block_sum_256(ss, red);
     const float r = 1.0f / sqrtf(ss / (float)d + eps);
-    for (int i = threadIdx.x; i < d; i += 256)
-        st(out, (size_t)t * d + i, xr[i] * r * ld(gamma, i));
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+        const int k = threadIdx.x + i * 256;
+        if (k < n4) {
+            const size_t o = (size_t)t * d + 4 * k;
+            st(out, o + 0, v[i].x * r * ld(gamma, 4 * k + 0));
+            st(out, o + 1, v[i].y * r * ld(gamma, 4 * k + 1));
+            st(out, o + 2, v[i].z * r * ld(gamma, 4 * k + 2));
+            st(out, o + 3, v[i].w * r * ld(gamma, 4 * k + 3));
+        }
+    }
+}
+
+template <typename TA>
+static void rmsnorm_dispatch(int T, const float* x, const TA* gamma, TA* out, int d, float eps,
+                             hipStream_t s) {
+    const int per = (d / 4 + 255) / 256;
+    if (per <= 1) hipLaunchKernelGGL((k_rmsnorm<TA, 1>), dim3(T), dim3(256), 0, s, x, gamma, out, d, eps);
+    else if (per <= 2) hipLaunchKernelGGL((k_rmsnorm<TA, 2>), dim3(T), dim3(256), 0, s, x, gamma, out, d, eps);
+    else if (per <= 5) hipLaunchKernelGGL((k_rmsnorm<TA, 5>), dim3(T), dim3(256), 0, s, x, gamma, out, d, eps);
+    else hipLaunchKernelGGL((k_rmsnorm<TA, 8>), dim3(T), dim3(256), 0, s, x, gamma, out, d, eps);
 }
 
 void launch_rmsnorm(const Dims& D, int T, const float* x, const void* gamma, void* out,
                     hipStream_t s) {
     if (D.bf16)
-        hipLaunchKernelGGL(k_rmsnorm<bf16_t>, dim3(T), dim3(256), 0, s, x, (const bf16_t*)gamma,
-                           (bf16_t*)out, D.d, D.eps);
+        rmsnorm_dispatch<bf16_t>(T, x, (const bf16_t*)gamma, (bf16_t*)out, D.d, D.eps, s);
     else
-        hipLaunchKernelGGL(k_rmsnorm<float>, dim3(T), dim3(256), 0, s, x, (const float*)gamma,
-                           (float*)out, D.d, D.eps);
+        rmsnorm_dispatch<float>(T, x, (const float*)gamma, (float*)out, D.d, D.eps, s);
 }
 
 // ---------------------------------------------------------------------------

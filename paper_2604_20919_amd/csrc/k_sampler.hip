@@ -3,8 +3,8 @@
 // token).  Two kernels, both split over vocab chunks so that every row is
 // read by many workgroups at once:
 //   phase A, per query slot: row max, sum of exp(z - max) and argmax (lowest
-//     index on ties); the last chunk workgroup of a slot merges the chunk
-//     partials in chunk order and takes the slot's accept decision:
+//     index on ties) per vocab chunk; a second kernel merges the chunk
+//     partials of a slot in chunk order and takes the slot's accept decision:
 //     greedy: draft == argmax; stochastic: u < p(d)/q(d) as an fp32
 //     division, u from the caller or from Philox;
 //   phase B, per user: a = number of leading accepts; greedy/force emit the
@@ -12,7 +12,9 @@
 //     argmax_k w_k / E_k with w = max(0, p - q) at slot a (p itself when all
 //     drafts passed, or when the residual is empty), E_k unit exponentials
 //     from Philox keyed by (round, user, slot, k).  Chunk winners are merged
-//     in chunk order (ties to the lowest index).
+//     in chunk order (ties to the lowest index) by a second kernel.
+// Merges run in separate launches (stream order makes the partials visible),
+// so no device-scope fence is needed.
 #include "sdv_device.h"
 #include "sdv_internal.h"
 
@@ -38,10 +40,10 @@ __device__ __forceinline__ void merge_ms(float& m, float& s, float m2, float s2)
     else s += s2 * expf(m2 - m);
 }
 
-__global__ __launch_bounds__(256) void k_sample_a(SampP p) {
+// A1: per (slot, vocab chunk): max, sum of exp(z - max), argmax (lowest index)
+__global__ __launch_bounds__(256) void k_samp_a1(SampP p) {
     __shared__ float sm[4], ss[4], sv[4];
     __shared__ int si[4];
-    __shared__ int last;
     const int t = blockIdx.x, c = blockIdx.y;
     const float* z = p.logits + (size_t)t * p.V;
     const int k0 = c * p.cw, k1 = min(p.V, k0 + p.cw);
@@ -53,7 +55,6 @@ __global__ __launch_bounds__(256) void k_sample_a(SampP p) {
         if (v > m) { s = (m == -INFINITY ? 0.f : s * expf(m - v)) + 1.f; m = v; }
         else if (v != -INFINITY) s += expf(v - m);
     }
-    // wave reduce (max, sum) and (value, index)
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
         const float m2 = __shfl_xor(m, o, 64), s2 = __shfl_xor(s, o, 64);
@@ -72,39 +73,40 @@ __global__ __launch_bounds__(256) void k_sample_a(SampP p) {
         }
         float* dst = p.spartA + ((size_t)t * kVocabChunks + c) * 4;
         dst[0] = m; dst[1] = s; dst[2] = bv; dst[3] = __int_as_float(bi);
-        __threadfence();
-        last = (atomicAdd(p.cntA + t, 1) == (int)gridDim.y - 1);
     }
-    __syncthreads();
-    if (!last || threadIdx.x != 0) return;
-    __threadfence();
+}
+
+// A2: one thread per slot: merge the chunk partials in chunk order and take
+// the slot's accept decision for the draft that follows it
+__global__ __launch_bounds__(256) void k_samp_a2(SampP p, int chunks) {
+    const int t = blockIdx.x * 256 + threadIdx.x;
+    const BatchView& bv = p.bv;
+    if (t >= bv.T) return;
     float M = -INFINITY, S = 0.f, BV = -INFINITY;
     int BI = 0;
-    for (int i = 0; i < (int)gridDim.y; ++i) {
+    for (int i = 0; i < chunks; ++i) {
         const float* e = p.spartA + ((size_t)t * kVocabChunks + i) * 4;
         merge_ms(M, S, e[0], e[1]);
         if (e[2] > BV) { BV = e[2]; BI = __float_as_int(e[3]); }
     }
-    p.cntA[t] = 0;
-    const BatchView& bv2 = p.bv;
-    const int b = bv2.slot_b[t], j = bv2.slot_j[t];
+    const int b = bv.slot_b[t], j = bv.slot_j[t];
     float acc = 0.f;
-    if (j < bv2.L[b]) {
-        const int di = bv2.draft_off[b] + j;
-        int d = bv2.drafts[di];
+    if (j < bv.L[b]) {
+        const int di = bv.draft_off[b] + j;
+        int d = bv.drafts[di];
         if (d < 0 || d >= p.V) d = 0;  // flagged by the prepare kernel
-        if (bv2.mode == 0) acc = (d == BI) ? 1.f : 0.f;
-        else if (bv2.mode == 2) acc = 1.f;
+        if (bv.mode == 0) acc = (d == BI) ? 1.f : 0.f;
+        else if (bv.mode == 2) acc = 1.f;
         else {
-            const float pd = expf(z[d] - M) / S;
-            const float qd = bv2.q[(size_t)di * p.V + d];
+            const float pd = expf(p.logits[(size_t)t * p.V + d] - M) / S;
+            const float qd = bv.q[(size_t)di * p.V + d];
             const float r = pd / qd;
             float u;
-            if (bv2.accept_u) u = bv2.accept_u[di];
+            if (bv.accept_u) u = bv.accept_u[di];
             else {
-                const u64x4 ctr = {bv2.round, (uint64_t)bv2.user_id[b],
+                const u64x4 ctr = {bv.round, (uint64_t)bv.user_id[b],
                                    ((uint64_t)PURPOSE_ACCEPT << 32) | (uint64_t)j, 0ull};
-                u = accept_uniform(philox4x64_10(ctr, bv2.seed, 0ull).x);
+                u = accept_uniform(philox4x64_10(ctr, bv.seed, 0ull).x);
             }
             acc = (u < r) ? 1.f : 0.f;
         }
@@ -113,34 +115,33 @@ __global__ __launch_bounds__(256) void k_sample_a(SampP p) {
     st4[0] = M; st4[1] = S; st4[2] = __int_as_float(BI); st4[3] = acc;
 }
 
-__global__ __launch_bounds__(256) void k_sample_b(SampP p) {
+__device__ __forceinline__ int leading_accepts(const SampP& p, int b) {
+    const int Lb = p.bv.L[b], so = p.bv.slot_off[b];
+    if (p.bv.mode == 2) return Lb;
+    int a = 0;
+    while (a < Lb && p.sstat[(size_t)(so + a) * 4 + 3] != 0.f) ++a;
+    return a;
+}
+
+// B1 (stochastic): per (user, vocab chunk): best race keys of the residual
+// max(0, p - q) at the stop slot and of p itself (the bonus draw, and the
+// fallback when the residual is empty); both use the same unit exponentials
+__global__ __launch_bounds__(256) void k_samp_b1(SampP p) {
     __shared__ float sk[2][4];
     __shared__ int sidx[2][4];
-    __shared__ int last;
     const int b = blockIdx.x, c = blockIdx.y;
     const BatchView& bv = p.bv;
     const int Lb = bv.L[b];
-    const int so = bv.slot_off[b];
-    int a = 0;
-    if (bv.mode == 2) a = Lb;
-    else
-        while (a < Lb && p.sstat[(size_t)(so + a) * 4 + 3] != 0.f) ++a;
-    const float* st4 = p.sstat + (size_t)(so + a) * 4;
-    if (bv.mode != 1) {
-        if (c == 0 && threadIdx.x == 0) {
-            p.result[b] = a;
-            p.result[p.bmax + b] = __float_as_int(st4[2]);
-            if (b == 0) p.result[2 * p.bmax] = *bv.flags;
-        }
-        return;
-    }
+    const int a = leading_accepts(p, b);
+    const int row = bv.slot_off[b] + a;
+    const float* st4 = p.sstat + (size_t)row * 4;
     const float M = st4[0], S = st4[1];
-    const float* z = p.logits + (size_t)(so + a) * p.V;
+    const float* z = p.logits + (size_t)row * p.V;
     const bool resid = a < Lb;
     const float* qr = resid ? bv.q + (size_t)(bv.draft_off[b] + a) * p.V : nullptr;
     const uint64_t user = (uint64_t)bv.user_id[b];
     const int k0 = c * p.cw, k1 = min(p.V, k0 + p.cw);
-    float br = -1.f, bp = -1.f;  // best residual / target keys
+    float br = -1.f, bp = -1.f;
     int ir = 0x7fffffff, ip = 0x7fffffff;
     for (int k4 = k0 + 4 * threadIdx.x; k4 < k1; k4 += 4 * 256) {
         const u64x4 ctr = {bv.round, user, ((uint64_t)PURPOSE_RACE << 32) | (uint64_t)a,
@@ -184,23 +185,33 @@ __global__ __launch_bounds__(256) void k_sample_b(SampP p) {
         }
         float* dst = p.spartB + ((size_t)b * kVocabChunks + c) * 4;
         dst[0] = br; dst[1] = __int_as_float(ir); dst[2] = bp; dst[3] = __int_as_float(ip);
-        __threadfence();
-        last = (atomicAdd(p.cntB + b, 1) == (int)gridDim.y - 1);
     }
-    __syncthreads();
-    if (!last || threadIdx.x != 0) return;
-    __threadfence();
-    float BR = -1.f, BP = -1.f;
-    int IR = 0, IP = 0;
-    for (int i = 0; i < (int)gridDim.y; ++i) {
-        const float* e = p.spartB + ((size_t)b * kVocabChunks + i) * 4;
-        if (e[0] > BR) { BR = e[0]; IR = __float_as_int(e[1]); }
-        if (e[2] > BP) { BP = e[2]; IP = __float_as_int(e[3]); }
-    }
-    p.cntB[b] = 0;
-    p.result[b] = a;
-    p.result[p.bmax + b] = (resid && BR > 0.f) ? IR : IP;
+}
+
+// B2: one thread per user: the stop slot a, then the token -- argmax of that
+// slot (greedy / force), or the race winner merged over chunks in chunk
+// order (ties to the lowest index)
+__global__ __launch_bounds__(256) void k_samp_b2(SampP p, int chunks) {
+    const int b = blockIdx.x * 256 + threadIdx.x;
+    const BatchView& bv = p.bv;
     if (b == 0) p.result[2 * p.bmax] = *bv.flags;
+    if (b >= bv.B) return;
+    const int a = leading_accepts(p, b);
+    int tok;
+    if (bv.mode != 1) {
+        tok = __float_as_int(p.sstat[(size_t)(bv.slot_off[b] + a) * 4 + 2]);
+    } else {
+        float BR = -1.f, BP = -1.f;
+        int IR = 0, IP = 0;
+        for (int i = 0; i < chunks; ++i) {
+            const float* e = p.spartB + ((size_t)b * kVocabChunks + i) * 4;
+            if (e[0] > BR) { BR = e[0]; IR = __float_as_int(e[1]); }
+            if (e[2] > BP) { BP = e[2]; IP = __float_as_int(e[3]); }
+        }
+        tok = (a < bv.L[b] && BR > 0.f) ? IR : IP;
+    }
+    p.result[b] = a;
+    p.result[p.bmax + b] = tok;
 }
 
 void launch_sampler(const Dims& D, const BatchView& bv, const SlotBufs& sb, const float* logits,
@@ -218,8 +229,10 @@ void launch_sampler(const Dims& D, const BatchView& bv, const SlotBufs& sb, cons
     p.result = sb.result;
     p.bmax = sb.bmax;
     const int chunks = (D.V + p.cw - 1) / p.cw;
-    hipLaunchKernelGGL(k_sample_a, dim3(bv.T, chunks), dim3(256), 0, s, p);
-    hipLaunchKernelGGL(k_sample_b, dim3(bv.B, chunks), dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_samp_a1, dim3(bv.T, chunks), dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_samp_a2, dim3((bv.T + 255) / 256), dim3(256), 0, s, p, chunks);
+    if (bv.mode == 1) hipLaunchKernelGGL(k_samp_b1, dim3(bv.B, chunks), dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_samp_b2, dim3((bv.B + 255) / 256), dim3(256), 0, s, p, chunks);
 }
 
 }  // namespace sdv

@@ -70,6 +70,7 @@ sd_status validate_config(const sd_config* c) {
         return SD_EINVAL;
     if (c->n_q_heads % c->n_kv_heads) return SD_EINVAL;
     if (c->head_dim % 2 || c->head_dim > 128) return SD_EINVAL;
+    if (c->d_model % 4 || c->d_model > 8192) return SD_ENOTIMPL;
     if (c->dtype != SD_F32 && c->dtype != SD_BF16) return SD_EINVAL;
     if (c->page_tokens != kPageTokens) return SD_EINVAL;
     if (c->n_pages < 1 || c->max_users < 1 || c->max_draft < 1 || c->max_draft > 64) return SD_EINVAL;
