@@ -232,14 +232,14 @@ sd_status sd_debug_logits(sd_ctx* ctx, int32_t batch, float* dst, sd_stream stre
 
 /* Kernel classes for sd_profile_begin. */
 enum {
-    SD_K_QKV = 1,      /* QKV projection GEMM */
+    SD_K_QKV = 1,      /* QKV projection GEMM + fused QK-norm/RoPE/KV append */
     SD_K_ATTN = 2,     /* paged attention + chunk combine */
-    SD_K_O = 3,        /* output projection GEMM + residual */
-    SD_K_GATEUP = 4,   /* gate/up GEMM + SwiGLU */
-    SD_K_DOWN = 5,     /* down projection GEMM + residual */
-    SD_K_LMHEAD = 6,   /* final norm + lm_head GEMM */
+    SD_K_O = 3,        /* output projection GEMM + fused residual/RMSNorm */
+    SD_K_GATEUP = 4,   /* gate/up GEMM with the SwiGLU epilogue */
+    SD_K_DOWN = 5,     /* down projection GEMM + fused residual/RMSNorm */
+    SD_K_LMHEAD = 6,   /* lm_head GEMM */
     SD_K_SAMPLER = 7,  /* accept/resample kernels */
-    SD_K_SMALL = 8     /* embedding, RMSNorm, QK-norm/RoPE/KV append */
+    SD_K_SMALL = 8     /* batch preparation, embedding + first RMSNorm */
 };
 
 /* Diagnostic timing: until sd_profile_end, every sd_verify_batch records a

@@ -61,7 +61,7 @@ __device__ __forceinline__ void swiglu_store4(const GemmP& p, int t, int col, f3
     *(uint2*)o = pk;
 }
 
-template <int MT, int NSUB, int KC, int EPI, bool SPLIT>
+template <int MT, int NSUB, int KC, int EPI, bool SPLIT, int PD = 2>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2)))
 void k_gemm_bf16(GemmP p) {
     constexpr int NT = 4 * NSUB * 16;  // virtual columns per tile
@@ -103,14 +103,19 @@ void k_gemm_bf16(GemmP p) {
     const int c_begin = split * p.kchunks / p.S;
     const int c_end = (split + 1) * p.kchunks / p.S;
 
-    // Ping-pong pipeline: while chunk c is multiplied out of (LDS buffer
-    // c&1, weight registers A or B), X(c+1) and W(c+1) are requested into the
-    // other set.  The loop is unrolled by two so the two register sets swap
-    // roles statically, and scheduling barriers keep the order issue loads ->
-    // multiply -> store X(c+1) to LDS.  X rows >= T are read as row T-1: they
+    // Register-ring pipeline with prefetch distance PD chunks: while chunk c
+    // is multiplied (X from LDS buffer c&1, W from ring set c % NB), X and W
+    // of chunk c+PD are requested into ring set (c+PD) % NB, and X(c+1),
+    // requested PD-1 chunks earlier, is stored to the other LDS buffer.  The
+    // loop is unrolled by NB so that ring indices are compile-time constants
+    // (register copies would force waits on loads still in flight), the
+    // loads are unconditional (the chunk index is clamped; the last steps
+    // re-read a cached chunk) and scheduling barriers keep the order issue
+    // loads -> multiply -> store X.  X rows >= T are read as row T-1: they
     // only feed output slots >= T, which are never stored.
-    uint4 xr[XPT];
-    bf16x8 wa[KS][NSUB], wb[KS][NSUB];
+    constexpr int NB = PD + 1;
+    uint4 xr[NB][XPT];
+    bf16x8 wr[NB][KS][NSUB];
     uint32_t xoff[XPT];
 #pragma unroll
     for (int i = 0; i < XPT; ++i) {
@@ -118,17 +123,17 @@ void k_gemm_bf16(GemmP p) {
         const int r = min(idx / PPR, p.T - 1), cc = idx % PPR;
         xoff[i] = ((uint32_t)r * (uint32_t)p.K + (uint32_t)cc * 8u) * 2u;
     }
-    auto load_x = [&](int c) {
+    auto load_x = [&](uint4 (&x)[XPT], int c) {
         const int so = c * KC * 2;
 #pragma unroll
         for (int i = 0; i < XPT; ++i)
-            xr[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xres, xoff[i], so, 0));
+            x[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xres, xoff[i], so, 0));
     };
-    auto store_x = [&](int buf) {
+    auto store_x = [&](const uint4 (&x)[XPT], int buf) {
 #pragma unroll
         for (int i = 0; i < XPT; ++i) {
             const int idx = threadIdx.x + i * 256;
-            *(uint4*)(&xs[buf][(idx / PPR) * LDX + (idx % PPR) * 8]) = xr[i];
+            *(uint4*)(&xs[buf][(idx / PPR) * LDX + (idx % PPR) * 8]) = x[i];
         }
     };
     auto load_w = [&](bf16x8 (&w)[KS][NSUB], int c) {
@@ -156,33 +161,27 @@ void k_gemm_bf16(GemmP p) {
         }
     };
 
-    load_x(c_begin);
-    load_w(wa, c_begin);
-    store_x(0);
-    __syncthreads();
-    // The prefetch is unconditional (the chunk index is clamped, so the last
-    // step re-reads the current chunk from cache): conditional loads would
-    // make the compiler's wait-count analysis merge states pessimistically
-    // and wait for the prefetch inside the multiply.
     const int c_last = c_end - 1;
-    for (int c = c_begin; c < c_end; c += 2) {
-        // even step: compute c from (LDS 0, wa), prefetch c+1 into (xr, wb)
-        load_x(min(c + 1, c_last));
-        load_w(wb, min(c + 1, c_last));
-        __builtin_amdgcn_sched_barrier(0);
-        compute(0, wa);
-        __builtin_amdgcn_sched_barrier(0);
-        store_x(1);
-        __syncthreads();
-        if (c + 1 >= c_end) break;
-        // odd step: compute c+1 from (LDS 1, wb), prefetch c+2 into (xr, wa)
-        load_x(min(c + 2, c_last));
-        load_w(wa, min(c + 2, c_last));
-        __builtin_amdgcn_sched_barrier(0);
-        compute(1, wb);
-        __builtin_amdgcn_sched_barrier(0);
-        store_x(0);
-        __syncthreads();
+#pragma unroll
+    for (int u = 0; u < PD; ++u) {
+        load_x(xr[u], min(c_begin + u, c_last));
+        load_w(wr[u], min(c_begin + u, c_last));
+    }
+    store_x(xr[0], 0);
+    __syncthreads();
+    for (int c0 = c_begin; c0 < c_end; c0 += NB) {
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const int c = c0 + u;
+            if (c >= c_end) break;
+            load_x(xr[(u + PD) % NB], min(c + PD, c_last));
+            load_w(wr[(u + PD) % NB], min(c + PD, c_last));
+            __builtin_amdgcn_sched_barrier(0);
+            compute((c - c_begin) & 1, wr[u]);
+            __builtin_amdgcn_sched_barrier(0);
+            store_x(xr[(u + 1) % NB], ((c - c_begin) & 1) ^ 1);
+            __syncthreads();
+        }
     }
 
     // lane holds D[n = 4*lg + r][t = lr] of each (sub-tile, slot tile)
@@ -395,7 +394,8 @@ static int choose_splits(int tiles, int kchunks) {
 }
 
 size_t gemm_partial_floats(const Dims& D, int Tmax) {
-    if (!D.bf16) return 0;
+    // fp32 path: one plane of the widest raw output
+    if (!D.bf16) return (size_t)Tmax * (size_t)std::max(D.nqkv(), D.d);
     // the split count is bounded by the CU count over the tile count, so
     // S * vcols <= ~2 * (CUs * NT) for every call; reserve generously
     const size_t widest = (size_t)std::max(std::max(D.nqkv(), D.d), 2 * D.F);
@@ -412,7 +412,7 @@ bool gemm_shape_ok(const Dims& D, int T, int K, int N, int epi) {
     return K % sh.KC == 0 && vcols % (64 * sh.NSUB) == 0;
 }
 
-void launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_t s) {
+int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_t s) {
     if (!D.bf16) {
         GemmF p;
         p.X = (const float*)g.X;
@@ -424,12 +424,12 @@ void launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream
         p.N = g.N;
         p.K = g.K;
         p.T = g.T;
-        p.epi = g.epi;
-        p.out = (float*)g.out;
-        p.ldo = g.ldo;
+        p.epi = g.raw ? EPI_STORE : g.epi;
+        p.out = g.raw ? sb.gpart : (float*)g.out;
+        p.ldo = g.raw ? g.N : g.ldo;
         const int n = g.T * g.N;
         hipLaunchKernelGGL(k_gemm_f32, dim3((n + 255) / 256), dim3(256), 0, s, p);
-        return;
+        return 1;
     }
     const GemmShape sh = shape_for(g.T, g.epi);
     const int nt = 64 * sh.NSUB;
@@ -452,7 +452,10 @@ void launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream
     p.part = sb.gpart;
     p.out = g.out;
     p.ldo = g.ldo;
-    if (S == 1) {
+    if (g.raw) {
+        // S partial planes [S][T][N] for a fused consumer to reduce
+        hipLaunchKernelGGL(pick<true>(sh, EPI_STORE), dim3(p.tiles * S), dim3(256), 0, s, p);
+    } else if (S == 1) {
         hipLaunchKernelGGL(pick<false>(sh, g.epi), dim3(p.tiles), dim3(256), 0, s, p);
     } else {
         hipLaunchKernelGGL(pick<true>(sh, g.epi), dim3(p.tiles * S), dim3(256), 0, s, p);
@@ -460,6 +463,7 @@ void launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream
         const int n = g.T * (ncols / 4);
         hipLaunchKernelGGL(pick_reduce(g.epi), dim3((n + 255) / 256), dim3(256), 0, s, p);
     }
+    return S;
 }
 
 }  // namespace sdv

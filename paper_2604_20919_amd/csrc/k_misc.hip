@@ -40,76 +40,141 @@ void launch_prepare(const Dims& D, const BatchView& bv, const SlotBufs& sb, hipS
 }
 
 // ---------------------------------------------------------------------------
-// embedding gather into the fp32 residual stream
+// Split-K reduction fused with the residual add and the next RMSNorm:
+// x[t] += sum_s part[s][t] (split order, fixed), h[t] = x[t] * rstd * gamma.
+// One workgroup per slot row, the row held in registers.
 // ---------------------------------------------------------------------------
-template <typename TW>
-__global__ void k_embed(const int32_t* tok, const TW* E, float* x, int d) {
+template <typename TA, int PER>
+__global__ __launch_bounds__(1024) void k_resid_norm(const float* part, int S, int T, float* x,
+                                                     const TA* gamma, TA* h, int d, float eps) {
+    __shared__ float red[16];
     const int t = blockIdx.x;
-    const size_t row = (size_t)tok[t] * d;
-    for (int i = threadIdx.x; i < d; i += blockDim.x) x[(size_t)t * d + i] = ld(E, row + i);
-}
-
-void launch_embed(const Dims& D, const BatchView& bv, const void* embed, const SlotBufs& sb,
-                  hipStream_t s) {
-    if (D.bf16)
-        hipLaunchKernelGGL(k_embed<bf16_t>, dim3(bv.T), dim3(256), 0, s, sb.tok,
-                           (const bf16_t*)embed, sb.x, D.d);
-    else
-        hipLaunchKernelGGL(k_embed<float>, dim3(bv.T), dim3(256), 0, s, sb.tok,
-                           (const float*)embed, sb.x, D.d);
-}
-
-// ---------------------------------------------------------------------------
-// RMSNorm of one fp32 row, output in the GEMM input type.  The row is read
-// once into registers (float4 loads, all issued before the reduction).
-// ---------------------------------------------------------------------------
-template <typename TA, int PER>  // PER: float4 loads per thread
-__global__ __launch_bounds__(256) void k_rmsnorm(const float* x, const TA* gamma, TA* out, int d,
-                                                 float eps) {
-    __shared__ float red[4];
-    const int t = blockIdx.x;
-    const float4* xr = (const float4*)(x + (size_t)t * d);
     const int n4 = d >> 2;
+    float4* xr = (float4*)(x + (size_t)t * d);
+    const size_t plane4 = (size_t)T * d / 4;
+    const float4* pr = (const float4*)(part + (size_t)t * d);
     float4 v[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) v[i] = float4{0.f, 0.f, 0.f, 0.f};
+    // partial planes in split order, four planes' loads in flight at a time
+    int sp = 0;
+    for (; sp + 4 <= S; sp += 4) {
+        float4 b[4][PER];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int i = 0; i < PER; ++i) {
+                const int k = threadIdx.x + i * 1024;
+                b[q][i] = k < n4 ? pr[(sp + q) * plane4 + k] : float4{0.f, 0.f, 0.f, 0.f};
+            }
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int i = 0; i < PER; ++i) {
+                v[i].x += b[q][i].x; v[i].y += b[q][i].y; v[i].z += b[q][i].z; v[i].w += b[q][i].w;
+            }
+    }
+    for (; sp < S; ++sp)
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int k = threadIdx.x + i * 1024;
+            if (k < n4) {
+                const float4 b = pr[sp * plane4 + k];
+                v[i].x += b.x; v[i].y += b.y; v[i].z += b.z; v[i].w += b.w;
+            }
+        }
     float ss = 0.f;
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-        const int k = threadIdx.x + i * 256;
-        v[i] = k < n4 ? xr[k] : float4{0.f, 0.f, 0.f, 0.f};
+        const int k = threadIdx.x + i * 1024;
+        if (k < n4) {
+            float4 r = xr[k];
+            r.x += v[i].x; r.y += v[i].y; r.z += v[i].z; r.w += v[i].w;
+            xr[k] = r;
+            v[i] = r;
+        }
+        ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
     }
+    ss = wave_sum(ss);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    float tot = 0.f;
 #pragma unroll
-    for (int i = 0; i < PER; ++i) ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
-    ss = block_sum_256(ss, red);
-    const float r = 1.0f / sqrtf(ss / (float)d + eps);
+    for (int w = 0; w < 16; ++w) tot += red[w];
+    const float rs = 1.0f / sqrtf(tot / (float)d + eps);
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-        const int k = threadIdx.x + i * 256;
+        const int k = threadIdx.x + i * 1024;
         if (k < n4) {
             const size_t o = (size_t)t * d + 4 * k;
-            st(out, o + 0, v[i].x * r * ld(gamma, 4 * k + 0));
-            st(out, o + 1, v[i].y * r * ld(gamma, 4 * k + 1));
-            st(out, o + 2, v[i].z * r * ld(gamma, 4 * k + 2));
-            st(out, o + 3, v[i].w * r * ld(gamma, 4 * k + 3));
+            st(h, o + 0, v[i].x * rs * ld(gamma, 4 * k + 0));
+            st(h, o + 1, v[i].y * rs * ld(gamma, 4 * k + 1));
+            st(h, o + 2, v[i].z * rs * ld(gamma, 4 * k + 2));
+            st(h, o + 3, v[i].w * rs * ld(gamma, 4 * k + 3));
         }
     }
 }
 
 template <typename TA>
-static void rmsnorm_dispatch(int T, const float* x, const TA* gamma, TA* out, int d, float eps,
-                             hipStream_t s) {
-    const int per = (d / 4 + 255) / 256;
-    if (per <= 1) hipLaunchKernelGGL((k_rmsnorm<TA, 1>), dim3(T), dim3(256), 0, s, x, gamma, out, d, eps);
-    else if (per <= 2) hipLaunchKernelGGL((k_rmsnorm<TA, 2>), dim3(T), dim3(256), 0, s, x, gamma, out, d, eps);
-    else if (per <= 5) hipLaunchKernelGGL((k_rmsnorm<TA, 5>), dim3(T), dim3(256), 0, s, x, gamma, out, d, eps);
-    else hipLaunchKernelGGL((k_rmsnorm<TA, 8>), dim3(T), dim3(256), 0, s, x, gamma, out, d, eps);
+static void resid_norm_dispatch(int T, const float* part, int S, float* x, const TA* gamma, TA* h,
+                                int d, float eps, hipStream_t s) {
+    const int per = (d / 4 + 1023) / 1024;
+    if (per <= 1) hipLaunchKernelGGL((k_resid_norm<TA, 1>), dim3(T), dim3(1024), 0, s, part, S, T, x, gamma, h, d, eps);
+    else hipLaunchKernelGGL((k_resid_norm<TA, 2>), dim3(T), dim3(1024), 0, s, part, S, T, x, gamma, h, d, eps);
 }
 
-void launch_rmsnorm(const Dims& D, int T, const float* x, const void* gamma, void* out,
-                    hipStream_t s) {
+void launch_resid_norm(const Dims& D, int T, const float* part, int S, float* x,
+                       const void* gamma, void* h, hipStream_t s) {
     if (D.bf16)
-        rmsnorm_dispatch<bf16_t>(T, x, (const bf16_t*)gamma, (bf16_t*)out, D.d, D.eps, s);
+        resid_norm_dispatch<bf16_t>(T, part, S, x, (const bf16_t*)gamma, (bf16_t*)h, D.d, D.eps, s);
     else
-        rmsnorm_dispatch<float>(T, x, (const float*)gamma, (float*)out, D.d, D.eps, s);
+        resid_norm_dispatch<float>(T, part, S, x, (const float*)gamma, (float*)h, D.d, D.eps, s);
+}
+
+// embedding gather fused with the first RMSNorm
+template <typename TA, int PER>
+__global__ __launch_bounds__(256) void k_embed_norm(const int32_t* tok, const TA* E,
+                                                    const TA* gamma, float* x, TA* h, int d,
+                                                    float eps) {
+    __shared__ float red[4];
+    const int t = blockIdx.x;
+    const size_t row = (size_t)tok[t] * d;
+    float v[PER][4];
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+        const int k = threadIdx.x + i * 256;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            v[i][e] = 4 * k < d ? ld(E, row + 4 * k + e) : 0.f;
+            ss += v[i][e] * v[i][e];
+        }
+        if (4 * k < d)
+            *(float4*)(x + (size_t)t * d + 4 * k) = float4{v[i][0], v[i][1], v[i][2], v[i][3]};
+    }
+    ss = block_sum_256(ss, red);
+    const float rs = 1.0f / sqrtf(ss / (float)d + eps);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+        const int k = threadIdx.x + i * 256;
+        if (4 * k < d)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                st(h, (size_t)t * d + 4 * k + e, v[i][e] * rs * ld(gamma, 4 * k + e));
+    }
+}
+
+void launch_embed_norm(const Dims& D, const BatchView& bv, const void* embed, const void* gamma,
+                       const SlotBufs& sb, hipStream_t s) {
+    const int per = (D.d / 4 + 255) / 256;
+#define EN(TA, P) hipLaunchKernelGGL((k_embed_norm<TA, P>), dim3(bv.T), dim3(256), 0, s, sb.tok, \
+                                     (const TA*)embed, (const TA*)gamma, sb.x, (TA*)sb.h, D.d, D.eps)
+    if (D.bf16) {
+        if (per <= 1) EN(bf16_t, 1); else if (per <= 2) EN(bf16_t, 2); else if (per <= 5) EN(bf16_t, 5); else EN(bf16_t, 8);
+    } else {
+        if (per <= 1) EN(float, 1); else if (per <= 2) EN(float, 2); else if (per <= 5) EN(float, 5); else EN(float, 8);
+    }
+#undef EN
 }
 
 // ---------------------------------------------------------------------------
@@ -120,10 +185,10 @@ void launch_rmsnorm(const Dims& D, int T, const float* x, const void* gamma, voi
 // value row (unrotated) into the V^T block.
 // ---------------------------------------------------------------------------
 template <typename TA>
-__global__ __launch_bounds__(256) void k_qkrope(BatchView bv, const float* qkv, const float* cs,
-                                                TA* qbuf, KVPool kv, int layer, const TA* qn,
-                                                const TA* kn, int hq, int hkv, int hd, int qk_norm,
-                                                float eps) {
+__global__ __launch_bounds__(256) void k_qkrope(BatchView bv, const float* qkv, int S,
+                                                const float* cs, TA* qbuf, KVPool kv, int layer,
+                                                const TA* qn, const TA* kn, int hq, int hkv, int hd,
+                                                int qk_norm, float eps) {
     const int wave = (blockIdx.x * 4) + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     const int nh = hq + hkv;
@@ -134,9 +199,15 @@ __global__ __launch_bounds__(256) void k_qkrope(BatchView bv, const float* qkv, 
     const bool act = lane < half;
     const bool is_q = h < hq;
     const int col = is_q ? h * hd : hq * hd + (h - hq) * hd;
+    // qkv holds S split-K partial planes [S][T][nqkv]; add them in order
+    const size_t plane = (size_t)bv.T * nqkv;
     const float* src = qkv + (size_t)t * nqkv + col;
-    float x0 = act ? src[lane] : 0.f;
-    float x1 = act ? src[lane + half] : 0.f;
+    float x0 = 0.f, x1 = 0.f;
+    if (act)
+        for (int sp = 0; sp < S; ++sp) {
+            x0 += src[sp * plane + lane];
+            x1 += src[sp * plane + lane + half];
+        }
     if (qk_norm) {
         const float ss = wave_sum(x0 * x0 + x1 * x1);
         const float r = 1.0f / sqrtf(ss / (float)hd + eps);
@@ -167,21 +238,27 @@ __global__ __launch_bounds__(256) void k_qkrope(BatchView bv, const float* qkv, 
     st(kd, lane, y0);
     st(kd, lane + half, y1);
     const float* vs = qkv + (size_t)t * nqkv + (size_t)(hq + hkv) * hd + (size_t)g * hd;
+    float v0 = 0.f, v1 = 0.f;
+    for (int sp = 0; sp < S; ++sp) {
+        v0 += vs[sp * plane + lane];
+        v1 += vs[sp * plane + lane + half];
+    }
     TA* vd = base + kv.v_off(layer, page, g);
-    st(vd, (size_t)lane * kPageTokens + off, vs[lane]);
-    st(vd, (size_t)(lane + half) * kPageTokens + off, vs[lane + half]);
+    st(vd, (size_t)lane * kPageTokens + off, v0);
+    st(vd, (size_t)(lane + half) * kPageTokens + off, v1);
 }
 
-void launch_qkrope(const Dims& D, const BatchView& bv, const SlotBufs& sb, const KVPool& kv,
-                   int layer, const void* qn, const void* kn, hipStream_t s) {
+void launch_qkv_finish(const Dims& D, const BatchView& bv, const SlotBufs& sb, const KVPool& kv,
+                       int layer, const float* part, int S, const void* qn, const void* kn,
+                       hipStream_t s) {
     const int waves = bv.T * (D.hq + D.hkv);
     const int blocks = (waves + 3) / 4;
     if (D.bf16)
-        hipLaunchKernelGGL(k_qkrope<bf16_t>, dim3(blocks), dim3(256), 0, s, bv, sb.qkv, sb.cs,
+        hipLaunchKernelGGL(k_qkrope<bf16_t>, dim3(blocks), dim3(256), 0, s, bv, part, S, sb.cs,
                            (bf16_t*)sb.qbuf, kv, layer, (const bf16_t*)qn, (const bf16_t*)kn, D.hq,
                            D.hkv, D.hd, D.qk_norm, D.eps);
     else
-        hipLaunchKernelGGL(k_qkrope<float>, dim3(blocks), dim3(256), 0, s, bv, sb.qkv, sb.cs,
+        hipLaunchKernelGGL(k_qkrope<float>, dim3(blocks), dim3(256), 0, s, bv, part, S, sb.cs,
                            (float*)sb.qbuf, kv, layer, (const float*)qn, (const float*)kn, D.hq,
                            D.hkv, D.hd, D.qk_norm, D.eps);
 }

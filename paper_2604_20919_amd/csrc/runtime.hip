@@ -38,7 +38,7 @@ struct Layout {
     size_t st_user, st_prefix, st_L, st_root, st_soff, st_doff, st_sb, st_sj, st_pt, st_items,
         st_ioff, st_flags, st_bytes;
     // slot buffers (byte offsets within the slot)
-    size_t stage, tok, cs, x, h, ffn, qkv, qbuf, attn, apart, aml, gpart, gcount, logits, sstat, spart,
+    size_t stage, tok, cs, x, h, ffn, qbuf, attn, apart, aml, gpart, gcount, logits, sstat, spart,
         spartB, scount, scountB, result, slot_bytes;
     size_t gpart_floats;
     int gcount_n;
@@ -129,7 +129,6 @@ Layout plan(const sd_config& c) {
     L.x = take((size_t)L.Tmax * D.d * 4);
     L.h = take((size_t)L.Tmax * D.d * es);
     L.ffn = take((size_t)L.Tmax * D.F * es);
-    L.qkv = take((size_t)L.Tmax * D.nqkv() * 4);
     L.qbuf = take((size_t)L.Tmax * D.nq() * es);
     L.attn = take((size_t)L.Tmax * D.nq() * es);
     const size_t nparts = D.bf16 ? (size_t)L.max_items * L.rows_max : 1;
@@ -376,96 +375,90 @@ struct ProfScope {
 sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t st) {
     const Dims& D = c->D;
     const SlotBufs& sb = s.bufs;
+    const int T = bv.T;
     {
         ProfScope ps(c, SD_K_SMALL, st);
         launch_prepare(D, bv, sb, st);
-        launch_embed(D, bv, c->w.embed, sb, st);
+        // x = E[tok]; h = RMSNorm(x) with the first layer's pre-attention gain
+        launch_embed_norm(D, bv, c->w.embed, c->layers[0].norm1, sb, st);
     }
-    const int T = bv.T;
     for (int l = 0; l < D.L; ++l) {
         const sd_layer_weights& w = c->layers[l];
-        {
-            ProfScope ps(c, SD_K_SMALL, st);
-            launch_rmsnorm(D, T, sb.x, w.norm1, sb.h, st);
-        }
-        GemmCall g{};
         const size_t lbase = (size_t)l * c->pl.layer * 2;
-        g.X = sb.h;
-        g.Wp = c->wpack + lbase + c->pl.qkv * 2;
-        g.W[0] = w.wq; g.W[1] = w.wk; g.W[2] = w.wv;
-        g.seg[0] = 0; g.seg[1] = D.nq(); g.seg[2] = D.nq() + D.nkv();
-        g.nseg = 3;
-        g.N = D.nqkv();
-        g.K = D.d;
-        g.T = T;
-        g.epi = EPI_STORE;
-        g.out = sb.qkv;
-        g.ldo = D.nqkv();
         {
+            // QKV projection (split-K partials), then their reduction fused
+            // with QK-norm, RoPE, the query store and the KV append
             ProfScope ps(c, SD_K_QKV, st);
-            launch_gemm(D, g, sb, st);
-        }
-        {
-            ProfScope ps(c, SD_K_SMALL, st);
-            launch_qkrope(D, bv, sb, c->kv, l, w.qnorm, w.knorm, st);
+            GemmCall g{};
+            g.X = sb.h;
+            g.Wp = c->wpack + lbase + c->pl.qkv * 2;
+            g.W[0] = w.wq; g.W[1] = w.wk; g.W[2] = w.wv;
+            g.seg[0] = 0; g.seg[1] = D.nq(); g.seg[2] = D.nq() + D.nkv();
+            g.nseg = 3;
+            g.N = D.nqkv();
+            g.K = D.d;
+            g.T = T;
+            g.epi = EPI_STORE;
+            g.raw = 1;
+            const int S = launch_gemm(D, g, sb, st);
+            launch_qkv_finish(D, bv, sb, c->kv, l, sb.gpart, S, w.qnorm, w.knorm, st);
         }
         {
             ProfScope ps(c, SD_K_ATTN, st);
             launch_attention(D, bv, sb, c->kv, l, st);
         }
-        GemmCall o{};
-        o.X = sb.attn;
-        o.Wp = c->wpack + lbase + c->pl.o * 2;
-        o.W[0] = w.wo;
-        o.nseg = 1;
-        o.N = D.d;
-        o.K = D.nq();
-        o.T = T;
-        o.epi = EPI_RESID;
-        o.out = sb.x;
-        o.ldo = D.d;
         {
+            // output projection, then residual add fused with the pre-FFN norm
             ProfScope ps(c, SD_K_O, st);
-            launch_gemm(D, o, sb, st);
+            GemmCall o{};
+            o.X = sb.attn;
+            o.Wp = c->wpack + lbase + c->pl.o * 2;
+            o.W[0] = w.wo;
+            o.nseg = 1;
+            o.N = D.d;
+            o.K = D.nq();
+            o.T = T;
+            o.epi = EPI_STORE;
+            o.raw = 1;
+            const int S = launch_gemm(D, o, sb, st);
+            launch_resid_norm(D, T, sb.gpart, S, sb.x, w.norm2, sb.h, st);
         }
-        {
-            ProfScope ps(c, SD_K_SMALL, st);
-            launch_rmsnorm(D, T, sb.x, w.norm2, sb.h, st);
-        }
-        GemmCall gu{};
-        gu.X = sb.h;
-        gu.Wp = c->wpack + lbase + c->pl.gu * 2;
-        gu.W[0] = w.wg; gu.W[1] = w.wu;
-        gu.nseg = 2;
-        gu.seg[1] = D.F;
-        gu.N = D.F;
-        gu.K = D.d;
-        gu.T = T;
-        gu.epi = EPI_SWIGLU;
-        gu.out = sb.ffn;
-        gu.ldo = D.F;
         {
             ProfScope ps(c, SD_K_GATEUP, st);
+            GemmCall gu{};
+            gu.X = sb.h;
+            gu.Wp = c->wpack + lbase + c->pl.gu * 2;
+            gu.W[0] = w.wg; gu.W[1] = w.wu;
+            gu.nseg = 2;
+            gu.seg[1] = D.F;
+            gu.N = D.F;
+            gu.K = D.d;
+            gu.T = T;
+            gu.epi = EPI_SWIGLU;
+            gu.out = sb.ffn;
+            gu.ldo = D.F;
             launch_gemm(D, gu, sb, st);
         }
-        GemmCall dn{};
-        dn.X = sb.ffn;
-        dn.Wp = c->wpack + lbase + c->pl.down * 2;
-        dn.W[0] = w.wd;
-        dn.nseg = 1;
-        dn.N = D.d;
-        dn.K = D.F;
-        dn.T = T;
-        dn.epi = EPI_RESID;
-        dn.out = sb.x;
-        dn.ldo = D.d;
         {
+            // down projection, then residual add fused with the next norm
+            // (next layer's pre-attention gain, or the final norm)
             ProfScope ps(c, SD_K_DOWN, st);
-            launch_gemm(D, dn, sb, st);
+            GemmCall dn{};
+            dn.X = sb.ffn;
+            dn.Wp = c->wpack + lbase + c->pl.down * 2;
+            dn.W[0] = w.wd;
+            dn.nseg = 1;
+            dn.N = D.d;
+            dn.K = D.F;
+            dn.T = T;
+            dn.epi = EPI_STORE;
+            dn.raw = 1;
+            const int S = launch_gemm(D, dn, sb, st);
+            const void* gnext = l + 1 < D.L ? c->layers[l + 1].norm1 : c->w.norm_f;
+            launch_resid_norm(D, T, sb.gpart, S, sb.x, gnext, sb.h, st);
         }
     }
     ProfScope ps_lm(c, SD_K_LMHEAD, st);
-    launch_rmsnorm(D, T, sb.x, c->w.norm_f, sb.h, st);
     GemmCall lm{};
     lm.X = sb.h;
     lm.Wp = c->wpack + c->pl.lm * 2;
@@ -571,7 +564,6 @@ sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_poo
         b.x = (float*)(s.base + L.x);
         b.h = s.base + L.h;
         b.ffn = s.base + L.ffn;
-        b.qkv = (float*)(s.base + L.qkv);
         b.qbuf = s.base + L.qbuf;
         b.attn = s.base + L.attn;
         b.apart = (float*)(s.base + L.apart);

@@ -69,7 +69,6 @@ struct SlotBufs {
     float* x;         // [Tmax][d]
     void* h;          // [Tmax][d] normed GEMM input (act type)
     void* ffn;        // [Tmax][F] SwiGLU output (act type)
-    float* qkv;       // [Tmax][nqkv]
     void* qbuf;       // [Tmax][nq] act type
     void* attn;       // [Tmax][nq] act type
     float* apart;     // [max_items][rows_max][hd] attention chunk partials
@@ -90,12 +89,6 @@ struct SlotBufs {
 
 // ---- launchers (all enqueue on `s`, no synchronisation) ----
 void launch_prepare(const Dims& D, const BatchView& bv, const SlotBufs& sb, hipStream_t s);
-void launch_embed(const Dims& D, const BatchView& bv, const void* embed, const SlotBufs& sb,
-                  hipStream_t s);
-void launch_rmsnorm(const Dims& D, int T, const float* x, const void* gamma, void* out,
-                    hipStream_t s);
-void launch_qkrope(const Dims& D, const BatchView& bv, const SlotBufs& sb, const KVPool& kv,
-                   int layer, const void* qn, const void* kn, hipStream_t s);
 void launch_attention(const Dims& D, const BatchView& bv, const SlotBufs& sb, const KVPool& kv,
                       int layer, hipStream_t s);
 
@@ -111,8 +104,21 @@ struct GemmCall {
     int epi;
     void* out;        // EPI_STORE: float [T][ldo]; EPI_RESID: float x [T][ldo]; SWIGLU: act [T][ldo]
     int ldo;
+    int raw;          // 1: write split-K partial planes [S][T][N] to the slot's
+                      //    partial buffer and leave the reduction to the consumer
 };
-void launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_t s);
+// Returns the number of partial planes S (raw mode), else the splits used.
+int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_t s);
+// x[t] += sum_s part[s][t] (split order); h[t] = RMSNorm(x[t]) * gamma
+void launch_resid_norm(const Dims& D, int T, const float* part, int S, float* x,
+                       const void* gamma, void* h, hipStream_t s);
+// embedding gather into x and h = RMSNorm(x) * gamma
+void launch_embed_norm(const Dims& D, const BatchView& bv, const void* embed, const void* gamma,
+                       const SlotBufs& sb, hipStream_t s);
+// QKV partial reduction fused with QK-norm, RoPE, query store and KV append
+void launch_qkv_finish(const Dims& D, const BatchView& bv, const SlotBufs& sb, const KVPool& kv,
+                       int layer, const float* part, int S, const void* qn, const void* kn,
+                       hipStream_t s);
 size_t gemm_partial_floats(const Dims& D, int Tmax);
 void launch_pack(const void* s0, const void* s1, const void* s2, int seg1, int seg2, int mode,
                  int K, int vrows, void* dst, hipStream_t s);
