@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--cpu-layers", type=int, default=16,
                     help="decoder layers the CPU-baseline sample runs (extrapolated to all)")
     ap.add_argument("--breakdown", action="store_true", help="time every kernel class")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run a plain 1 GiB device copy (scale reference for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -63,6 +65,14 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     sv.lib()  # fails loudly if the HIP library is not built
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("copy calibration: 3 x 1 GiB device-to-device copies done")
+        del src, dst
 
     w = wl.workload(args.workload)
     m = w.model
@@ -153,9 +163,11 @@ def main():
     pair_ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
     gu_avg_s = max(gu_ms / max(gu_n, 1) - pair_ms, 1e-6) / 1e3
     achieved = gu_bytes / gu_avg_s / 1e9
+    traffic = measured_traffic(args.workload)
     roofline = {"bound": "hbm", "kernel": "k_gemm_bf16 (gate/up + SwiGLU epilogue)",
                 "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "traffic_over_algorithmic": round(traffic / gu_bytes, 4) if traffic else None,
                 "bytes_per_launch": gu_bytes, "avg_launch_us": round(gu_avg_s * 1e6, 2),
                 "launches": gu_n, "event_pair_us_subtracted": round(pair_ms * 1e3, 2),
                 "mfma_tflops": round(2.0 * T * 2 * m.d_ffn * m.d_model / gu_avg_s / 1e12, 1),
@@ -204,6 +216,26 @@ def main():
         result["cpu_baseline"] = cpu_baseline(w, batches[0], args.cpu_layers, acc_step / verified_step)
     v.close()
     print(json.dumps(result), flush=True)
+
+
+def measured_traffic(workload):
+    """HBM bytes per gate/up launch from the committed FETCH_SIZE/WRITE_SIZE
+    summary, or None when it covers another workload or the GEMM source has
+    changed since the counters were taken."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", f"k_gemm_gateup_{workload}_hbm_traffic.md")
+    src = os.path.join(ROOT, "paper_2604_20919_amd", "csrc", "k_gemm.hip")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"traffic_bytes_per_launch: (\d+)", text)
+    h = re.search(r"k_gemm.hip sha256: ([0-9a-f]{64})", text)
+    if not (m and h):
+        return None
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != h.group(1):
+        return None
+    return int(m.group(1))
 
 
 def plant_greedy_drafts(v, w, batches, dev_in, torch):

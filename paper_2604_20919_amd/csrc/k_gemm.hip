@@ -61,15 +61,17 @@ __device__ __forceinline__ void swiglu_store4(const GemmP& p, int t, int col, f3
     *(uint2*)o = pk;
 }
 
-template <int MT, int NSUB, int KC, int EPI, bool SPLIT, int PD = 2>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2)))
+template <int MT, int NSUB, int KC, int EPI, bool SPLIT, int NW = 4, int PD = 2>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, 2)))
 void k_gemm_bf16(GemmP p) {
-    constexpr int NT = 4 * NSUB * 16;  // virtual columns per tile
-    constexpr int KS = KC / 32;        // MFMA k-steps per chunk
-    constexpr int LDX = KC + 8;        // padded LDS row (bf16 elements)
-    constexpr int PPR = KC / 8;        // 16-byte pieces per staged row
-    constexpr int XPT = (MT * 16 * PPR) / 256;  // X pieces per thread
-    static_assert((MT * 16 * PPR) % 256 == 0, "X chunk must split evenly over 256 threads");
+    constexpr int NTH = 64 * NW;         // threads per workgroup
+    constexpr int NT = NW * NSUB * 16;   // virtual columns per tile
+    constexpr int KS = KC / 32;          // MFMA k-steps per chunk
+    constexpr int LDX = KC + 8;          // padded LDS row (bf16 elements)
+    constexpr int PPR = KC / 8;          // 16-byte pieces per staged row
+    constexpr int NPC = MT * 16 * PPR;   // pieces per staged chunk
+    constexpr int XPT = (NPC + NTH - 1) / NTH;  // X pieces per thread
+    constexpr bool XEVEN = NPC % NTH == 0;
     static_assert(EPI != EPI_SWIGLU || NSUB % 2 == 0, "SwiGLU pairs gate/up sub-tiles");
     __shared__ __attribute__((aligned(16))) bf16_t xs[2][MT * 16 * LDX];
 
@@ -88,7 +90,7 @@ void k_gemm_bf16(GemmP p) {
     uint32_t woff[NSUB];
 #pragma unroll
     for (int s = 0; s < NSUB; ++s) {
-        const uint32_t vs = (uint32_t)((tile * 4 + wv) * NSUB + s);  // 16-row group
+        const uint32_t vs = (uint32_t)((tile * NW + wv) * NSUB + s);  // 16-row group
         woff[s] = vs * (uint32_t)p.KT * 1024u + (uint32_t)lane * 16u;
     }
     const __amdgpu_buffer_rsrc_t xres =
@@ -119,7 +121,7 @@ void k_gemm_bf16(GemmP p) {
     uint32_t xoff[XPT];
 #pragma unroll
     for (int i = 0; i < XPT; ++i) {
-        const int idx = threadIdx.x + i * 256;
+        const int idx = min((int)threadIdx.x + i * NTH, NPC - 1);
         const int r = min(idx / PPR, p.T - 1), cc = idx % PPR;
         xoff[i] = ((uint32_t)r * (uint32_t)p.K + (uint32_t)cc * 8u) * 2u;
     }
@@ -132,8 +134,8 @@ void k_gemm_bf16(GemmP p) {
     auto store_x = [&](const uint4 (&x)[XPT], int buf) {
 #pragma unroll
         for (int i = 0; i < XPT; ++i) {
-            const int idx = threadIdx.x + i * 256;
-            *(uint4*)(&xs[buf][(idx / PPR) * LDX + (idx % PPR) * 8]) = x[i];
+            const int idx = threadIdx.x + i * NTH;
+            if (XEVEN || idx < NPC) *(uint4*)(&xs[buf][(idx / PPR) * LDX + (idx % PPR) * 8]) = x[i];
         }
     };
     auto load_w = [&](bf16x8 (&w)[KS][NSUB], int c) {
@@ -199,7 +201,7 @@ void k_gemm_bf16(GemmP p) {
             // groups 2j / 2j+1 hold gate / up rows 16j..16j+15
 #pragma unroll
             for (int s = 0; s < NSUB; s += 2)
-                swiglu_store4(p, t, ((tile * 4 + wave) * NSUB + s) / 2 * 16 + 4 * lg, acc[s][m],
+                swiglu_store4(p, t, ((tile * NW + wave) * NSUB + s) / 2 * 16 + 4 * lg, acc[s][m],
                               acc[s + 1][m]);
         } else {
 #pragma unroll
@@ -313,48 +315,60 @@ __global__ void k_gemm_f32(GemmF p) {
 // ---------------------------------------------------------------------------
 
 // Tile shape per slot-count class: MT slot tiles of 16, NSUB weight
-// sub-tiles of 16 rows per wave, KC k elements per pipeline chunk.
-struct GemmShape { int MT, NSUB, KC; };
+// sub-tiles of 16 rows per wave, KC k elements per pipeline chunk, NW waves
+// per workgroup.  Eight waves share one staged X chunk where the row count
+// allows (it halves the X staging per weight byte; measured 96 vs 107 us
+// for the 32B gate/up at T = 80); more than 16 slot tiles need the larger
+// register budget of one wave per SIMD, so they use four.
+struct GemmShape { int MT, NSUB, KC, NW; };
 
-static GemmShape shape_for(int T, int epi) {
-    (void)epi;
+static GemmShape shape_for(int T, int vcols) {
     const int mt = (T + 15) / 16;
-    if (mt <= 2) return {2, 2, 64};
-    if (mt <= 4) return {4, 2, 64};
-    if (mt <= 6) return {6, 2, 64};
-    if (mt <= 8) return {8, 2, 64};
-    if (mt <= 12) return {12, 2, 64};
-    if (mt <= 16) return {16, 2, 64};
-    if (mt <= 20) return {20, 2, 64};
-    if (mt <= 26) return {26, 2, 64};
-    return {0, 0, 0};
+    static const int classes[] = {2, 4, 6, 8, 12, 16, 20, 26};
+    for (int c : classes)
+        if (mt <= c) {
+            const int nw = (c <= 16 && vcols % (16 * 2 * 8) == 0) ? 8 : 4;
+            return {c, 2, 64, nw};
+        }
+    return {0, 0, 0, 0};
 }
 
 typedef void (*GemmFn)(GemmP);
 typedef void (*ReduceFn)(GemmP);
 
-template <int MT, int NSUB, int KC, bool SPLIT>
+// split-K kernels write raw partial planes; the epilogue runs in the reducer
+template <int MT, int NW, bool SPLIT>
 static GemmFn pick_epi(int epi) {
+    if (SPLIT) return k_gemm_bf16<MT, 2, 64, EPI_STORE, true, NW>;
     switch (epi) {
-        case EPI_RESID: return k_gemm_bf16<MT, NSUB, KC, EPI_RESID, SPLIT>;
-        case EPI_SWIGLU:
-            if constexpr (NSUB % 2 == 0) return k_gemm_bf16<MT, NSUB, KC, EPI_SWIGLU, SPLIT>;
-            return nullptr;
-        default: return k_gemm_bf16<MT, NSUB, KC, EPI_STORE, SPLIT>;
+        case EPI_RESID: return k_gemm_bf16<MT, 2, 64, EPI_RESID, false, NW>;
+        case EPI_SWIGLU: return k_gemm_bf16<MT, 2, 64, EPI_SWIGLU, false, NW>;
+        default: return k_gemm_bf16<MT, 2, 64, EPI_STORE, false, NW>;
     }
 }
 
 template <bool SPLIT>
 static GemmFn pick(const GemmShape& sh, int epi) {
+    if (sh.NW == 8) {
+        switch (sh.MT) {
+            case 2: return pick_epi<2, 8, SPLIT>(epi);
+            case 4: return pick_epi<4, 8, SPLIT>(epi);
+            case 6: return pick_epi<6, 8, SPLIT>(epi);
+            case 8: return pick_epi<8, 8, SPLIT>(epi);
+            case 12: return pick_epi<12, 8, SPLIT>(epi);
+            case 16: return pick_epi<16, 8, SPLIT>(epi);
+        }
+        return nullptr;
+    }
     switch (sh.MT) {
-        case 2: return pick_epi<2, 2, 64, SPLIT>(epi);
-        case 4: return pick_epi<4, 2, 64, SPLIT>(epi);
-        case 6: return pick_epi<6, 2, 64, SPLIT>(epi);
-        case 8: return pick_epi<8, 2, 64, SPLIT>(epi);
-        case 12: return pick_epi<12, 2, 64, SPLIT>(epi);
-        case 16: return pick_epi<16, 2, 64, SPLIT>(epi);
-        case 20: return pick_epi<20, 2, 64, SPLIT>(epi);
-        case 26: return pick_epi<26, 2, 64, SPLIT>(epi);
+        case 2: return pick_epi<2, 4, SPLIT>(epi);
+        case 4: return pick_epi<4, 4, SPLIT>(epi);
+        case 6: return pick_epi<6, 4, SPLIT>(epi);
+        case 8: return pick_epi<8, 4, SPLIT>(epi);
+        case 12: return pick_epi<12, 4, SPLIT>(epi);
+        case 16: return pick_epi<16, 4, SPLIT>(epi);
+        case 20: return pick_epi<20, 4, SPLIT>(epi);
+        case 26: return pick_epi<26, 4, SPLIT>(epi);
     }
     return nullptr;
 }
@@ -378,10 +392,21 @@ static int cu_count() {
     return n;
 }
 
-// k splits (a divisor of kchunks): the largest count giving 1.25 to 1.75
-// workgroups per CU, else the smallest giving at least 1.25 (measured on
-// the 32B shapes: fewer leave CUs idle, more add partial traffic)
-static int choose_splits(int tiles, int kchunks) {
+// k splits (a divisor of kchunks).  Four-wave tiles: the largest count
+// giving 1.25 to 1.75 workgroups per CU, else the smallest giving at least
+// 1.25.  Eight-wave tiles: the largest count keeping the grid within 0.8
+// workgroups per CU (measured on the 32B shapes at T = 80: QKV 40 tiles x 5,
+// O 20 x 8, down 20 x 10; larger grids lose more to partial-sum traffic and
+// co-resident workgroups than they gain in parallelism).
+static int choose_splits(int tiles, int kchunks, int nw) {
+    if (nw == 8) {
+        const int hi = cu_count() * 4 / 5;
+        if (tiles >= hi / 2) return 1;
+        int best = 1;
+        for (int s = 2; s <= kchunks; ++s)
+            if (kchunks % s == 0 && tiles * s <= hi) best = s;
+        return best;
+    }
     const int lo = cu_count() * 5 / 4, hi = cu_count() * 7 / 4;
     if (tiles >= lo) return 1;
     int best = 0;
@@ -406,10 +431,10 @@ int gemm_counter_count(const Dims&) { return 1; }
 
 bool gemm_shape_ok(const Dims& D, int T, int K, int N, int epi) {
     if (!D.bf16) return true;
-    const GemmShape sh = shape_for(T, epi);
-    if (sh.MT == 0) return false;
     const int vcols = epi == EPI_SWIGLU ? 2 * N : N;
-    return K % sh.KC == 0 && vcols % (64 * sh.NSUB) == 0;
+    const GemmShape sh = shape_for(T, vcols);
+    if (sh.MT == 0) return false;
+    return K % sh.KC == 0 && vcols % (16 * sh.NW * sh.NSUB) == 0;
 }
 
 int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_t s) {
@@ -431,8 +456,9 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
         hipLaunchKernelGGL(k_gemm_f32, dim3((n + 255) / 256), dim3(256), 0, s, p);
         return 1;
     }
-    const GemmShape sh = shape_for(g.T, g.epi);
-    const int nt = 64 * sh.NSUB;
+    const int vcols = g.epi == EPI_SWIGLU ? 2 * g.N : g.N;
+    const GemmShape sh = shape_for(g.T, vcols);
+    const int nt = 16 * sh.NW * sh.NSUB;
     GemmP p;
     p.X = (const bf16_t*)g.X;
     p.Wp = (const bf16_t*)g.Wp;
@@ -440,9 +466,9 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
     p.KT = g.K / 32;
     p.T = g.T;
     p.kchunks = g.K / sh.KC;
-    p.vcols = g.epi == EPI_SWIGLU ? 2 * g.N : g.N;
+    p.vcols = vcols;
     p.tiles = p.vcols / nt;
-    int S = choose_splits(p.tiles, p.kchunks);
+    int S = choose_splits(p.tiles, p.kchunks, sh.NW);
     while (S > 1 && (size_t)S * g.T * p.vcols > sb.gpart_floats) {
         int t = S - 1;
         while (t > 1 && p.kchunks % t) --t;
@@ -454,11 +480,11 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
     p.ldo = g.ldo;
     if (g.raw) {
         // S partial planes [S][T][N] for a fused consumer to reduce
-        hipLaunchKernelGGL(pick<true>(sh, EPI_STORE), dim3(p.tiles * S), dim3(256), 0, s, p);
+        hipLaunchKernelGGL(pick<true>(sh, EPI_STORE), dim3(p.tiles * S), dim3(64 * sh.NW), 0, s, p);
     } else if (S == 1) {
-        hipLaunchKernelGGL(pick<false>(sh, g.epi), dim3(p.tiles), dim3(256), 0, s, p);
+        hipLaunchKernelGGL(pick<false>(sh, g.epi), dim3(p.tiles), dim3(64 * sh.NW), 0, s, p);
     } else {
-        hipLaunchKernelGGL(pick<true>(sh, g.epi), dim3(p.tiles * S), dim3(256), 0, s, p);
+        hipLaunchKernelGGL(pick<true>(sh, g.epi), dim3(p.tiles * S), dim3(64 * sh.NW), 0, s, p);
         const int ncols = g.epi == EPI_SWIGLU ? p.vcols / 2 : p.vcols;
         const int n = g.T * (ncols / 4);
         hipLaunchKernelGGL(pick_reduce(g.epi), dim3((n + 255) / 256), dim3(256), 0, s, p);
