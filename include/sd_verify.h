@@ -129,8 +129,11 @@ sd_status sd_verify_query_sizes(const sd_config* cfg, uint64_t* kv_pool_bytes,
  *   read in place until destroy.  With SD_F32 every pointer is kept.
  * kv_pool / workspace / weight_pack: device buffers of at least the queried
  *   sizes, 256-byte aligned, owned by the caller, kept until destroy
- *   (weight_pack may be NULL when its size is 0).  Initialisation work runs on
- *   the null stream and is synchronised before returning.
+ *   (weight_pack may be NULL when its size is 0).  The KV pool is zero-filled
+ *   here (attention reads whole blocks past a context's end and needs those
+ *   rows finite); KV contents written later must be finite too.
+ *   Initialisation work runs on the null stream and is synchronised before
+ *   returning.
  * out: receives the context.  Errors: SD_EINVAL (cfg, NULL pointer),
  * SD_ENODEV (current device is not gfx950), SD_EHIP. */
 sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_pool,

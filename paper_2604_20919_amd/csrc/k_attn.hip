@@ -8,8 +8,10 @@
 // bf16 path (MFMA).  A workgroup takes one work item (b, g, context chunk);
 // the host sizes chunks so that a batch has about 512 items of equal length.
 // The chunk is streamed in 32-token blocks (two KV pages, 16 KB of K and V)
-// through double-buffered LDS; the blocks are written to LDS in MFMA
-// fragment order, so every operand read is one contiguous 1 KB wave read.
+// with direct global-to-LDS loads into a ring of LDS buffers, so several
+// blocks per workgroup are in flight without staging registers.  Each lane
+// gathers the piece that belongs to its LDS slot, which leaves the block in
+// MFMA fragment order: every operand read is one contiguous 1 KB wave read.
 // Wave w owns query-row tiles w, w+4, ... (16 rows each) and, per block:
 //   S^T = K Q^T   K rows as the A operand (16 tokens x 32 dims), in the token
 //                 order (0-3, 8-11, 16-19, 24-27 | 4-7, 12-15, 20-23, 28-31)
@@ -41,69 +43,120 @@ struct AttnP {
 constexpr int HD = 128;
 constexpr int RT_MAX = 2;  // row tiles per wave and pass
 
-// LDS fragment index of K element (token t of the block, 16-byte dim piece j)
-__device__ __forceinline__ int k_frag_slot(int t, int j) {
-    const int tt = (t >> 2) & 1, lr = 4 * (t >> 3) + (t & 3);
-    const int ds = j >> 2, lg = j & 3;
-    return (tt * 4 + ds) * 64 + lr + 16 * lg;
+// Gather map of the direct-to-LDS block loads.  A block is 32 tokens (two
+// pages) of K and V for one KV head, 16 KB, held in LDS as 1024 16-byte
+// slots in MFMA fragment order: K slots 0..511, V^T slots 512..1023.  Slot
+// s is filled by thread s % 256 of load instruction s / 256, and since a
+// wave's direct load writes its 64 lanes to 64 consecutive slots, each lane
+// gathers the global piece that belongs to its slot:
+//   K slot s: fragment q = s/64 (token half tt = q/4, dim step ds = q%4),
+//     lane r = s%64 (lr = r%16, lg = r/16) holds token
+//     t = 8*(lr/4) + 4*tt + lr%4 of the block, dims 32*ds + 8*lg .. +7;
+//     this token order makes each lane of S^T = K Q^T end up with 8
+//     consecutive tokens of one query row (the B layout of O^T += V^T P^T);
+//   V slot s: dim tile dt = s/64, r = s%64: dim 16*dt + r%16, tokens
+//     8*(r/16 % 2) .. +7 of page r/32 (V pages are dim-major, so this is
+//     16 contiguous bytes).
+// Returns the page (0/1) of the block and the byte offset inside that
+// page's K or V block.
+__device__ __forceinline__ void k_slot_src(int s, int& pg, int& off) {
+    const int q = s >> 6, r = s & 63;
+    const int tt = q >> 2, ds = q & 3, lr = r & 15, lg = r >> 4;
+    const int t = 8 * (lr >> 2) + 4 * tt + (lr & 3);
+    pg = t >> 4;
+    off = ((t & 15) * HD + 32 * ds + 8 * lg) * 2;
 }
-// LDS fragment index of V^T piece (dim d, tokens 8h..8h+7 of page pg)
-__device__ __forceinline__ int v_frag_slot(int d, int pg, int h) {
-    return (d >> 4) * 64 + (d & 15) + 16 * (pg * 2 + h);
+__device__ __forceinline__ void v_slot_src(int s, int& pg, int& off) {
+    const int dt = s >> 6, r = s & 63;
+    const int d = 16 * dt + (r & 15), x = r >> 4;
+    pg = x >> 1;
+    off = (d * kPageTokens + 8 * (x & 1)) * 2;
 }
 
-__global__ __launch_bounds__(256) void k_attn_bf16(AttnP p) {
-    __shared__ __attribute__((aligned(16))) uint4 kvs[2][1024];  // [buf][K 512 | V 512] x 16 B
+typedef __attribute__((address_space(4))) const int32_t cint32_t;
+
+// s_waitcnt immediate for "vector memory counter <= N" (LGK counter <= 0
+// when LGK0, else free)
+template <int N, bool LGK0 = false>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | ((LGK0 ? 0 : 15) << 8));
+}
+
+// Reductions over the four lanes l, l^16, l^32, l^48 that hold one query
+// row: each cross-lane swap returns the row halves exchanged between its two
+// operands, so combining both results with the own value pairs every lane
+// with its partner 16 (then 32) lanes away.
+__device__ __forceinline__ float row_max4(float v) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float row_sum4(float v) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// Workgroup barrier without the memory fence of __syncthreads(): the fence
+// would wait for every outstanding load, including the direct-to-LDS loads
+// of later blocks that are meant to stay in flight.  Callers wait for what
+// must be complete themselves; the empty asm statements keep the compiler
+// from moving memory accesses across the barrier.
+__device__ __forceinline__ void barrier_nofence() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+template <int NBUF>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_attn_bf16(AttnP p) {
+    constexpr int PD = NBUF - 1;  // blocks in flight
+    __shared__ __attribute__((aligned(16))) uint4 kvs[NBUF][1024];
+    // The batch metadata is read-only while the kernel runs: reading it
+    // through the constant address space gives scalar loads, which keep the
+    // vector memory counter (waited on below) free of anything but KV.
+    const cint32_t* items = (const cint32_t*)p.bv.items;
     const int item = blockIdx.x;
-    const int4 it = p.bv.items[item];
-    const int b = it.x, g = it.y, c0 = it.z, c1 = it.w;
+    const int b = items[4 * item + 0], g = items[4 * item + 1];
+    const int c0 = items[4 * item + 2], c1 = items[4 * item + 3];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int lr = lane & 15, lg = lane >> 4;
     const int G = p.G;
-    const int R = (p.bv.L[b] + 1) * G;
-    const int prefix = p.bv.prefix[b];
-    const int tbase = p.bv.slot_off[b];
-    const int32_t* pt = p.bv.page_table + (size_t)b * p.bv.max_pages;
+    const int R = (((const cint32_t*)p.bv.L)[b] + 1) * G;
+    const int prefix = ((const cint32_t*)p.bv.prefix)[b];
+    const int tbase = ((const cint32_t*)p.bv.slot_off)[b];
+    const cint32_t* pt = (const cint32_t*)p.bv.page_table + (size_t)b * p.bv.max_pages;
     const char* kvb = (const char*)p.kv.base;
     const int nblk = (c1 - c0 + 31) >> 5;
 
-    // staging: thread i moves K piece (token i/16, dims 8*(i%16)) and V^T
-    // piece (dim i/2, tokens 8*(i%2)) of both pages of the block
-    const int tid = threadIdx.x;
-    const int kt = tid >> 4, kj = tid & 15;   // K: token 0..15 of a page, piece
-    const int vd = tid >> 1, vh = tid & 1;    // V: dim 0..127, token half
-    uint4 st[4];
-    auto load_blk = [&](int blk) {
+    // this thread's four gather sources (page of the block, byte offset)
+    int kpg0, koff0, kpg1, koff1, vpg0, voff0, vpg1, voff1;
+    k_slot_src(threadIdx.x, kpg0, koff0);
+    k_slot_src(256 + threadIdx.x, kpg1, koff1);
+    v_slot_src(threadIdx.x, vpg0, voff0);
+    v_slot_src(256 + threadIdx.x, vpg1, voff1);
+    const size_t kstride = p.kv.v_off(0, 0, 0) - p.kv.k_off(0, 0, 0);  // K block -> V block
+    // Requests block blk into LDS buffer buf: four 16-byte direct loads per
+    // thread.  Tokens past the chunk end are read from the chunk's last page
+    // (the page index is clamped); their scores are masked, and V there is
+    // finite (pool zeroed at init, later only model values), so p = 0
+    // contributes exactly 0.
+    auto issue = [&](int blk, int buf) {
         const int t0 = c0 + blk * 32;
-#pragma unroll
-        for (int pg = 0; pg < 2; ++pg) {
-            // clamp to the last valid token: masked tokens only need finite data
-            const int tok = min(t0 + pg * 16, c1 - 1);
-            const int page = pt[tok >> 4];
-            const char* kp = kvb + (p.kv.k_off(p.layer, page, g) * 2);
-            const char* vp = kvb + (p.kv.v_off(p.layer, page, g) * 2);
-            st[pg * 2 + 0] = *(const uint4*)(kp + (kt * HD + kj * 8) * 2);
-            uint4 v = *(const uint4*)(vp + (vd * kPageTokens + vh * 8) * 2);
-            // value slots past the chunk end may hold stale bits (even NaN):
-            // zero them so that p = 0 times v stays 0 (masked keys are
-            // handled by the score mask)
-            const int vt = t0 + pg * 16 + vh * 8;  // token of element 0
-            uint32_t* w = (uint32_t*)&v;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const uint32_t lo = vt + 2 * e < c1 ? 0x0000ffffu : 0u;
-                const uint32_t hi = vt + 2 * e + 1 < c1 ? 0xffff0000u : 0u;
-                w[e] &= lo | hi;
-            }
-            st[pg * 2 + 1] = v;
-        }
-    };
-    auto store_blk = [&](int buf) {
-#pragma unroll
-        for (int pg = 0; pg < 2; ++pg) {
-            kvs[buf][k_frag_slot(pg * 16 + kt, kj)] = st[pg * 2 + 0];
-            kvs[buf][512 + v_frag_slot(vd, pg, vh)] = st[pg * 2 + 1];
-        }
+        const int page0 = pt[min(t0, c1 - 1) >> 4];
+        const int page1 = pt[min(t0 + 16, c1 - 1) >> 4];
+        const char* k0 = kvb + p.kv.k_off(p.layer, page0, g) * 2;
+        const char* k1 = kvb + p.kv.k_off(p.layer, page1, g) * 2;
+        uint4* dst = &kvs[buf][wave * 64];
+        __builtin_amdgcn_global_load_lds((const void*)((kpg0 ? k1 : k0) + koff0), (void*)dst, 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((const void*)((kpg1 ? k1 : k0) + koff1), (void*)(dst + 256), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((const void*)((vpg0 ? k1 : k0) + kstride * 2 + voff0),
+                                         (void*)(dst + 512), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((const void*)((vpg1 ? k1 : k0) + kstride * 2 + voff1),
+                                         (void*)(dst + 768), 16, 0, 0);
     };
 
     const int ntiles = (R + 15) >> 4;
@@ -130,89 +183,110 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnP p) {
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt) o[i][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
+        // the query loads must not be counted by the block waits below
+        wait_vm<0>();
 
+        // One 32-token block for this wave's row tiles.  Scores stay in the
+        // raw (unscaled) domain until the exponent, which folds the scale in:
+        // p = 2^(s*c - m*c) with c = log2(e)/sqrt(hd).  Blocks that every
+        // row sees completely skip the causal/chunk mask; the running output
+        // is rescaled only when some row's maximum grew; the row sum stays
+        // per lane until the end of the chunk.
         auto compute = [&](int buf, int blk) {
             const int t0 = c0 + blk * 32;
+            const bool full = t0 + 32 <= c1 && t0 + 31 <= prefix;
             const uint4* kb = kvs[buf];
             const uint4* vb = kvs[buf] + 512;
+            bf16x8 kf[8], vf[8];
+#pragma unroll
+            for (int f = 0; f < 8; ++f) kf[f] = __builtin_bit_cast(bf16x8, kb[f * 64 + lane]);
+#pragma unroll
+            for (int f = 0; f < 8; ++f) vf[f] = __builtin_bit_cast(bf16x8, vb[f * 64 + lane]);
 #pragma unroll
             for (int i = 0; i < RT_MAX; ++i) {
                 if (!act[i]) continue;
                 f32x4 sa = f32x4{0.f, 0.f, 0.f, 0.f}, sb = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int ds = 0; ds < 4; ++ds) {
-                    const bf16x8 ka = __builtin_bit_cast(bf16x8, kb[(0 * 4 + ds) * 64 + lane]);
-                    const bf16x8 kk = __builtin_bit_cast(bf16x8, kb[(1 * 4 + ds) * 64 + lane]);
-                    sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[i][ds], sa, 0, 0, 0);
-                    sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qf[i][ds], sb, 0, 0, 0);
+                    sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ds], qf[i][ds], sa, 0, 0, 0);
+                    sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[4 + ds], qf[i][ds], sb, 0, 0, 0);
                 }
                 // lane holds the scores of its query row at tokens t0 + 8*lg + e
                 float sc[8];
-                float bm = -INFINITY;
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int tok = t0 + 8 * lg + e;
-                    const float v = e < 4 ? sa[e] : sb[e - 4];
-                    sc[e] = (tok < c1 && tok <= lim[i]) ? v * p.scale_log2 : -INFINITY;
-                    bm = fmaxf(bm, sc[e]);
+                for (int e = 0; e < 4; ++e) {
+                    sc[e] = sa[e];
+                    sc[4 + e] = sb[e];
                 }
-                bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
-                bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+                if (!full) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int tok = t0 + 8 * lg + e;
+                        sc[e] = (tok < c1 && tok <= lim[i]) ? sc[e] : -INFINITY;
+                    }
+                }
+                float bm = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
+                                 fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
+                bm = row_max4(bm);
                 const float mn = fmaxf(m[i], bm);
                 const bool live = mn != -INFINITY;  // something visible for this row
-                const float alpha = live ? exp2f(m[i] - mn) : 1.f;
+                const float ms = live ? mn * p.scale_log2 : 0.f;
+                const float alpha = live ? __builtin_amdgcn_exp2f((m[i] - mn) * p.scale_log2) : 1.f;
                 float rs = 0.f;
                 bf16x8 pb;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
-                    const float pe = live ? exp2f(sc[e] - mn) : 0.f;
+                    const float pe = __builtin_amdgcn_exp2f(fmaf(sc[e], p.scale_log2, -ms));
                     rs += pe;
                     pb[e] = (__bf16)pe;
                 }
-                rs += __shfl_xor(rs, 16, 64);
-                rs += __shfl_xor(rs, 32, 64);
-                l[i] = l[i] * alpha + rs;
-                m[i] = live ? mn : m[i];
+                l[i] = fmaf(l[i], alpha, rs);
+                m[i] = mn;
+                if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
 #pragma unroll
-                for (int dt = 0; dt < 8; ++dt) {
-                    const bf16x8 vf = __builtin_bit_cast(bf16x8, vb[dt * 64 + lane]);
-                    o[i][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb, o[i][dt] * alpha, 0, 0, 0);
+                    for (int dt = 0; dt < 8; ++dt) o[i][dt] *= alpha;
                 }
+#pragma unroll
+                for (int dt = 0; dt < 8; ++dt)
+                    o[i][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt], pb, o[i][dt], 0, 0, 0);
             }
         };
 
-        // ping-pong over blocks: prefetch block k+1 while computing block k;
-        // the prefetch index is clamped so the loads stay unconditional
+        // Ring pipeline over NBUF LDS buffers.  Iteration k waits for its own
+        // loads of block k (the 4*(PD-1) loads of blocks k+1..k+PD-1 may stay
+        // in flight) and its LDS reads, then a barrier makes every wave's
+        // loads of block k visible and retires every wave's reads of block
+        // k-1, whose buffer then receives block k+PD.  Block indices are clamped so every
+        // iteration issues exactly four loads (the counts above stay exact);
+        // the tail re-reads the last block.
         const int last = nblk - 1;
-        load_blk(0);
-        store_blk(0);
-        __syncthreads();
-        for (int k = 0; k < nblk; k += 2) {
-            load_blk(min(k + 1, last));
-            __builtin_amdgcn_sched_barrier(0);
-            compute(0, k);
-            __builtin_amdgcn_sched_barrier(0);
-            store_blk(1);
-            __syncthreads();
-            if (k + 1 >= nblk) break;
-            load_blk(min(k + 2, last));
-            __builtin_amdgcn_sched_barrier(0);
-            compute(1, k + 1);
-            __builtin_amdgcn_sched_barrier(0);
-            store_blk(0);
-            __syncthreads();
+#pragma unroll
+        for (int u = 0; u < PD; ++u) issue(min(u, last), u);
+        for (int k0 = 0; k0 < nblk; k0 += NBUF) {
+#pragma unroll
+            for (int u = 0; u < NBUF; ++u) {
+                const int k = k0 + u;
+                if (k >= nblk) break;
+                wait_vm<4 * (PD - 1), true>();
+                barrier_nofence();
+                issue(min(k + PD, last), (u + PD) % NBUF);
+                compute(u, k);
+            }
         }
+        // drain the tail loads before the buffers are reused or released
+        wait_vm<0>();
 
         // partial of this item: lane holds O^T[d = dt*16 + 4*lg + r][row lr]
 #pragma unroll
         for (int i = 0; i < RT_MAX; ++i) {
             if (!act[i]) continue;
             const int row = (rp + wave + 4 * i) * 16 + lr;
+            const float lsum = row_sum4(l[i]);  // all lanes take part in the swaps
             if (row >= R) continue;
             const size_t pr = (size_t)item * p.bv.rows_max + row;
             if (lg == 0) {
-                p.aml[pr * 2 + 0] = m[i];
-                p.aml[pr * 2 + 1] = l[i];
+                p.aml[pr * 2 + 0] = m[i] == -INFINITY ? -INFINITY : m[i] * p.scale_log2;
+                p.aml[pr * 2 + 1] = lsum;
             }
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt)
@@ -310,7 +384,7 @@ void launch_attention(const Dims& D, const BatchView& bv, const SlotBufs& sb, co
     p.scale_log2 = 1.4426950408889634f / sqrtf((float)D.hd);
     p.apart = sb.apart;
     p.aml = sb.aml;
-    hipLaunchKernelGGL(k_attn_bf16, dim3(bv.n_items), dim3(256), 0, s, p);
+    hipLaunchKernelGGL(k_attn_bf16<kAttnBuffers>, dim3(bv.n_items), dim3(256), 0, s, p);
     hipLaunchKernelGGL(k_attn_combine<bf16_t>, dim3(blocks), dim3(256), 0, s, bv, sb.apart, sb.aml,
                        (bf16_t*)sb.attn, D.hq, D.hkv, D.hd);
 }

@@ -99,9 +99,9 @@ Layout plan(const sd_config& c) {
     L.Tmax = c.max_batch_tokens;
     L.Bmax = c.max_batch_users;
     L.max_pages = ceil_div(c.max_ctx, kPageTokens);
-    // the chunk length is chosen per batch so that there are at most
-    // kAttnItems + (users * kv heads) work items
-    L.max_items = kAttnItems + L.Bmax * D.hkv;
+    // the chunk lengths are chosen per batch so that there are at most
+    // max(kAttnItemsMax, users * kv heads) work items
+    L.max_items = std::max(kAttnItemsMax, L.Bmax * D.hkv);
     L.rows_max = (c.max_draft + 1) * D.G();
     const size_t es = D.bf16 ? 2 : 4;
     // staging block
@@ -208,6 +208,7 @@ struct sd_ctx {
     Slot slots[kMaxPending];
     int32_t* kvw_host = nullptr;  // pinned page list for kv copies
     int device = 0;
+    int attn_cap = 512;  // attention work items that run in one wave of workgroups
     // diagnostic timing of one kernel class
     int prof_class = 0;
     int prof_used = 0;
@@ -316,11 +317,28 @@ void build_stage(sd_ctx* c, Slot& s, int mode, bool with_items, int* n_items, in
     doff[0] = 0;
     int maxL = 0, ni = 0;
     ioff[0] = 0;
-    // attention chunk: a multiple of 32 tokens giving about kAttnItems items
+    // Attention work items: each (user, KV head) context is cut into chunks
+    // (multiples of 32 tokens, the kernel's block) so that the whole batch
+    // has at most attn_cap items -- one wave of co-resident workgroups, so
+    // no workgroup waits for a second round -- and each user's chunks are
+    // of equal length.  Fewer, longer items also keep the partial-sum
+    // traffic (one [rows][head_dim] fp32 partial per item) small.
+    const int hkv = c->D.hkv;
+    const int cap = std::max(c->attn_cap, s.B * hkv);
     long total = 0;
-    for (int b = 0; b < s.B; ++b) total += (long)c->users[s.users[b]].prefix + s.L[b] + 1;
-    int chunk = (int)std::min<long>(1 << 20, std::max<long>(64, (total * c->D.hkv + kAttnItems - 1) / kAttnItems));
-    chunk = (chunk + 31) & ~31;
+    int max_ctx = 1;
+    for (int b = 0; b < s.B; ++b) {
+        const int ctx = c->users[s.users[b]].prefix + s.L[b] + 1;
+        total += ctx;
+        max_ctx = std::max(max_ctx, ctx);
+    }
+    auto n_items_for = [&](int ch) {
+        long n = 0;
+        for (int b = 0; b < s.B; ++b) n += ceil_div(c->users[s.users[b]].prefix + s.L[b] + 1, ch);
+        return n * hkv;
+    };
+    int chunk = (int)std::max<long>(32, ((total * hkv + cap - 1) / cap + 31) & ~31L);
+    while (chunk < max_ctx && n_items_for(chunk) > cap) chunk += 32;
     for (int b = 0; b < s.B; ++b) {
         const User& u = c->users[s.users[b]];
         user[b] = s.users[b];
@@ -338,13 +356,15 @@ void build_stage(sd_ctx* c, Slot& s, int mode, bool with_items, int* n_items, in
         maxL = std::max(maxL, s.L[b]);
         if (with_items) {
             const int ctx = u.prefix + s.L[b] + 1;
-            const int nch = ceil_div(ctx, chunk);
-            for (int g = 0; g < c->D.hkv; ++g)
+            // equal chunks for this user: as many as `chunk` needs, evened out
+            const int cb = (ceil_div(ctx, ceil_div(ctx, chunk)) + 31) & ~31;
+            const int nch = ceil_div(ctx, cb);
+            for (int g = 0; g < hkv; ++g)
                 for (int ch = 0; ch < nch; ++ch) {
                     items[ni * 4 + 0] = b;
                     items[ni * 4 + 1] = g;
-                    items[ni * 4 + 2] = ch * chunk;
-                    items[ni * 4 + 3] = std::min(ctx, (ch + 1) * chunk);
+                    items[ni * 4 + 2] = ch * cb;
+                    items[ni * 4 + 3] = std::min(ctx, (ch + 1) * cb);
                     ++ni;
                 }
         }
@@ -538,6 +558,7 @@ sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_poo
     c->layers.assign(w->layers, w->layers + cfg->n_layers);
     c->w.layers = nullptr;
     c->device = dev;
+    c->attn_cap = std::min(kAttnItemsMax, kAttnWGsPerCU * std::max(prop.multiProcessorCount, 1));
     c->kv.base = kv_pool;
     c->kv.n_pages = cfg->n_pages;
     c->kv.hkv = c->D.hkv;
@@ -589,6 +610,14 @@ sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_poo
     }
     ok = ok && hipHostMalloc((void**)&c->kvw_host, (size_t)L.max_pages * 4, hipHostMallocDefault) ==
                    hipSuccess;
+    if (ok) {
+        // The attention kernel reads whole 32-token blocks and multiplies the
+        // value rows past a user's context by an exact 0; zeroing the pool
+        // once keeps never-written rows finite (0 * NaN would not be 0).
+        const Dims& D = c->D;
+        const size_t kv_bytes = (size_t)D.L * cfg->n_pages * 2 * D.hkv * kPageTokens * D.hd * c->kv.esize;
+        ok &= hipMemset(kv_pool, 0, kv_bytes) == hipSuccess;
+    }
     if (ok && c->D.bf16) {
         // repack the projection matrices and the lm_head into fragment order
         const Dims& D = c->D;

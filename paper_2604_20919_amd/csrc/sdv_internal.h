@@ -7,7 +7,9 @@
 namespace sdv {
 
 constexpr int kPageTokens = 16;   // tokens per KV page
-constexpr int kAttnItems = 512;   // target attention work items per batch
+constexpr int kAttnItemsMax = 1024;  // attention work items per batch (beyond one per (user, KV head))
+constexpr int kAttnWGsPerCU = 2;     // co-resident attention workgroups per CU (register bound)
+constexpr int kAttnBuffers = 3;      // LDS ring of the attention kernel (buffers - 1 blocks in flight)
 constexpr int kVocabChunks = 16;  // vocab split of the sampler kernels
 constexpr int kMaxPending = 8;
 
