@@ -49,7 +49,7 @@ def build(force: bool = True) -> str:
 class _Model(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "n_layers", "d_model", "n_q_heads", "n_kv_heads", "head_dim", "d_ffn", "vocab",
-        "qk_norm", "act_bf16", "wdtype")] + [("rope_base", ctypes.c_double),
+        "qk_norm", "kv_bf16", "wdtype")] + [("rope_base", ctypes.c_double),
                                              ("rms_eps", ctypes.c_double)]
 
 
@@ -157,9 +157,9 @@ def attend(q, k, v, scale: Optional[float] = None) -> np.ndarray:
 # forward
 # ----------------------------------------------------------------------------
 
-def _model_struct(m: wl.ModelShape, act_bf16: Optional[bool] = None) -> _Model:
+def _model_struct(m: wl.ModelShape, kv_bf16: Optional[bool] = None) -> _Model:
     return _Model(m.n_layers, m.d_model, m.n_q_heads, m.n_kv_heads, m.head_dim, m.d_ffn, m.vocab,
-                  int(m.qk_norm), int(m.dtype == "bf16" if act_bf16 is None else act_bf16),
+                  int(m.qk_norm), int(m.dtype == "bf16" if kv_bf16 is None else kv_bf16),
                   int(m.dtype == "bf16"), m.rope_base, m.rms_eps)
 
 
@@ -208,7 +208,7 @@ class KVSource:
 
 
 def forward(m: wl.ModelShape, weights: WeightSource, kv: Optional[KVSource], prefix_len, n_slots,
-            tokens, want_kv: bool = False, act_bf16: Optional[bool] = None):
+            tokens, want_kv: bool = False, kv_bf16: Optional[bool] = None):
     """Logits [T][V] (float32) of the verify forward; optionally the new
     slots' K and V [J][T][hkv][hd]."""
     prefix_len = np.ascontiguousarray(prefix_len, dtype=np.int32)
@@ -253,7 +253,7 @@ def forward(m: wl.ModelShape, weights: WeightSource, kv: Optional[KVSource], pre
             return -1
 
     lcb, kcb = _LAYER_FN(layer_cb), _KV_FN(kv_cb)
-    ms = _model_struct(m, act_bf16)
+    ms = _model_struct(m, kv_bf16)
     rc = lib().or_forward(ctypes.byref(ms), len(n_slots), _p(prefix_len), _p(n_slots), _p(tokens),
                           _p(weights.global_(wl.EMBED)), _p(weights.global_(wl.NORM_F)),
                           _p(weights.global_(wl.LM_HEAD)), lcb, kcb, None, _p(logits),
@@ -265,11 +265,11 @@ def forward(m: wl.ModelShape, weights: WeightSource, kv: Optional[KVSource], pre
     return logits
 
 
-def prefill(m: wl.ModelShape, weights: WeightSource, tokens, act_bf16: Optional[bool] = None):
+def prefill(m: wl.ModelShape, weights: WeightSource, tokens, kv_bf16: Optional[bool] = None):
     """Keys/values [J][P][hkv][hd] of a full causal forward over `tokens`."""
     tokens = np.ascontiguousarray(tokens, dtype=np.int32)
     P = tokens.size
-    _, K, V = forward(m, weights, None, [0], [P], tokens, want_kv=True, act_bf16=act_bf16)
+    _, K, V = forward(m, weights, None, [0], [P], tokens, want_kv=True, kv_bf16=kv_bf16)
     if m.dtype == "bf16":
         K = wl.bf16_to_f32(wl.f32_to_bf16(K))
         V = wl.bf16_to_f32(wl.f32_to_bf16(V))

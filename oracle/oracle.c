@@ -20,9 +20,12 @@
  * The forward is a pre-RMSNorm decoder with grouped-query attention, optional
  * per-head QK-RMSNorm, rotate-half RoPE and a SwiGLU FFN (the Qwen3 shape the
  * paper evaluates in Sec. IV-A, Table II).  Dot products and softmax sums are
- * accumulated in double.  When act_bf16 is set the oracle rounds to bf16 at
- * the points a bf16 datapath stores values: GEMM inputs, and q/k/v after
- * QK-norm and RoPE (the KV cache holds bf16).
+ * accumulated in double and activations are kept in double.  When kv_bf16
+ * is set (bf16 models) the keys and values of the new slots are rounded to
+ * bf16 after QK-norm and RoPE, because that is what a bf16 KV cache stores and
+ * what later slots of the same batch read back; the cached prefix is given
+ * in bf16 already.  The paper fixes no precision; weights and the KV cache
+ * are the only bf16 quantities of this reading.
  *
  * Sampler decisions are taken in fp32 (the precision of the GPU sampler):
  * r = p(d)/q(d) is an fp32 division compared with an fp32 uniform, and race
@@ -174,7 +177,7 @@ static inline double silu(double g) { return g / (1.0 + exp(-g)); }
 typedef struct {
     int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, vocab;
     int32_t qk_norm;  /* per-head RMSNorm on q and k before RoPE */
-    int32_t act_bf16; /* bf16 rounding points of a bf16 datapath */
+    int32_t kv_bf16;  /* new keys / values rounded to bf16 (bf16 KV cache) */
     int32_t wdtype;   /* weight arrays: 0 = fp32, 1 = bf16 bits */
     double rope_base, rms_eps;
 } or_model;
@@ -191,7 +194,7 @@ typedef int (*or_layer_fn)(void* cb, int32_t layer, or_layer* out);
  * as [prefix][n_kv_heads][head_dim] fp32 arrays; returns 0 on success */
 typedef int (*or_kv_fn)(void* cb, int32_t layer, int32_t b, float* k, float* v);
 
-static double actr(const or_model* m, double x) { return m->act_bf16 ? or_round_bf16(x) : x; }
+static double kvr(const or_model* m, double x) { return m->kv_bf16 ? or_round_bf16(x) : x; }
 
 /* y[t][o] = sum_i x[t][i] * W[o][i] for t < rows, o < nout */
 static void matmul_rows(const double* x, int rows, int nin, const void* w, int dt, int nout,
@@ -259,7 +262,6 @@ int or_forward(const or_model* m, int32_t n_users, const int32_t* prefix_len,
         /* attention block */
         for (int t = 0; t < T; ++t) {
             or_rmsnorm(x + (size_t)t * d, d, w.norm1, dt, m->rms_eps, h + (size_t)t * d);
-            for (int i = 0; i < d; ++i) h[(size_t)t * d + i] = actr(m, h[(size_t)t * d + i]);
         }
         matmul_rows(h, T, d, w.wq, dt, nq, q);
         matmul_rows(h, T, d, w.wk, dt, nk, kk);
@@ -273,15 +275,14 @@ int or_forward(const or_model* m, int32_t n_users, const int32_t* prefix_len,
                     double* v = q + (size_t)t * nq + (size_t)hh * hd;
                     if (m->qk_norm) { or_rmsnorm(v, hd, w.qnorm, dt, m->rms_eps, tmp); memcpy(v, tmp, sizeof(double) * hd); }
                     or_rope(v, hd, pos, m->rope_base);
-                    for (int i = 0; i < hd; ++i) v[i] = actr(m, v[i]);
                 }
                 for (int hh = 0; hh < hkv; ++hh) {
                     double* v = kk + (size_t)t * nk + (size_t)hh * hd;
                     if (m->qk_norm) { or_rmsnorm(v, hd, w.knorm, dt, m->rms_eps, tmp); memcpy(v, tmp, sizeof(double) * hd); }
                     or_rope(v, hd, pos, m->rope_base);
-                    for (int i = 0; i < hd; ++i) v[i] = actr(m, v[i]);
+                    for (int i = 0; i < hd; ++i) v[i] = kvr(m, v[i]);
                     double* u = vv + (size_t)t * nk + (size_t)hh * hd;
-                    for (int i = 0; i < hd; ++i) u[i] = actr(m, u[i]);
+                    for (int i = 0; i < hd; ++i) u[i] = kvr(m, u[i]);
                 }
             }
         }
@@ -319,18 +320,16 @@ int or_forward(const or_model* m, int32_t n_users, const int32_t* prefix_len,
                           att + (size_t)t * nq + (size_t)hh * hd);
             }
         }
-        for (size_t i = 0; i < (size_t)T * nq; ++i) att[i] = actr(m, att[i]);
         matmul_rows(att, T, nq, w.wo, dt, d, y);
         for (size_t i = 0; i < (size_t)T * d; ++i) x[i] += y[i];
 
         /* FFN block */
         for (int t = 0; t < T; ++t) {
             or_rmsnorm(x + (size_t)t * d, d, w.norm2, dt, m->rms_eps, h + (size_t)t * d);
-            for (int i = 0; i < d; ++i) h[(size_t)t * d + i] = actr(m, h[(size_t)t * d + i]);
         }
         matmul_rows(h, T, d, w.wg, dt, F, g);
         matmul_rows(h, T, d, w.wu, dt, F, y);
-        for (size_t i = 0; i < (size_t)T * F; ++i) g[i] = actr(m, silu(g[i]) * y[i]);
+        for (size_t i = 0; i < (size_t)T * F; ++i) g[i] = silu(g[i]) * y[i];
         matmul_rows(g, T, F, w.wd, dt, d, y);
         for (size_t i = 0; i < (size_t)T * d; ++i) x[i] += y[i];
     }
@@ -338,7 +337,6 @@ int or_forward(const or_model* m, int32_t n_users, const int32_t* prefix_len,
     if (rc == 0) {
         for (int t = 0; t < T; ++t) {
             or_rmsnorm(x + (size_t)t * d, d, norm_f, dt, m->rms_eps, h + (size_t)t * d);
-            for (int i = 0; i < d; ++i) h[(size_t)t * d + i] = actr(m, h[(size_t)t * d + i]);
         }
 #pragma omp parallel for schedule(static)
         for (int o = 0; o < V; ++o) {

@@ -31,7 +31,7 @@ namespace sdv {
 
 struct AttnP {
     BatchView bv;
-    const bf16_t* q;   // [T][hq][hd]
+    const bf16_t* q;   // [2][T][hq][hd]: hi and lo planes
     KVPool kv;
     int layer;
     int hq, hkv, G;
@@ -75,14 +75,6 @@ __device__ __forceinline__ void v_slot_src(int s, int& pg, int& off) {
 
 typedef __attribute__((address_space(4))) const int32_t cint32_t;
 
-// s_waitcnt immediate for "vector memory counter <= N" (LGK counter <= 0
-// when LGK0, else free)
-template <int N, bool LGK0 = false>
-__device__ __forceinline__ void wait_vm() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | ((LGK0 ? 0 : 15) << 8));
-}
-
 // Reductions over the four lanes l, l^16, l^32, l^48 that hold one query
 // row: each cross-lane swap returns the row halves exchanged between its two
 // operands, so combining both results with the own value pairs every lane
@@ -98,17 +90,6 @@ __device__ __forceinline__ float row_sum4(float v) {
     v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
     const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
-}
-
-// Workgroup barrier without the memory fence of __syncthreads(): the fence
-// would wait for every outstanding load, including the direct-to-LDS loads
-// of later blocks that are meant to stay in flight.  Callers wait for what
-// must be complete themselves; the empty asm statements keep the compiler
-// from moving memory accesses across the barrier.
-__device__ __forceinline__ void barrier_nofence() {
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
 }
 
 template <int NBUF>
@@ -162,7 +143,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const int ntiles = (R + 15) >> 4;
     for (int rp = 0; rp < ntiles; rp += 4 * RT_MAX) {
         // this wave's row tiles in this pass: rp + wave + 4*i
-        bf16x8 qf[RT_MAX][4];
+        bf16x8 qf[RT_MAX][4], ql[RT_MAX][4];  // query hi / lo planes
         int lim[RT_MAX];
         float m[RT_MAX], l[RT_MAX];
         f32x4 o[RT_MAX][8];
@@ -175,8 +156,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             const bool ok = act[i] && row < R;
             const int j = ok ? row / G : 0, hh = ok ? row % G : 0;
             const bf16_t* qs = p.q + ((size_t)(tbase + j) * p.hq + g * G + hh) * HD + 8 * lg;
+            const size_t qpl = (size_t)p.bv.T * p.hq * HD;
 #pragma unroll
-            for (int ds = 0; ds < 4; ++ds) qf[i][ds] = ok ? *(const bf16x8*)(qs + ds * 32) : bf16x8{};
+            for (int ds = 0; ds < 4; ++ds) {
+                qf[i][ds] = ok ? *(const bf16x8*)(qs + ds * 32) : bf16x8{};
+                ql[i][ds] = ok ? *(const bf16x8*)(qs + qpl + ds * 32) : bf16x8{};
+            }
             lim[i] = prefix + j;
             m[i] = -INFINITY;
             l[i] = 0.f;
@@ -197,19 +182,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             const bool full = t0 + 32 <= c1 && t0 + 31 <= prefix;
             const uint4* kb = kvs[buf];
             const uint4* vb = kvs[buf] + 512;
-            bf16x8 kf[8], vf[8];
-#pragma unroll
-            for (int f = 0; f < 8; ++f) kf[f] = __builtin_bit_cast(bf16x8, kb[f * 64 + lane]);
-#pragma unroll
-            for (int f = 0; f < 8; ++f) vf[f] = __builtin_bit_cast(bf16x8, vb[f * 64 + lane]);
 #pragma unroll
             for (int i = 0; i < RT_MAX; ++i) {
                 if (!act[i]) continue;
+                // S^T = K (Q_hi + Q_lo)^T
                 f32x4 sa = f32x4{0.f, 0.f, 0.f, 0.f}, sb = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int ds = 0; ds < 4; ++ds) {
-                    sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ds], qf[i][ds], sa, 0, 0, 0);
-                    sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[4 + ds], qf[i][ds], sb, 0, 0, 0);
+                    const bf16x8 ka = __builtin_bit_cast(bf16x8, kb[ds * 64 + lane]);
+                    const bf16x8 kk = __builtin_bit_cast(bf16x8, kb[(4 + ds) * 64 + lane]);
+                    sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[i][ds], sa, 0, 0, 0);
+                    sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, ql[i][ds], sa, 0, 0, 0);
+                    sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qf[i][ds], sb, 0, 0, 0);
+                    sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, ql[i][ds], sb, 0, 0, 0);
                 }
                 // lane holds the scores of its query row at tokens t0 + 8*lg + e
                 float sc[8];
@@ -232,13 +217,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
                 const bool live = mn != -INFINITY;  // something visible for this row
                 const float ms = live ? mn * p.scale_log2 : 0.f;
                 const float alpha = live ? __builtin_amdgcn_exp2f((m[i] - mn) * p.scale_log2) : 1.f;
+                // P as hi + lo bf16 pair (about 16 significant bits)
                 float rs = 0.f;
-                bf16x8 pb;
+                bf16x8 pb, pl;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     const float pe = __builtin_amdgcn_exp2f(fmaf(sc[e], p.scale_log2, -ms));
                     rs += pe;
                     pb[e] = (__bf16)pe;
+                    pl[e] = (__bf16)(pe - (float)pb[e]);
                 }
                 l[i] = fmaf(l[i], alpha, rs);
                 m[i] = mn;
@@ -247,8 +234,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
                     for (int dt = 0; dt < 8; ++dt) o[i][dt] *= alpha;
                 }
 #pragma unroll
-                for (int dt = 0; dt < 8; ++dt)
-                    o[i][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt], pb, o[i][dt], 0, 0, 0);
+                for (int dt = 0; dt < 8; ++dt) {
+                    const bf16x8 vf = __builtin_bit_cast(bf16x8, vb[dt * 64 + lane]);
+                    o[i][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb, o[i][dt], 0, 0, 0);
+                    o[i][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl, o[i][dt], 0, 0, 0);
+                }
             }
         };
 
@@ -324,9 +314,9 @@ __global__ __launch_bounds__(256) void k_attn_combine(BatchView bv, const float*
         if (lane + 64 < hd) acc1 += apart[pr * hd + lane + 64] * w;
     }
     const float inv = 1.0f / Ls;
-    TA* dst = out + (size_t)t * hq * hd + (size_t)h * hd;
-    if (lane < hd) st(dst, lane, acc0 * inv);
-    if (lane + 64 < hd) st(dst, lane + 64, acc1 * inv);
+    const size_t o0 = ((size_t)t * hq + h) * hd, pl = (size_t)bv.T * hq * hd;
+    if (lane < hd) st_act(out, pl, o0 + lane, acc0 * inv);
+    if (lane + 64 < hd) st_act(out, pl, o0 + lane + 64, acc1 * inv);
 }
 
 // fp32 path: one wave per (slot, query head); lanes split head_dim

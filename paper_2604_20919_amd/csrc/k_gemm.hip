@@ -37,6 +37,7 @@ struct GemmP {
     int vcols;
     void* out;
     int ldo;
+    size_t oplane;  // SwiGLU: elements between the hi and lo output planes
 };
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + expf(-g)); }
@@ -53,15 +54,22 @@ __device__ __forceinline__ void epi_store4(const GemmP& p, int t, int col, f32x4
     }
 }
 
+// SwiGLU output as the next GEMM's activation planes: hi = bf16(a) at out,
+// lo = bf16(a - hi) one plane (oplane elements) further
 __device__ __forceinline__ void swiglu_store4(const GemmP& p, int t, int col, f32x4 g, f32x4 u) {
     bf16_t* o = (bf16_t*)p.out + (size_t)t * p.ldo + col;
-    uint2 pk;
-    pk.x = (uint32_t)f32_to_bf16(silu(g[0]) * u[0]) | ((uint32_t)f32_to_bf16(silu(g[1]) * u[1]) << 16);
-    pk.y = (uint32_t)f32_to_bf16(silu(g[2]) * u[2]) | ((uint32_t)f32_to_bf16(silu(g[3]) * u[3]) << 16);
-    *(uint2*)o = pk;
+    uint32_t hi[4], lo[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const float a = silu(g[e]) * u[e];
+        hi[e] = f32_to_bf16(a);
+        lo[e] = f32_to_bf16(a - bf16_to_f32((bf16_t)hi[e]));
+    }
+    *(uint2*)o = uint2{hi[0] | (hi[1] << 16), hi[2] | (hi[3] << 16)};
+    *(uint2*)(o + p.oplane) = uint2{lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16)};
 }
 
-template <int MT, int NSUB, int KC, int EPI, bool SPLIT, int NW = 4, int PD = 2>
+template <int MT, int NSUB, int KC, int EPI, bool SPLIT, int NW, int PL, int PD = 2>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, 2)))
 void k_gemm_bf16(GemmP p) {
     constexpr int NTH = 64 * NW;         // threads per workgroup
@@ -69,11 +77,14 @@ void k_gemm_bf16(GemmP p) {
     constexpr int KS = KC / 32;          // MFMA k-steps per chunk
     constexpr int LDX = KC + 8;          // padded LDS row (bf16 elements)
     constexpr int PPR = KC / 8;          // 16-byte pieces per staged row
-    constexpr int NPC = MT * 16 * PPR;   // pieces per staged chunk
+    constexpr int NPP = MT * 16 * PPR;   // pieces per staged plane
+    constexpr int NPC = PL * NPP;        // pieces per staged chunk (all planes)
     constexpr int XPT = (NPC + NTH - 1) / NTH;  // X pieces per thread
     constexpr bool XEVEN = NPC % NTH == 0;
+    constexpr int PLANE = MT * 16 * LDX;  // LDS elements per plane
     static_assert(EPI != EPI_SWIGLU || NSUB % 2 == 0, "SwiGLU pairs gate/up sub-tiles");
-    __shared__ __attribute__((aligned(16))) bf16_t xs[2][MT * 16 * LDX];
+    static_assert(2 * PL * PLANE * 2 <= 160 * 1024, "X staging exceeds LDS");
+    __shared__ __attribute__((aligned(16))) bf16_t xs[2][PL * PLANE];
 
     const int tile = SPLIT ? blockIdx.x / p.S : blockIdx.x;
     const int split = SPLIT ? blockIdx.x % p.S : 0;
@@ -94,7 +105,7 @@ void k_gemm_bf16(GemmP p) {
         woff[s] = vs * (uint32_t)p.KT * 1024u + (uint32_t)lane * 16u;
     }
     const __amdgpu_buffer_rsrc_t xres =
-        __builtin_amdgcn_make_buffer_rsrc((void*)p.X, (short)0, p.T * p.K * 2, 0x00020000);
+        __builtin_amdgcn_make_buffer_rsrc((void*)p.X, (short)0, PL * p.T * p.K * 2, 0x00020000);
 
     f32x4 acc[NSUB][MT];
 #pragma unroll
@@ -122,8 +133,9 @@ void k_gemm_bf16(GemmP p) {
 #pragma unroll
     for (int i = 0; i < XPT; ++i) {
         const int idx = min((int)threadIdx.x + i * NTH, NPC - 1);
-        const int r = min(idx / PPR, p.T - 1), cc = idx % PPR;
-        xoff[i] = ((uint32_t)r * (uint32_t)p.K + (uint32_t)cc * 8u) * 2u;
+        const int pl = idx / NPP, pi = idx % NPP;
+        const int r = min(pi / PPR, p.T - 1), cc = pi % PPR;
+        xoff[i] = (((uint32_t)pl * (uint32_t)p.T + (uint32_t)r) * (uint32_t)p.K + (uint32_t)cc * 8u) * 2u;
     }
     auto load_x = [&](uint4 (&x)[XPT], int c) {
         const int so = c * KC * 2;
@@ -135,7 +147,9 @@ void k_gemm_bf16(GemmP p) {
 #pragma unroll
         for (int i = 0; i < XPT; ++i) {
             const int idx = threadIdx.x + i * NTH;
-            if (XEVEN || idx < NPC) *(uint4*)(&xs[buf][(idx / PPR) * LDX + (idx % PPR) * 8]) = x[i];
+            const int pl = idx / NPP, pi = idx % NPP;
+            if (XEVEN || idx < NPC)
+                *(uint4*)(&xs[buf][pl * PLANE + (pi / PPR) * LDX + (pi % PPR) * 8]) = x[i];
         }
     };
     auto load_w = [&](bf16x8 (&w)[KS][NSUB], int c) {
@@ -153,11 +167,15 @@ void k_gemm_bf16(GemmP p) {
 #pragma unroll
             for (int m = 0; m < MT; ++m) {
                 if (m < mt_act) {
-                    const bf16x8 xf = *(const bf16x8*)(xb + (m * 16 + lr) * LDX + ks * 32 + 8 * lg);
 #pragma unroll
-                    for (int s = 0; s < NSUB; ++s)
-                        acc[s][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[ks][s], xf, acc[s][m],
-                                                                             0, 0, 0);
+                    for (int pl = 0; pl < PL; ++pl) {
+                        const bf16x8 xf = *(const bf16x8*)(xb + pl * PLANE + (m * 16 + lr) * LDX +
+                                                           ks * 32 + 8 * lg);
+#pragma unroll
+                        for (int s = 0; s < NSUB; ++s)
+                            acc[s][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[ks][s], xf,
+                                                                                 acc[s][m], 0, 0, 0);
+                    }
                 }
             }
         }
@@ -318,8 +336,10 @@ __global__ void k_gemm_f32(GemmF p) {
 // sub-tiles of 16 rows per wave, KC k elements per pipeline chunk, NW waves
 // per workgroup.  Eight waves share one staged X chunk where the row count
 // allows (it halves the X staging per weight byte; measured 96 vs 107 us
-// for the 32B gate/up at T = 80); more than 16 slot tiles need the larger
-// register budget of one wave per SIMD, so they use four.
+// for the 32B gate/up at T = 80); more than 12 slot tiles need the larger
+// register budget of one wave per SIMD, so they use four, and above 16 slot
+// tiles the chunk shrinks to 32 k so that the two activation planes of a
+// double-buffered chunk fit in LDS.
 struct GemmShape { int MT, NSUB, KC, NW; };
 
 static GemmShape shape_for(int T, int vcols) {
@@ -327,8 +347,8 @@ static GemmShape shape_for(int T, int vcols) {
     static const int classes[] = {2, 4, 6, 8, 12, 16, 20, 26};
     for (int c : classes)
         if (mt <= c) {
-            const int nw = (c <= 16 && vcols % (16 * 2 * 8) == 0) ? 8 : 4;
-            return {c, 2, 64, nw};
+            const int nw = (c <= 12 && vcols % (16 * 2 * 8) == 0) ? 8 : 4;
+            return {c, 2, c > 16 ? 32 : 64, nw};
         }
     return {0, 0, 0, 0};
 }
@@ -336,14 +356,15 @@ static GemmShape shape_for(int T, int vcols) {
 typedef void (*GemmFn)(GemmP);
 typedef void (*ReduceFn)(GemmP);
 
-// split-K kernels write raw partial planes; the epilogue runs in the reducer
-template <int MT, int NW, bool SPLIT>
+// Activations always come as two planes (hi, lo); split-K kernels write raw
+// partial planes and the epilogue runs in the reducer.
+template <int MT, int NW, int KC, bool SPLIT>
 static GemmFn pick_epi(int epi) {
-    if (SPLIT) return k_gemm_bf16<MT, 2, 64, EPI_STORE, true, NW>;
+    if (SPLIT) return k_gemm_bf16<MT, 2, KC, EPI_STORE, true, NW, 2>;
     switch (epi) {
-        case EPI_RESID: return k_gemm_bf16<MT, 2, 64, EPI_RESID, false, NW>;
-        case EPI_SWIGLU: return k_gemm_bf16<MT, 2, 64, EPI_SWIGLU, false, NW>;
-        default: return k_gemm_bf16<MT, 2, 64, EPI_STORE, false, NW>;
+        case EPI_RESID: return k_gemm_bf16<MT, 2, KC, EPI_RESID, false, NW, 2>;
+        case EPI_SWIGLU: return k_gemm_bf16<MT, 2, KC, EPI_SWIGLU, false, NW, 2>;
+        default: return k_gemm_bf16<MT, 2, KC, EPI_STORE, false, NW, 2>;
     }
 }
 
@@ -351,24 +372,23 @@ template <bool SPLIT>
 static GemmFn pick(const GemmShape& sh, int epi) {
     if (sh.NW == 8) {
         switch (sh.MT) {
-            case 2: return pick_epi<2, 8, SPLIT>(epi);
-            case 4: return pick_epi<4, 8, SPLIT>(epi);
-            case 6: return pick_epi<6, 8, SPLIT>(epi);
-            case 8: return pick_epi<8, 8, SPLIT>(epi);
-            case 12: return pick_epi<12, 8, SPLIT>(epi);
-            case 16: return pick_epi<16, 8, SPLIT>(epi);
+            case 2: return pick_epi<2, 8, 64, SPLIT>(epi);
+            case 4: return pick_epi<4, 8, 64, SPLIT>(epi);
+            case 6: return pick_epi<6, 8, 64, SPLIT>(epi);
+            case 8: return pick_epi<8, 8, 64, SPLIT>(epi);
+            case 12: return pick_epi<12, 8, 64, SPLIT>(epi);
         }
         return nullptr;
     }
     switch (sh.MT) {
-        case 2: return pick_epi<2, 4, SPLIT>(epi);
-        case 4: return pick_epi<4, 4, SPLIT>(epi);
-        case 6: return pick_epi<6, 4, SPLIT>(epi);
-        case 8: return pick_epi<8, 4, SPLIT>(epi);
-        case 12: return pick_epi<12, 4, SPLIT>(epi);
-        case 16: return pick_epi<16, 4, SPLIT>(epi);
-        case 20: return pick_epi<20, 4, SPLIT>(epi);
-        case 26: return pick_epi<26, 4, SPLIT>(epi);
+        case 2: return pick_epi<2, 4, 64, SPLIT>(epi);
+        case 4: return pick_epi<4, 4, 64, SPLIT>(epi);
+        case 6: return pick_epi<6, 4, 64, SPLIT>(epi);
+        case 8: return pick_epi<8, 4, 64, SPLIT>(epi);
+        case 12: return pick_epi<12, 4, 64, SPLIT>(epi);
+        case 16: return pick_epi<16, 4, 64, SPLIT>(epi);
+        case 20: return pick_epi<20, 4, 32, SPLIT>(epi);
+        case 26: return pick_epi<26, 4, 32, SPLIT>(epi);
     }
     return nullptr;
 }
@@ -478,6 +498,7 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
     p.part = sb.gpart;
     p.out = g.out;
     p.ldo = g.ldo;
+    p.oplane = (size_t)g.T * g.ldo;  // SwiGLU output planes are [2][T][ldo]
     if (g.raw) {
         // S partial planes [S][T][N] for a fused consumer to reduce
         hipLaunchKernelGGL(pick<true>(sh, EPI_STORE), dim3(p.tiles * S), dim3(64 * sh.NW), 0, s, p);

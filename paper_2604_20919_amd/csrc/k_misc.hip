@@ -41,8 +41,9 @@ void launch_prepare(const Dims& D, const BatchView& bv, const SlotBufs& sb, hipS
 
 // ---------------------------------------------------------------------------
 // Split-K reduction fused with the residual add and the next RMSNorm:
-// x[t] += sum_s part[s][t] (split order, fixed), h[t] = x[t] * rstd * gamma.
-// One workgroup per slot row, the row held in registers.
+// x[t] += sum_s part[s][t] (split order, fixed), h[t] = x[t] * rstd * gamma
+// (h as activation planes, see st_act).  One workgroup per slot row, the
+// row held in registers.
 // ---------------------------------------------------------------------------
 template <typename TA, int PER>
 __global__ __launch_bounds__(1024) void k_resid_norm(const float* part, int S, int T, float* x,
@@ -106,11 +107,11 @@ __global__ __launch_bounds__(1024) void k_resid_norm(const float* part, int S, i
     for (int i = 0; i < PER; ++i) {
         const int k = threadIdx.x + i * 1024;
         if (k < n4) {
-            const size_t o = (size_t)t * d + 4 * k;
-            st(h, o + 0, v[i].x * rs * ld(gamma, 4 * k + 0));
-            st(h, o + 1, v[i].y * rs * ld(gamma, 4 * k + 1));
-            st(h, o + 2, v[i].z * rs * ld(gamma, 4 * k + 2));
-            st(h, o + 3, v[i].w * rs * ld(gamma, 4 * k + 3));
+            const size_t o = (size_t)t * d + 4 * k, pl = (size_t)T * d;
+            st_act(h, pl, o + 0, v[i].x * rs * ld(gamma, 4 * k + 0));
+            st_act(h, pl, o + 1, v[i].y * rs * ld(gamma, 4 * k + 1));
+            st_act(h, pl, o + 2, v[i].z * rs * ld(gamma, 4 * k + 2));
+            st_act(h, pl, o + 3, v[i].w * rs * ld(gamma, 4 * k + 3));
         }
     }
 }
@@ -135,7 +136,7 @@ void launch_resid_norm(const Dims& D, int T, const float* part, int S, float* x,
 template <typename TA, int PER>
 __global__ __launch_bounds__(256) void k_embed_norm(const int32_t* tok, const TA* E,
                                                     const TA* gamma, float* x, TA* h, int d,
-                                                    float eps) {
+                                                    float eps, int T) {
     __shared__ float red[4];
     const int t = blockIdx.x;
     const size_t row = (size_t)tok[t] * d;
@@ -160,7 +161,7 @@ __global__ __launch_bounds__(256) void k_embed_norm(const int32_t* tok, const TA
         if (4 * k < d)
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-                st(h, (size_t)t * d + 4 * k + e, v[i][e] * rs * ld(gamma, 4 * k + e));
+                st_act(h, (size_t)T * d, (size_t)t * d + 4 * k + e, v[i][e] * rs * ld(gamma, 4 * k + e));
     }
 }
 
@@ -168,7 +169,7 @@ void launch_embed_norm(const Dims& D, const BatchView& bv, const void* embed, co
                        const SlotBufs& sb, hipStream_t s) {
     const int per = (D.d / 4 + 255) / 256;
 #define EN(TA, P) hipLaunchKernelGGL((k_embed_norm<TA, P>), dim3(bv.T), dim3(256), 0, s, sb.tok, \
-                                     (const TA*)embed, (const TA*)gamma, sb.x, (TA*)sb.h, D.d, D.eps)
+                                     (const TA*)embed, (const TA*)gamma, sb.x, (TA*)sb.h, D.d, D.eps, bv.T)
     if (D.bf16) {
         if (per <= 1) EN(bf16_t, 1); else if (per <= 2) EN(bf16_t, 2); else if (per <= 5) EN(bf16_t, 5); else EN(bf16_t, 8);
     } else {
@@ -223,9 +224,9 @@ __global__ __launch_bounds__(256) void k_qkrope(BatchView bv, const float* qkv, 
     const float y0 = x0 * c - x1 * sn;
     const float y1 = x1 * c + x0 * sn;
     if (is_q) {
-        TA* dst = qbuf + (size_t)t * hq * hd + (size_t)h * hd;
-        st(dst, lane, y0);
-        st(dst, lane + half, y1);
+        const size_t q0 = ((size_t)t * hq + h) * hd, pl = (size_t)bv.T * hq * hd;
+        st_act(qbuf, pl, q0 + lane, y0);
+        st_act(qbuf, pl, q0 + lane + half, y1);
         return;
     }
     const int g = h - hq;

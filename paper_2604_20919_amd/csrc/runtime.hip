@@ -127,10 +127,13 @@ Layout plan(const sd_config& c) {
     L.tok = take((size_t)L.Tmax * 4);
     L.cs = take((size_t)L.Tmax * (D.hd / 2) * 2 * 4);
     L.x = take((size_t)L.Tmax * D.d * 4);
-    L.h = take((size_t)L.Tmax * D.d * es);
-    L.ffn = take((size_t)L.Tmax * D.F * es);
-    L.qbuf = take((size_t)L.Tmax * D.nq() * es);
-    L.attn = take((size_t)L.Tmax * D.nq() * es);
+    // activations that feed matrix products: two bf16 planes (hi, lo) each
+    // in the bf16 configuration, one fp32 plane otherwise
+    const size_t ap = D.bf16 ? 2 : 1;
+    L.h = take(ap * L.Tmax * D.d * es);
+    L.ffn = take(ap * L.Tmax * D.F * es);
+    L.qbuf = take(ap * L.Tmax * D.nq() * es);
+    L.attn = take(ap * L.Tmax * D.nq() * es);
     const size_t nparts = D.bf16 ? (size_t)L.max_items * L.rows_max : 1;
     L.apart = take(nparts * D.hd * 4);
     L.aml = take(nparts * 2 * 4);

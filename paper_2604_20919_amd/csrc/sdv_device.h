@@ -33,6 +33,20 @@ template <> __device__ __forceinline__ void st<bf16_t>(bf16_t* p, size_t i, floa
     p[i] = f32_to_bf16(v);
 }
 
+// Store of an activation that feeds a matrix product.  fp32 model: one
+// plane.  bf16 model: two bf16 planes, hi = bf16(v) at p[i] and
+// lo = bf16(v - hi) at p[plane + i]; the products consume both, so the
+// activation keeps about 16 significant bits instead of 8.
+template <typename T> __device__ __forceinline__ void st_act(T* p, size_t plane, size_t i, float v);
+template <> __device__ __forceinline__ void st_act<float>(float* p, size_t, size_t i, float v) {
+    p[i] = v;
+}
+template <> __device__ __forceinline__ void st_act<bf16_t>(bf16_t* p, size_t plane, size_t i, float v) {
+    const bf16_t hi = f32_to_bf16(v);
+    p[i] = hi;
+    p[plane + i] = f32_to_bf16(v - bf16_to_f32(hi));
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -53,6 +67,25 @@ __device__ __forceinline__ float block_sum_256(float v, float* red) {
     float s = red[0] + red[1] + red[2] + red[3];
     __syncthreads();
     return s;
+}
+
+// s_waitcnt immediate for "vector memory counter <= N" (LGK counter <= 0
+// when LGK0, else free)
+template <int N, bool LGK0 = false>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | ((LGK0 ? 0 : 15) << 8));
+}
+
+// Workgroup barrier without the memory fence of __syncthreads(): the fence
+// would wait for every outstanding load, including direct-to-LDS loads of
+// later pipeline stages that are meant to stay in flight.  Callers wait for what
+// must be complete themselves; the empty asm statements keep the compiler
+// from moving memory accesses across the barrier.
+__device__ __forceinline__ void barrier_nofence() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
 }
 
 // ---------------------------------------------------------------------------

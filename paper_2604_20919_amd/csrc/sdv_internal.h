@@ -69,10 +69,12 @@ struct SlotBufs {
     int32_t* tok;     // [Tmax]
     float* cs;        // [Tmax][hd/2][2]
     float* x;         // [Tmax][d]
-    void* h;          // [Tmax][d] normed GEMM input (act type)
-    void* ffn;        // [Tmax][F] SwiGLU output (act type)
-    void* qbuf;       // [Tmax][nq] act type
-    void* attn;       // [Tmax][nq] act type
+    // activations feeding matrix products; bf16 configuration: [2][T][...]
+    // hi and lo planes of the batch's T slots (plane stride T * width)
+    void* h;          // [T][d] normed GEMM input
+    void* ffn;        // [T][F] SwiGLU output
+    void* qbuf;       // [T][nq] rotated queries
+    void* attn;       // [T][nq] attention output
     float* apart;     // [max_items][rows_max][hd] attention chunk partials
     float* aml;       // [max_items][rows_max][2]
     float* gpart;     // GEMM split-K partials

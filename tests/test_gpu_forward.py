@@ -194,3 +194,29 @@ def test_determinism_two_runs_bit_identical():
     assert np.array_equal(a.logits, c.logits)
     assert np.array_equal(a.n_acc, c.n_acc) and np.array_equal(a.token, c.token)
     v.close()
+
+
+@pytest.mark.parametrize("T_target", [17, 70, 150, 250, 300, 416])
+def test_bf16_every_gemm_tile_class(T_target):
+    """Query-slot totals that select each GEMM tile class (2..26 slot tiles;
+    eight-wave tiles up to 16 slot tiles, four-wave tiles above) and the
+    split-K and unsplit paths, up to the 416-slot maximum."""
+    rng = np.random.default_rng(T_target)
+    L, T = [], 0
+    while T < T_target:
+        l = int(min(rng.integers(1, 13), T_target - T - 1)) if T_target - T > 1 else 0
+        if l < 1:
+            break
+        L.append(l)
+        T += l + 1
+    prefix = [int(p) for p in rng.integers(0, 200, size=len(L))]
+    w = wl.custom_workload("tiny-bf16", prefix, L, seed=40 + T_target, q_sigma=1.0)
+    dw = DeviceWeights(w.model, w.seed, gamma="uniform")
+    v = make_verifier(w, dw)
+    load_synthetic_kv(v, w)
+    b = w.batch(0)
+    ws = oracle.WeightSource(w.model, w.seed, "uniform")
+    gpu = run_gpu(v, w, 0, b, "stochastic", seed=2, round_=3)
+    rl, ref = run_oracle(w, b, "stochastic", seed=2, round_=3, weights=ws)
+    _check(w, b, gpu, rl, ref, 2e-2, f"tiny-bf16/T={b.T}")
+    v.close()

@@ -1,0 +1,263 @@
+"""Parity at the benchmark sizes.
+
+The Qwen3-32B-shaped workloads (16-user batch, 32-user ragged batch, four
+pipelined 16-user batches) run through the C ABI exactly as the benchmark
+runs them; the oracle recomputes sampled users one by one (users are
+independent, so a user's logits and decisions do not depend on the rest of
+its batch).  All 32B workloads are drawn with one seed (their shapes and
+distributions are the benchmark's; the draws differ from the benchmark's
+own seeds) so that the host generates the 64 layers once for the oracle.  The Qwen3-1.7B-shaped batch is
+compared in full.  Properties that hold at any size (q = p accepts every
+draft; planted greedy prefixes; run-to-run bit identity) are checked on the
+whole 32B batch.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workload as wl
+from gpu_harness import compare_decisions, load_synthetic_kv, logit_rel_err, make_verifier
+from workload.device import DeviceWeights, batch_to_device
+
+pytestmark = pytest.mark.gpu
+
+SEED32 = 3  # the seed of the 16-user workload; shared by every 32B workload here
+WORKLOADS32 = ("qwen3-32b-b16", "qwen3-32b-ragged32", "qwen3-32b-pipe4x16")
+TOL = 2e-2
+
+
+@dataclasses.dataclass
+class Sampled:
+    """GPU results of one sampled user plus what the oracle needs."""
+    workload: str
+    user: int
+    prefix: int
+    L: int
+    tokens: np.ndarray      # slot tokens (root, drafts)
+    drafts: np.ndarray
+    q: np.ndarray
+    accept_u: object
+    logits: np.ndarray      # GPU logits [L+1][V]
+    n_acc: int
+    token: int
+
+
+def _pick(w: wl.Workload, n: int, b: wl.Batch):
+    """Indices (within batch n) of the users the oracle recomputes: both ends
+    of a uniform batch; the user with most slots and the one with the
+    longest prefix of a ragged batch; of the pipelined batches, the user
+    with most slots in the first and the one with the longest prefix in the
+    last."""
+    if w.n_batches > 1:
+        if n == 0:
+            return [int(np.argmax(b.draft_len))]
+        return [int(np.argmax(b.prefix_len))] if n == w.n_batches - 1 else []
+    if np.all(b.draft_len == b.draft_len[0]) and np.all(b.prefix_len == b.prefix_len[0]):
+        return [0, len(b.users) - 1]
+    return sorted({int(np.argmax(b.draft_len)), int(np.argmax(b.prefix_len))})
+
+
+def _run_workload(name, dw, mode="stochastic"):
+    w = wl.workload(name, seed=SEED32)
+    v = make_verifier(w, dw, max_pending=min(w.n_batches, 8))
+    load_synthetic_kv(v, w)
+    streams = [torch.cuda.Stream() for _ in range(min(w.n_batches, 2))]
+    batches = [w.batch(n) for n in range(w.n_batches)]
+    dev = [batch_to_device(b) for b in batches]
+    for b in batches:
+        for i, u in enumerate(b.users):
+            v.reset_user(int(u), int(b.prefix_len[i]), int(b.root[i]))
+    torch.cuda.synchronize()
+    # all batches in flight on alternating streams, as the benchmark runs them
+    for n in range(w.n_batches):
+        d, q, au = dev[n]
+        v.verify(n, w.assign, w.draft_len, d, q, mode, seed=w.seed, round_=0, accept_u=au,
+                 stream=streams[n % len(streams)])
+    torch.cuda.synchronize()
+    out = []
+    for n, b in enumerate(batches):
+        lg = v.logits(n, b.T).cpu().numpy()
+        n_acc, tok = v.accept(n, w.n_users)
+        so = np.concatenate([[0], np.cumsum(b.n_slots)])
+        do = np.concatenate([[0], np.cumsum(b.draft_len)])
+        for i in _pick(w, n, b):
+            u, L = int(b.users[i]), int(b.draft_len[i])
+            out.append(Sampled(
+                name, u, int(b.prefix_len[i]), L,
+                b.slot_tokens()[so[i]:so[i + 1]], b.drafts[do[i]:do[i + 1]], b.q[do[i]:do[i + 1]],
+                None if b.accept_u is None else b.accept_u[do[i]:do[i + 1]],
+                lg[so[i]:so[i + 1]].copy(), int(n_acc[u]), int(tok[u])))
+    v.close()
+    del v, dev
+    torch.cuda.empty_cache()
+    return w, out
+
+
+@pytest.fixture(scope="module")
+def results32():
+    m = wl.MODELS["qwen3-32b"]
+    dw = DeviceWeights(m, SEED32)
+    samples, seeds = [], {}
+    for name in WORKLOADS32:
+        w, s = _run_workload(name, dw)
+        seeds[name] = w.seed
+        samples += s
+        print(f"{name}: GPU done, {len(s)} users sampled", flush=True)
+    del dw
+    torch.cuda.empty_cache()
+    # one oracle pass over every sampled user (each with its own prefix)
+    users = [s.user for s in samples]
+    prefix = [s.prefix for s in samples]
+    kv = oracle.KVSource(m, SEED32, users, prefix)
+    ref = oracle.forward(m, oracle.WeightSource(m, SEED32), kv, prefix, [s.L + 1 for s in samples],
+                         np.concatenate([s.tokens for s in samples]))
+    print("oracle forward done", flush=True)
+    return samples, ref, seeds
+
+
+def _compare(samples, ref_logits, seed, label):
+    off = np.concatenate([[0], np.cumsum([s.L + 1 for s in samples])])
+    worst = 0.0
+    for k, s in enumerate(samples):
+        rl = ref_logits[off[k]:off[k + 1]]
+        err = logit_rel_err(s.logits, rl)
+        worst = max(worst, float(err.max()))
+        assert err.max() < TOL, f"{label} user {s.user}: logit error {err.max()}"
+        res = oracle.sample("stochastic", [s.user], [s.L], rl, s.drafts, s.q, s.accept_u, seed, 0)
+        extra = np.expm1(2.0 * np.array([float(np.max(np.abs(s.logits - rl)))]))
+        bad, border = compare_decisions([s.n_acc], [s.token], res, [s.L], extra=extra)
+        print(f"{label} user {s.user} (prefix {s.prefix}, l {s.L}): rel err {err.max():.2e}, "
+              f"n_acc {s.n_acc}/{res['n_acc'][0]}, token {s.token}/{res['token'][0]}, "
+              f"mismatch {bad}, borderline {border}")
+        assert bad == 0
+    return worst
+
+
+@pytest.mark.parametrize("name", WORKLOADS32)
+def test_qwen3_32b_sampled_users_match_oracle(results32, name):
+    samples, ref, seeds = results32
+    off = np.concatenate([[0], np.cumsum([s.L + 1 for s in samples])])
+    mine = [k for k, s in enumerate(samples) if s.workload == name]
+    assert mine
+    rows = np.concatenate([np.arange(off[k], off[k + 1]) for k in mine])
+    _compare([samples[k] for k in mine], ref[rows], seeds[name], name)
+
+
+def test_qwen3_1p7b_full_batch_matches_oracle():
+    w = wl.workload("qwen3-1.7b-b8")
+    m = w.model
+    dw = DeviceWeights(m, w.seed)
+    v = make_verifier(w, dw)
+    load_synthetic_kv(v, w)
+    b = w.batch(0)
+    for i, u in enumerate(b.users):
+        v.reset_user(int(u), int(b.prefix_len[i]), int(b.root[i]))
+    d, q, au = batch_to_device(b)
+    v.verify(0, w.assign, w.draft_len, d, q, "stochastic", seed=w.seed, round_=0, accept_u=au)
+    lg = v.logits(0, b.T).cpu().numpy()
+    n_acc, tok = v.accept(0, w.n_users)
+    v.close()
+    del dw
+    torch.cuda.empty_cache()
+    ref = oracle.forward(m, oracle.WeightSource(m, w.seed),
+                         oracle.KVSource(m, w.seed, b.users, b.prefix_len), b.prefix_len, b.n_slots,
+                         b.slot_tokens())
+    err = logit_rel_err(lg, ref)
+    print(f"qwen3-1.7b-b8: logit rel err max {err.max():.3e} mean {err.mean():.3e}")
+    assert err.max() < TOL
+    res = oracle.sample("stochastic", b.users, b.draft_len, ref, b.drafts, b.q, b.accept_u, w.seed, 0)
+    per_user = []
+    o = 0
+    for n in b.n_slots:
+        per_user.append(float(np.max(np.abs(lg[o:o + n] - ref[o:o + n]))))
+        o += int(n)
+    bad, border = compare_decisions(n_acc[b.users], tok[b.users], res, b.draft_len,
+                                    extra=np.expm1(2.0 * np.array(per_user)))
+    print(f"qwen3-1.7b-b8: decision mismatches {bad}, borderline {border}")
+    assert bad == 0
+
+
+@pytest.fixture(scope="module")
+def b16():
+    w = wl.workload("qwen3-32b-b16")
+    dw = DeviceWeights(w.model, w.seed)
+    v = make_verifier(w, dw)
+    load_synthetic_kv(v, w)
+    b = w.batch(0)
+    for i, u in enumerate(b.users):
+        v.reset_user(int(u), int(b.prefix_len[i]), int(b.root[i]))
+    yield w, v, b
+    v.close()
+    del dw
+    torch.cuda.empty_cache()
+
+
+def _slot_rows(b):
+    so = np.concatenate([[0], np.cumsum(b.n_slots)])
+    do = np.concatenate([[0], np.cumsum(b.draft_len)])
+    return so, do
+
+
+def test_qwen3_32b_q_equal_p_accepts_every_draft(b16):
+    """With each draft row q equal to the target distribution the draft is
+    judged by (computed from the GPU's own logits of a first pass, drafts
+    unchanged), every draft is accepted: p/q = 1 > u up to rounding."""
+    w, v, b = b16
+    d, q, au = batch_to_device(b)
+    v.verify(0, w.assign, w.draft_len, d, q, "force")
+    lg = v.logits(0, b.T)
+    v.accept(0, w.n_users)
+    so, do = _slot_rows(b)
+    p = torch.softmax(lg, dim=1)
+    for i in range(len(b.users)):
+        for j in range(int(b.draft_len[i])):
+            q[do[i] + j] = p[so[i] + j]
+    v.verify(0, w.assign, w.draft_len, d, q, "stochastic", seed=5, round_=1)
+    n_acc, _ = v.accept(0, w.n_users)
+    assert np.array_equal(n_acc[b.users], b.draft_len), (n_acc[b.users], b.draft_len)
+
+
+def test_qwen3_32b_greedy_planted_prefix(b16):
+    """Greedy mode at full size: drafts that follow the target's own argmax
+    for k_m steps and then deviate give n_acc = k_m and the target's argmax
+    at slot k_m as the correction (or bonus) token."""
+    w, v, b = b16
+    rng = np.random.default_rng(7)
+    k = rng.integers(0, b.draft_len + 1)
+    drafts = b.drafts.copy()
+    so, do = _slot_rows(b)
+    d, q, au = batch_to_device(b)
+    for j in range(int(b.draft_len.max())):
+        d.copy_(torch.from_numpy(drafts))
+        v.verify(0, w.assign, w.draft_len, d, q, "force")
+        am = v.logits(0, b.T).argmax(dim=1).cpu().numpy()
+        v.accept(0, w.n_users)
+        for i in range(len(b.users)):
+            if j < b.draft_len[i]:
+                if j < k[i]:
+                    drafts[do[i] + j] = am[so[i] + j]
+                elif j == k[i]:
+                    drafts[do[i] + j] = (am[so[i] + j] + 1) % w.model.vocab
+    d.copy_(torch.from_numpy(drafts))
+    v.verify(0, w.assign, w.draft_len, d, q, "greedy")
+    am = v.logits(0, b.T).argmax(dim=1).cpu().numpy()
+    n_acc, tok = v.accept(0, w.n_users)
+    for i, u in enumerate(b.users):
+        assert n_acc[u] == k[i], (i, n_acc[u], k[i])
+        assert tok[u] == am[so[i] + k[i]]
+
+
+def test_qwen3_32b_two_runs_bit_identical(b16):
+    w, v, b = b16
+    d, q, au = batch_to_device(b)
+    outs = []
+    for _ in range(2):
+        v.verify(0, w.assign, w.draft_len, d, q, "stochastic", seed=w.seed, round_=0)
+        lg = v.logits(0, b.T).cpu().numpy()
+        n_acc, tok = v.accept(0, w.n_users)
+        outs.append((lg, n_acc.copy(), tok.copy()))
+    assert np.array_equal(outs[0][0].view(np.uint32), outs[1][0].view(np.uint32))
+    assert np.array_equal(outs[0][1], outs[1][1]) and np.array_equal(outs[0][2], outs[1][2])
