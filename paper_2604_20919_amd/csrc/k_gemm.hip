@@ -160,23 +160,35 @@ void k_gemm_bf16(GemmP p) {
                 w[ks][s] = __builtin_bit_cast(
                     bf16x8, __builtin_amdgcn_raw_buffer_load_b128(wres, woff[s], (c * KS + ks) * 1024, 0));
     };
+    // The X fragments of a group of slot tiles are read before their MFMAs
+    // (all tiles of the k-step up to 8 tiles, groups of 4 above), and every
+    // slot tile of the class is computed (tiles past T multiply clamped
+    // copies of row T-1 and are never stored): a per-tile branch would
+    // serialise LDS latency and MFMAs tile by tile.
+    constexpr int MG = MT <= 8 ? MT : 4;
     auto compute = [&](int buf, const bf16x8 (&w)[KS][NSUB]) {
         const bf16_t* xb = xs[buf];
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
-            for (int m = 0; m < MT; ++m) {
-                if (m < mt_act) {
+            for (int m0 = 0; m0 < MT; m0 += MG) {
+                bf16x8 xf[PL][MG];
 #pragma unroll
-                    for (int pl = 0; pl < PL; ++pl) {
-                        const bf16x8 xf = *(const bf16x8*)(xb + pl * PLANE + (m * 16 + lr) * LDX +
-                                                           ks * 32 + 8 * lg);
+                for (int pl = 0; pl < PL; ++pl)
 #pragma unroll
-                        for (int s = 0; s < NSUB; ++s)
-                            acc[s][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[ks][s], xf,
-                                                                                 acc[s][m], 0, 0, 0);
-                    }
-                }
+                    for (int g = 0; g < MG; ++g)
+                        if (m0 + g < MT)
+                            xf[pl][g] = *(const bf16x8*)(xb + pl * PLANE + ((m0 + g) * 16 + lr) * LDX +
+                                                         ks * 32 + 8 * lg);
+#pragma unroll
+                for (int g = 0; g < MG; ++g)
+                    if (m0 + g < MT)
+#pragma unroll
+                        for (int pl = 0; pl < PL; ++pl)
+#pragma unroll
+                            for (int s = 0; s < NSUB; ++s)
+                                acc[s][m0 + g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                    w[ks][s], xf[pl][g], acc[s][m0 + g], 0, 0, 0);
             }
         }
     };
@@ -333,24 +345,33 @@ __global__ void k_gemm_f32(GemmF p) {
 // ---------------------------------------------------------------------------
 
 // Tile shape per slot-count class: MT slot tiles of 16, NSUB weight
-// sub-tiles of 16 rows per wave, KC k elements per pipeline chunk, NW waves
-// per workgroup.  Eight waves share one staged X chunk where the row count
-// allows (it halves the X staging per weight byte; measured 96 vs 107 us
-// for the 32B gate/up at T = 80); more than 12 slot tiles need the larger
-// register budget of one wave per SIMD, so they use four, and above 16 slot
-// tiles the chunk shrinks to 32 k so that the two activation planes of a
-// double-buffered chunk fit in LDS.
-struct GemmShape { int MT, NSUB, KC, NW; };
+// sub-tiles of 16 rows per wave, KC k elements per pipeline chunk, PD chunks
+// of prefetch, NW waves per workgroup.  Measured on the 32B shapes (two
+// activation planes):
+//   * eight waves share one staged X chunk where the row count allows; it
+//     halves the X staging per weight byte (gate/up at T = 80: 107 -> 96 us
+//     with one plane);
+//   * up to 8 slot tiles, 128-k chunks with one chunk of prefetch (fewer
+//     barriers per weight byte: gate/up 124 -> 120 us);
+//   * more than 12 slot tiles need the register budget of one wave per
+//     SIMD (four waves); above 16 the chunk shrinks to 32 k so that a
+//     double-buffered two-plane chunk fits in LDS, with one chunk of
+//     prefetch so that the staging registers fit beside the accumulators;
+//   * classes follow the slot count closely: padded slot tiles cost MFMA
+//     issue and LDS reads (down projection at T = 80: 61 us with 6 tiles,
+//     57 us with 5).
+struct GemmShape { int MT, NSUB, KC, NW, PD; };
 
 static GemmShape shape_for(int T, int vcols) {
     const int mt = (T + 15) / 16;
-    static const int classes[] = {2, 4, 6, 8, 12, 16, 20, 26};
+    static const int classes[] = {2, 3, 4, 5, 6, 7, 8, 10, 12, 16, 20, 26};
     for (int c : classes)
         if (mt <= c) {
-            const int nw = (c <= 12 && vcols % (16 * 2 * 8) == 0) ? 8 : 4;
-            return {c, 2, c > 16 ? 32 : 64, nw};
+            const bool wide = c <= 12 && vcols % (16 * 2 * 8) == 0;
+            if (wide) return c <= 8 ? GemmShape{c, 2, 128, 8, 1} : GemmShape{c, 2, 64, 8, 2};
+            return c > 16 ? GemmShape{c, 2, 32, 4, 1} : GemmShape{c, 2, 64, 4, 2};
         }
-    return {0, 0, 0, 0};
+    return {0, 0, 0, 0, 0};
 }
 
 typedef void (*GemmFn)(GemmP);
@@ -358,13 +379,13 @@ typedef void (*ReduceFn)(GemmP);
 
 // Activations always come as two planes (hi, lo); split-K kernels write raw
 // partial planes and the epilogue runs in the reducer.
-template <int MT, int NW, int KC, bool SPLIT>
+template <int MT, int NW, int KC, int PD, bool SPLIT>
 static GemmFn pick_epi(int epi) {
-    if (SPLIT) return k_gemm_bf16<MT, 2, KC, EPI_STORE, true, NW, 2>;
+    if (SPLIT) return k_gemm_bf16<MT, 2, KC, EPI_STORE, true, NW, 2, PD>;
     switch (epi) {
-        case EPI_RESID: return k_gemm_bf16<MT, 2, KC, EPI_RESID, false, NW, 2>;
-        case EPI_SWIGLU: return k_gemm_bf16<MT, 2, KC, EPI_SWIGLU, false, NW, 2>;
-        default: return k_gemm_bf16<MT, 2, KC, EPI_STORE, false, NW, 2>;
+        case EPI_RESID: return k_gemm_bf16<MT, 2, KC, EPI_RESID, false, NW, 2, PD>;
+        case EPI_SWIGLU: return k_gemm_bf16<MT, 2, KC, EPI_SWIGLU, false, NW, 2, PD>;
+        default: return k_gemm_bf16<MT, 2, KC, EPI_STORE, false, NW, 2, PD>;
     }
 }
 
@@ -372,23 +393,31 @@ template <bool SPLIT>
 static GemmFn pick(const GemmShape& sh, int epi) {
     if (sh.NW == 8) {
         switch (sh.MT) {
-            case 2: return pick_epi<2, 8, 64, SPLIT>(epi);
-            case 4: return pick_epi<4, 8, 64, SPLIT>(epi);
-            case 6: return pick_epi<6, 8, 64, SPLIT>(epi);
-            case 8: return pick_epi<8, 8, 64, SPLIT>(epi);
-            case 12: return pick_epi<12, 8, 64, SPLIT>(epi);
+            case 2: return pick_epi<2, 8, 128, 1, SPLIT>(epi);
+            case 3: return pick_epi<3, 8, 128, 1, SPLIT>(epi);
+            case 4: return pick_epi<4, 8, 128, 1, SPLIT>(epi);
+            case 5: return pick_epi<5, 8, 128, 1, SPLIT>(epi);
+            case 6: return pick_epi<6, 8, 128, 1, SPLIT>(epi);
+            case 7: return pick_epi<7, 8, 128, 1, SPLIT>(epi);
+            case 8: return pick_epi<8, 8, 128, 1, SPLIT>(epi);
+            case 10: return pick_epi<10, 8, 64, 2, SPLIT>(epi);
+            case 12: return pick_epi<12, 8, 64, 2, SPLIT>(epi);
         }
         return nullptr;
     }
     switch (sh.MT) {
-        case 2: return pick_epi<2, 4, 64, SPLIT>(epi);
-        case 4: return pick_epi<4, 4, 64, SPLIT>(epi);
-        case 6: return pick_epi<6, 4, 64, SPLIT>(epi);
-        case 8: return pick_epi<8, 4, 64, SPLIT>(epi);
-        case 12: return pick_epi<12, 4, 64, SPLIT>(epi);
-        case 16: return pick_epi<16, 4, 64, SPLIT>(epi);
-        case 20: return pick_epi<20, 4, 32, SPLIT>(epi);
-        case 26: return pick_epi<26, 4, 32, SPLIT>(epi);
+        case 2: return pick_epi<2, 4, 64, 2, SPLIT>(epi);
+        case 3: return pick_epi<3, 4, 64, 2, SPLIT>(epi);
+        case 4: return pick_epi<4, 4, 64, 2, SPLIT>(epi);
+        case 5: return pick_epi<5, 4, 64, 2, SPLIT>(epi);
+        case 6: return pick_epi<6, 4, 64, 2, SPLIT>(epi);
+        case 7: return pick_epi<7, 4, 64, 2, SPLIT>(epi);
+        case 8: return pick_epi<8, 4, 64, 2, SPLIT>(epi);
+        case 10: return pick_epi<10, 4, 64, 2, SPLIT>(epi);
+        case 12: return pick_epi<12, 4, 64, 2, SPLIT>(epi);
+        case 16: return pick_epi<16, 4, 64, 2, SPLIT>(epi);
+        case 20: return pick_epi<20, 4, 32, 1, SPLIT>(epi);
+        case 26: return pick_epi<26, 4, 32, 1, SPLIT>(epi);
     }
     return nullptr;
 }
