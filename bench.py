@@ -147,8 +147,11 @@ def main():
 
     # ---- roofline of the dominant kernel (gate/up GEMM + SwiGLU), timed live ----
     T = batches[0].T
-    per_layer_w = 2 * m.d_ffn * m.d_model * 2
-    gu_bytes = per_layer_w + T * m.d_model * 2 + T * m.d_ffn * 2
+    per_layer_w = 2 * m.d_ffn * m.d_model * m.wbytes
+    # weights once, plus the activation input and SwiGLU output at 4 B per
+    # element: two bf16 planes (hi, lo) in the bf16 path, fp32 otherwise
+    act_bytes = 4
+    gu_bytes = per_layer_w + T * m.d_model * act_bytes + T * m.d_ffn * act_bytes
     prof_steps = max(3, args.steps // 2)
     sv.sd_profile_begin(v.ctx, sv.SD_K_GATEUP, prof_steps * nb * m.n_layers + 8)
     for _ in range(prof_steps):
@@ -164,7 +167,7 @@ def main():
     gu_avg_s = max(gu_ms / max(gu_n, 1) - pair_ms, 1e-6) / 1e3
     achieved = gu_bytes / gu_avg_s / 1e9
     traffic = measured_traffic(args.workload)
-    roofline = {"bound": "hbm", "kernel": "k_gemm_bf16 (gate/up + SwiGLU epilogue)",
+    roofline = {"bound": "hbm", "kernel": "k_gemm16/k_gemm32 (gate/up + SwiGLU epilogue)",
                 "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "traffic_over_algorithmic": round(traffic / gu_bytes, 4) if traffic else None,

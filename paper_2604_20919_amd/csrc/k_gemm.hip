@@ -1,26 +1,34 @@
 // Skinny GEMMs of the verify forward: Y[t][n] = sum_k X[t][k] W[n][k] for
 // T = sum(l_m + 1) query slots (tens to a few hundred) against weight
 // matrices of thousands of rows.  At these shapes the work is bound by
-// streaming the weights from HBM once, so the kernel is built around that
+// streaming the weights from HBM once, so the kernels are built around that
 // stream:
 //   * weights are repacked once (at init) into fragment order: the A operand
 //     of v_mfma_f32_16x16x32_bf16 for 16 weight rows x 32 k is one 1 KB block
-//     laid out lane by lane, and the blocks of a 16-row group follow each
-//     other along k, so every wave-wide weight load reads 1 KB contiguously;
+//     laid out lane by lane (lane l: row l % 16, k 8*(l/16)..+7), and the
+//     blocks of a 16-row group follow each other along k, so a wave-wide
+//     weight load reads 1 KB (or, for the 32x32 form, two 512-byte runs)
+//     contiguously;
+//   * two MFMA forms share that layout: 16x16x32 tiles (16 slots per tile)
+//     for small slot counts, where their finer slot padding wins, and
+//     32x32x16 tiles (32 slots per tile) above, where the form's higher
+//     rate (measured 2.1 vs 1.2 PFLOP/s) wins; every product runs twice, once
+//     per activation plane, so the MFMA rate matters even here;
 //   * the activation chunk X[0:T][k0:k0+KC] is staged in LDS (double
-//     buffered) and read by the 4 waves of the workgroup as the B operand
-//     (32 k x 16 slots);
+//     buffered) and read by all waves of the workgroup as the B operand;
+//     activations come as two bf16 planes (hi, lo = x - hi) that are
+//     multiplied separately, which carries them at about 16 significant bits;
 //   * software pipeline per chunk: the loads of X(c+1) are issued before the
 //     weight loads of chunk c+1, so storing X(c+1) to LDS after computing
 //     chunk c waits for X only and the weight prefetch stays in flight;
-//   * each wave owns NSUB groups of 16 weight rows and all T slots, so every
+//   * each wave owns a fixed set of weight rows and all T slots, so every
 //     weight byte is read once per call;
 //   * when there are too few column tiles to fill the GPU the k range is
 //     split over S workgroups; partial sums are written to a workspace and a
-//     second kernel adds them in split order and applies the epilogue (no
-//     device-wide fences, deterministic results);
+//     second kernel (or a fused consumer) adds them in split order and
+//     applies the epilogue (no device-wide fences, deterministic results);
 //   * epilogues: fp32 store, residual add into the fp32 stream, or SwiGLU
-//     silu(g) * u with gate/up rows interleaved per wave.
+//     silu(g) * u with gate/up rows interleaved per 16-row group.
 // An fp32 fallback (plain FMA loop) serves the fp32 model configuration.
 #include <algorithm>
 
@@ -32,7 +40,7 @@ namespace sdv {
 struct GemmP {
     const bf16_t* X;
     const bf16_t* Wp;  // packed weights: [vcols/16][K/32][64 lanes][8]
-    int K, KT, T, S, kchunks, tiles;
+    int K, KT, T, S, kchunks, tiles;  // KT = K / 32 fragments per 16-row group
     float* part;     // [S][T][vcols] when S > 1
     int vcols;
     void* out;
@@ -69,9 +77,12 @@ __device__ __forceinline__ void swiglu_store4(const GemmP& p, int t, int col, f3
     *(uint2*)(o + p.oplane) = uint2{lo[0] | (lo[1] << 16), lo[2] | (lo[3] << 16)};
 }
 
-template <int MT, int NSUB, int KC, int EPI, bool SPLIT, int NW, int PL, int PD = 2>
+// 16x16x32 form.  MT: 16-slot tiles; NSUB: 16-row weight groups per wave;
+// KC: k per chunk (a multiple of 32); NW: waves per workgroup; PL:
+// activation planes; PD: chunks of prefetch.
+template <int MT, int NSUB, int KC, int EPI, bool SPLIT, int NW, int PL, int PD>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, 2)))
-void k_gemm_bf16(GemmP p) {
+void k_gemm16(GemmP p) {
     constexpr int NTH = 64 * NW;         // threads per workgroup
     constexpr int NT = NW * NSUB * 16;   // virtual columns per tile
     constexpr int KS = KC / 32;          // MFMA k-steps per chunk
@@ -241,6 +252,194 @@ void k_gemm_bf16(GemmP p) {
     }
 }
 
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// 32x32x16 form.  MT: 32-slot tiles; NS: 32-row weight groups (pairs of
+// 16-row groups) per wave; KC: k per chunk (a multiple of 16); NW: waves per
+// workgroup; PL: activation planes; PD: chunks of prefetch.
+template <int MT, int NS, int KC, int EPI, bool SPLIT, int NW, int PL, int PD>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, 2)))
+void k_gemm32(GemmP p) {
+    constexpr int NTH = 64 * NW;         // threads per workgroup
+    constexpr int NT = NW * NS * 32;     // virtual columns per tile
+    constexpr int KS = KC / 16;          // MFMA k-steps per chunk
+    constexpr int LDX = KC + 8;          // padded LDS row (bf16 elements)
+    constexpr int PPR = KC / 8;          // 16-byte pieces per staged row
+    constexpr int NPP = MT * 32 * PPR;   // pieces per staged plane
+    constexpr int NPC = PL * NPP;        // pieces per staged chunk (all planes)
+    constexpr int XPT = (NPC + NTH - 1) / NTH;  // X pieces per thread
+    constexpr bool XEVEN = NPC % NTH == 0;
+    constexpr int PLANE = MT * 32 * LDX;  // LDS elements per plane
+    static_assert(2 * PL * PLANE * 2 <= 160 * 1024, "X staging exceeds LDS");
+    __shared__ __attribute__((aligned(16))) bf16_t xs[2][PL * PLANE];
+
+    const int tile = SPLIT ? blockIdx.x / p.S : blockIdx.x;
+    const int split = SPLIT ? blockIdx.x % p.S : 0;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int lc = lane & 31, lh = lane >> 5;
+
+    // Buffer resources: one uniform resource per operand, fixed 32-bit
+    // per-lane offsets, uniform chunk offsets.  Out-of-range reads return 0.
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    const uint64_t wbytes = (uint64_t)p.vcols * (uint64_t)p.K * 2u;
+    const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)p.Wp, (short)0, (int)(wbytes > 0x7fffffffu ? 0x7fffffffu : wbytes), 0x00020000);
+    // The A operand of a 16-k step (lane l: row l % 32, k 8*(l/32)..+7)
+    // taken from the 16-row fragments: rows 0-15 / 16-31 are 16-row groups
+    // 2g / 2g+1; k-step j sits in fragment j/2 at k 16*(j%2), i.e. lane slot
+    // (l % 16) + 16*(l/32) + 32*(j%2).  Per lane that is a fixed offset plus
+    // a uniform 512*j.
+    uint32_t woff[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        const uint32_t g16 = (uint32_t)(((tile * NW + wv) * NS + s) * 2 + (lc >> 4));
+        woff[s] = g16 * (uint32_t)p.KT * 1024u + (uint32_t)((lane & 15) + 16 * lh) * 16u;
+    }
+    const __amdgpu_buffer_rsrc_t xres =
+        __builtin_amdgcn_make_buffer_rsrc((void*)p.X, (short)0, PL * p.T * p.K * 2, 0x00020000);
+
+    f32x16 acc[NS][MT];
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[s][m][e] = 0.f;
+
+    const int c_begin = split * p.kchunks / p.S;
+    const int c_end = (split + 1) * p.kchunks / p.S;
+
+    // Register-ring pipeline with prefetch distance PD chunks: while chunk c
+    // is multiplied (X from LDS buffer c&1, W from ring set c % NB), X and W
+    // of chunk c+PD are requested into ring set (c+PD) % NB, and X(c+1),
+    // requested PD-1 chunks earlier, is stored to the other LDS buffer.  The
+    // loop is unrolled by NB so that ring indices are compile-time constants
+    // (register copies would force waits on loads still in flight), the
+    // loads are unconditional (the chunk index is clamped; the last steps
+    // re-read a cached chunk) and scheduling barriers keep the order issue
+    // loads -> multiply -> store X.  X rows >= T are read as row T-1: they
+    // only feed output slots >= T, which are never stored.
+    constexpr int NB = PD + 1;
+    uint4 xr[NB][XPT];
+    bf16x8 wr[NB][KS][NS];
+    uint32_t xoff[XPT];
+#pragma unroll
+    for (int i = 0; i < XPT; ++i) {
+        const int idx = min((int)threadIdx.x + i * NTH, NPC - 1);
+        const int pl = idx / NPP, pi = idx % NPP;
+        const int r = min(pi / PPR, p.T - 1), cc = pi % PPR;
+        xoff[i] = (((uint32_t)pl * (uint32_t)p.T + (uint32_t)r) * (uint32_t)p.K + (uint32_t)cc * 8u) * 2u;
+    }
+    auto load_x = [&](uint4 (&x)[XPT], int c) {
+        const int so = c * KC * 2;
+#pragma unroll
+        for (int i = 0; i < XPT; ++i)
+            x[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xres, xoff[i], so, 0));
+    };
+    auto store_x = [&](const uint4 (&x)[XPT], int buf) {
+#pragma unroll
+        for (int i = 0; i < XPT; ++i) {
+            const int idx = threadIdx.x + i * NTH;
+            const int pl = idx / NPP, pi = idx % NPP;
+            if (XEVEN || idx < NPC)
+                *(uint4*)(&xs[buf][pl * PLANE + (pi / PPR) * LDX + (pi % PPR) * 8]) = x[i];
+        }
+    };
+    auto load_w = [&](bf16x8 (&w)[KS][NS], int c) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+            for (int s = 0; s < NS; ++s)
+                w[ks][s] = __builtin_bit_cast(
+                    bf16x8, __builtin_amdgcn_raw_buffer_load_b128(wres, woff[s], (c * KS + ks) * 512, 0));
+    };
+    // The B fragments of a k-step (lane l: slot l % 32 of the tile, k
+    // 8*(l/32)..+7) are read for all tiles before their MFMAs, one k-step
+    // ahead, and every slot tile of the class is computed (tiles past T
+    // multiply clamped copies of row T-1 and are never stored).  MFMAs on one
+    // accumulator are MT*NS instructions apart (planes outermost).
+    auto read_x = [&](bf16x8 (&xf)[PL][MT], const bf16_t* xb, int ks) {
+#pragma unroll
+        for (int pl = 0; pl < PL; ++pl)
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+                xf[pl][m] = *(const bf16x8*)(xb + pl * PLANE + (m * 32 + lc) * LDX + ks * 16 + 8 * lh);
+    };
+    auto compute = [&](int buf, const bf16x8 (&w)[KS][NS]) {
+        const bf16_t* xb = xs[buf];
+        bf16x8 xf[2][PL][MT];
+        read_x(xf[0], xb, 0);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            if (ks + 1 < KS) read_x(xf[(ks + 1) & 1], xb, ks + 1);
+#pragma unroll
+            for (int pl = 0; pl < PL; ++pl)
+#pragma unroll
+                for (int m = 0; m < MT; ++m)
+#pragma unroll
+                    for (int s = 0; s < NS; ++s)
+                        acc[s][m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w[ks][s], xf[ks & 1][pl][m],
+                                                                             acc[s][m], 0, 0, 0);
+        }
+    };
+
+    const int c_last = c_end - 1;
+#pragma unroll
+    for (int u = 0; u < PD; ++u) {
+        load_x(xr[u], min(c_begin + u, c_last));
+        load_w(wr[u], min(c_begin + u, c_last));
+    }
+    store_x(xr[0], 0);
+    __syncthreads();
+    for (int c0 = c_begin; c0 < c_end; c0 += NB) {
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            const int c = c0 + u;
+            if (c >= c_end) break;
+            load_x(xr[(u + PD) % NB], min(c + PD, c_last));
+            load_w(wr[(u + PD) % NB], min(c + PD, c_last));
+            __builtin_amdgcn_sched_barrier(0);
+            compute((c - c_begin) & 1, wr[u]);
+            __builtin_amdgcn_sched_barrier(0);
+            store_x(xr[(u + 1) % NB], ((c - c_begin) & 1) ^ 1);
+            __syncthreads();
+        }
+    }
+
+    // Accumulator layout: lane l holds slot t = 32*m + l % 32 and, in
+    // registers 4q..4q+3, weight rows 8q + 4*(l/32) + 0..3 of its group.
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+        const int t = m * 32 + lc;
+        if (t >= p.T) continue;
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            const int grp = (tile * NW + wave) * NS + s;
+            if (SPLIT) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int v = grp * 32 + 8 * q + 4 * lh;
+                    *(f32x4*)(p.part + ((size_t)split * p.T + t) * p.vcols + v) =
+                        f32x4{acc[s][m][4 * q], acc[s][m][4 * q + 1], acc[s][m][4 * q + 2], acc[s][m][4 * q + 3]};
+                }
+            } else if (EPI == EPI_SWIGLU) {
+                // rows 0-15 of the group are gate rows 16*grp.., 16-31 the
+                // matching up rows; both sit in the same lane
+#pragma unroll
+                for (int q = 0; q < 2; ++q)
+                    swiglu_store4(p, t, grp * 16 + 8 * q + 4 * lh,
+                                  f32x4{acc[s][m][4 * q], acc[s][m][4 * q + 1], acc[s][m][4 * q + 2], acc[s][m][4 * q + 3]},
+                                  f32x4{acc[s][m][4 * q + 8], acc[s][m][4 * q + 9], acc[s][m][4 * q + 10], acc[s][m][4 * q + 11]});
+            } else {
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    epi_store4<EPI>(p, t, grp * 32 + 8 * q + 4 * lh,
+                                    f32x4{acc[s][m][4 * q], acc[s][m][4 * q + 1], acc[s][m][4 * q + 2], acc[s][m][4 * q + 3]});
+            }
+        }
+    }
+}
+
 // Sum of the S split-K partials (in split order) plus the epilogue; one
 // thread per 4 output columns of one slot.
 template <int EPI>
@@ -344,34 +543,38 @@ __global__ void k_gemm_f32(GemmF p) {
 // host-side configuration
 // ---------------------------------------------------------------------------
 
-// Tile shape per slot-count class: MT slot tiles of 16, NSUB weight
-// sub-tiles of 16 rows per wave, KC k elements per pipeline chunk, PD chunks
-// of prefetch, NW waves per workgroup.  Measured on the 32B shapes (two
-// activation planes):
-//   * eight waves share one staged X chunk where the row count allows; it
-//     halves the X staging per weight byte (gate/up at T = 80: 107 -> 96 us
-//     with one plane);
-//   * up to 8 slot tiles, 128-k chunks with one chunk of prefetch (fewer
-//     barriers per weight byte: gate/up 124 -> 120 us);
-//   * more than 12 slot tiles need the register budget of one wave per
-//     SIMD (four waves); above 16 the chunk shrinks to 32 k so that a
-//     double-buffered two-plane chunk fits in LDS, with one chunk of
-//     prefetch so that the staging registers fit beside the accumulators;
-//   * classes follow the slot count closely: padded slot tiles cost MFMA
-//     issue and LDS reads (down projection at T = 80: 61 us with 6 tiles,
-//     57 us with 5).
-struct GemmShape { int MT, NSUB, KC, NW, PD; };
+// Tile shape per slot-count class: form F (16: 16x16x32 MFMA, 16-slot
+// tiles, NSUB = 2 row groups of 16 per wave; 32: 32x32x16 MFMA, 32-slot
+// tiles, one 32-row group per wave), MT slot tiles, KC k elements per
+// pipeline chunk, PD chunks of prefetch, NW waves per workgroup.  Measured
+// on the 32B shapes (two activation planes):
+//   * eight waves (256 weight rows) share one staged X chunk where the row
+//     count allows; it halves the X staging per weight byte;
+//   * up to 96 slots the 16x16 form (128-k chunks, one chunk of prefetch)
+//     wins: at T = 80 its 5 slot tiles pad nothing, where the 32x32 form
+//     computes 96 slots (gate/up 113 vs 119 us in the full step);
+//   * above, the 32x32 form wins by its MFMA rate: gate/up at T = 128 / 176
+//     / 240 takes 141 / 188 / 390 us against 181 / 237 / 509 us;
+//   * above 224 slots tiles need the register budget of one wave per SIMD
+//     (four waves) and shorter chunks so that a double-buffered two-plane
+//     chunk fits in LDS.
+struct GemmShape { int F, MT, NSUB, KC, NW, PD; };
+
+constexpr int kT32 = 97;  // first slot count served by the 32x32 form
 
 static GemmShape shape_for(int T, int vcols) {
-    const int mt = (T + 15) / 16;
-    static const int classes[] = {2, 3, 4, 5, 6, 7, 8, 10, 12, 16, 20, 26};
-    for (int c : classes)
-        if (mt <= c) {
-            const bool wide = c <= 12 && vcols % (16 * 2 * 8) == 0;
-            if (wide) return c <= 8 ? GemmShape{c, 2, 128, 8, 1} : GemmShape{c, 2, 64, 8, 2};
-            return c > 16 ? GemmShape{c, 2, 32, 4, 1} : GemmShape{c, 2, 64, 4, 2};
-        }
-    return {0, 0, 0, 0, 0};
+    const bool wide = vcols % 256 == 0;
+    if (T < kT32) {
+        const int mt = std::max(2, (T + 15) / 16);
+        return wide ? GemmShape{16, mt, 2, 128, 8, 1} : GemmShape{16, mt, 2, 64, 4, 2};
+    }
+    const int mt = (T + 31) / 32;
+    if (mt <= 4) return wide ? GemmShape{32, mt, 1, 64, 8, 2} : GemmShape{32, mt, 1, 64, 4, 2};
+    if (mt <= 7) return wide ? GemmShape{32, mt, 1, 64, 8, 1} : GemmShape{32, mt, 1, 64, 4, 1};
+    if (mt <= 8) return {32, 8, 1, 64, 4, 1};
+    if (mt <= 10) return {32, 10, 1, 32, 4, 1};
+    if (mt <= 13) return {32, 13, 1, 16, 4, 1};
+    return {0, 0, 0, 0, 0, 0};
 }
 
 typedef void (*GemmFn)(GemmP);
@@ -379,47 +582,53 @@ typedef void (*ReduceFn)(GemmP);
 
 // Activations always come as two planes (hi, lo); split-K kernels write raw
 // partial planes and the epilogue runs in the reducer.
-template <int MT, int NW, int KC, int PD, bool SPLIT>
+template <int F, int MT, int NW, int KC, int PD, bool SPLIT>
 static GemmFn pick_epi(int epi) {
-    if (SPLIT) return k_gemm_bf16<MT, 2, KC, EPI_STORE, true, NW, 2, PD>;
-    switch (epi) {
-        case EPI_RESID: return k_gemm_bf16<MT, 2, KC, EPI_RESID, false, NW, 2, PD>;
-        case EPI_SWIGLU: return k_gemm_bf16<MT, 2, KC, EPI_SWIGLU, false, NW, 2, PD>;
-        default: return k_gemm_bf16<MT, 2, KC, EPI_STORE, false, NW, 2, PD>;
+    if constexpr (F == 16) {
+        if (SPLIT) return k_gemm16<MT, 2, KC, EPI_STORE, true, NW, 2, PD>;
+        switch (epi) {
+            case EPI_RESID: return k_gemm16<MT, 2, KC, EPI_RESID, false, NW, 2, PD>;
+            case EPI_SWIGLU: return k_gemm16<MT, 2, KC, EPI_SWIGLU, false, NW, 2, PD>;
+            default: return k_gemm16<MT, 2, KC, EPI_STORE, false, NW, 2, PD>;
+        }
+    } else {
+            if (SPLIT) return k_gemm32<MT, 1, KC, EPI_STORE, true, NW, 2, PD>;
+        switch (epi) {
+            case EPI_RESID: return k_gemm32<MT, 1, KC, EPI_RESID, false, NW, 2, PD>;
+            case EPI_SWIGLU: return k_gemm32<MT, 1, KC, EPI_SWIGLU, false, NW, 2, PD>;
+            default: return k_gemm32<MT, 1, KC, EPI_STORE, false, NW, 2, PD>;
+        }
     }
 }
 
-template <bool SPLIT>
-static GemmFn pick(const GemmShape& sh, int epi) {
-    if (sh.NW == 8) {
+template <int NW, bool SPLIT>
+static GemmFn pick_nw(const GemmShape& sh, int epi) {
+    constexpr int KC16 = NW == 8 ? 128 : 64, PD16 = NW == 8 ? 1 : 2;
+    if (sh.F == 16) {
         switch (sh.MT) {
-            case 2: return pick_epi<2, 8, 128, 1, SPLIT>(epi);
-            case 3: return pick_epi<3, 8, 128, 1, SPLIT>(epi);
-            case 4: return pick_epi<4, 8, 128, 1, SPLIT>(epi);
-            case 5: return pick_epi<5, 8, 128, 1, SPLIT>(epi);
-            case 6: return pick_epi<6, 8, 128, 1, SPLIT>(epi);
-            case 7: return pick_epi<7, 8, 128, 1, SPLIT>(epi);
-            case 8: return pick_epi<8, 8, 128, 1, SPLIT>(epi);
-            case 10: return pick_epi<10, 8, 64, 2, SPLIT>(epi);
-            case 12: return pick_epi<12, 8, 64, 2, SPLIT>(epi);
+            case 2: return pick_epi<16, 2, NW, KC16, PD16, SPLIT>(epi);
+            case 3: return pick_epi<16, 3, NW, KC16, PD16, SPLIT>(epi);
+            case 4: return pick_epi<16, 4, NW, KC16, PD16, SPLIT>(epi);
+            case 5: return pick_epi<16, 5, NW, KC16, PD16, SPLIT>(epi);
+            case 6: return pick_epi<16, 6, NW, KC16, PD16, SPLIT>(epi);
         }
         return nullptr;
     }
     switch (sh.MT) {
-        case 2: return pick_epi<2, 4, 64, 2, SPLIT>(epi);
-        case 3: return pick_epi<3, 4, 64, 2, SPLIT>(epi);
-        case 4: return pick_epi<4, 4, 64, 2, SPLIT>(epi);
-        case 5: return pick_epi<5, 4, 64, 2, SPLIT>(epi);
-        case 6: return pick_epi<6, 4, 64, 2, SPLIT>(epi);
-        case 7: return pick_epi<7, 4, 64, 2, SPLIT>(epi);
-        case 8: return pick_epi<8, 4, 64, 2, SPLIT>(epi);
-        case 10: return pick_epi<10, 4, 64, 2, SPLIT>(epi);
-        case 12: return pick_epi<12, 4, 64, 2, SPLIT>(epi);
-        case 16: return pick_epi<16, 4, 64, 2, SPLIT>(epi);
-        case 20: return pick_epi<20, 4, 32, 1, SPLIT>(epi);
-        case 26: return pick_epi<26, 4, 32, 1, SPLIT>(epi);
+        case 4: return pick_epi<32, 4, NW, 64, 2, SPLIT>(epi);
+        case 5: return pick_epi<32, 5, NW, 64, 1, SPLIT>(epi);
+        case 6: return pick_epi<32, 6, NW, 64, 1, SPLIT>(epi);
+        case 7: return pick_epi<32, 7, NW, 64, 1, SPLIT>(epi);
     }
     return nullptr;
+}
+
+template <bool SPLIT>
+static GemmFn pick(const GemmShape& sh, int epi) {
+    if (sh.F == 32 && sh.MT == 8) return pick_epi<32, 8, 4, 64, 1, SPLIT>(epi);
+    if (sh.F == 32 && sh.MT == 10) return pick_epi<32, 10, 4, 32, 1, SPLIT>(epi);
+    if (sh.F == 32 && sh.MT == 13) return pick_epi<32, 13, 4, 16, 1, SPLIT>(epi);
+    return sh.NW == 8 ? pick_nw<8, SPLIT>(sh, epi) : pick_nw<4, SPLIT>(sh, epi);
 }
 
 static ReduceFn pick_reduce(int epi) {
@@ -483,7 +692,7 @@ bool gemm_shape_ok(const Dims& D, int T, int K, int N, int epi) {
     const int vcols = epi == EPI_SWIGLU ? 2 * N : N;
     const GemmShape sh = shape_for(T, vcols);
     if (sh.MT == 0) return false;
-    return K % sh.KC == 0 && vcols % (16 * sh.NW * sh.NSUB) == 0;
+    return K % sh.KC == 0 && K % 32 == 0 && vcols % (sh.F * sh.NW * sh.NSUB) == 0;
 }
 
 int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_t s) {
@@ -507,7 +716,7 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
     }
     const int vcols = g.epi == EPI_SWIGLU ? 2 * g.N : g.N;
     const GemmShape sh = shape_for(g.T, vcols);
-    const int nt = 16 * sh.NW * sh.NSUB;
+    const int nt = sh.F * sh.NW * sh.NSUB;
     GemmP p;
     p.X = (const bf16_t*)g.X;
     p.Wp = (const bf16_t*)g.Wp;
