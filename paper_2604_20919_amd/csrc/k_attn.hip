@@ -287,7 +287,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 }
 
 // Merge the partials of the chunks of (b, g) for one query row in chunk
-// order; one wave per (slot, query head).
+// order; one wave per (slot, query head).  Chunks are taken eight at a time
+// with all their loads issued before the merge (online maximum: the running
+// sums are rescaled when a group raises it).
 template <typename TA>
 __global__ __launch_bounds__(256) void k_attn_combine(BatchView bv, const float* apart,
                                                       const float* aml, TA* out, int hq, int hkv,
@@ -301,22 +303,41 @@ __global__ __launch_bounds__(256) void k_attn_combine(BatchView bv, const float*
     const int row = j * G + hh;
     const int i0 = bv.item_off[b], nch = (bv.item_off[b + 1] - i0) / hkv;
     const int p0 = i0 + g * nch, p1 = p0 + nch;
-    float M = -INFINITY;
-    for (int pi = p0; pi < p1; ++pi) M = fmaxf(M, aml[((size_t)pi * bv.rows_max + row) * 2]);
-    float Ls = 0.f, acc0 = 0.f, acc1 = 0.f;
-    for (int pi = p0; pi < p1; ++pi) {
-        const size_t pr = (size_t)pi * bv.rows_max + row;
-        const float mi = aml[pr * 2];
-        if (mi == -INFINITY) continue;
-        const float w = exp2f(mi - M);
-        Ls += aml[pr * 2 + 1] * w;
-        acc0 += apart[pr * hd + lane] * w;
-        if (lane + 64 < hd) acc1 += apart[pr * hd + lane + 64] * w;
+    const bool hi_ok = lane + 64 < hd;
+    float M = -INFINITY, Ls = 0.f, acc0 = 0.f, acc1 = 0.f;
+    for (int pg = p0; pg < p1; pg += 8) {
+        float mi[8], li[8], a0[8], a1[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const bool ok = pg + u < p1;
+            const size_t pr = (size_t)(ok ? pg + u : p0) * bv.rows_max + row;
+            mi[u] = ok ? aml[pr * 2] : -INFINITY;
+            li[u] = ok ? aml[pr * 2 + 1] : 0.f;
+            a0[u] = ok && lane < hd ? apart[pr * hd + lane] : 0.f;
+            a1[u] = ok && hi_ok ? apart[pr * hd + lane + 64] : 0.f;
+        }
+        float mg = M;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) mg = fmaxf(mg, mi[u]);
+        if (mg == -INFINITY) continue;  // no key of these chunks is visible to the row
+        const float sc = exp2f(M - mg);  // 0 while M is still -inf
+        Ls *= sc;
+        acc0 *= sc;
+        acc1 *= sc;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            if (mi[u] == -INFINITY) continue;
+            const float w = exp2f(mi[u] - mg);
+            Ls += li[u] * w;
+            acc0 += a0[u] * w;
+            acc1 += a1[u] * w;
+        }
+        M = mg;
     }
     const float inv = 1.0f / Ls;
     const size_t o0 = ((size_t)t * hq + h) * hd, pl = (size_t)bv.T * hq * hd;
     if (lane < hd) st_act(out, pl, o0 + lane, acc0 * inv);
-    if (lane + 64 < hd) st_act(out, pl, o0 + lane + 64, acc1 * inv);
+    if (hi_ok) st_act(out, pl, o0 + lane + 64, acc1 * inv);
 }
 
 // fp32 path: one wave per (slot, query head); lanes split head_dim

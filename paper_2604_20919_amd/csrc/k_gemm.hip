@@ -46,12 +46,40 @@ struct GemmP {
     void* out;
     int ldo;
     size_t oplane;  // SwiGLU: elements between the hi and lo output planes
+    // RMSNorm applied after the product: when nss is set the input planes
+    // hold x * gamma (not normalised) and every output of slot t is scaled
+    // by rstd(t) = 1 / sqrt(sum_b nss[t][b] / K + eps), which commutes with
+    // the product (one factor per slot row)
+    const float* nss;
+    int nnb;
+    float eps;
 };
+
+// block sums of one slot row, all loads issued before the sum (at most
+// kNormKMax / kNormBlock blocks)
+__device__ __forceinline__ void load_row_ss(const GemmP& p, int t, bool on, float (&v)[kNormKMax / kNormBlock]) {
+#pragma unroll
+    for (int b = 0; b < kNormKMax / kNormBlock; ++b)
+        v[b] = on && b < p.nnb ? p.nss[(size_t)t * p.nnb + b] : 0.f;
+}
+__device__ __forceinline__ float rstd_of(const GemmP& p, const float (&v)[kNormKMax / kNormBlock]) {
+    float ss = 0.f;
+#pragma unroll
+    for (int b = 0; b < kNormKMax / kNormBlock; ++b) ss += v[b];
+    return 1.0f / sqrtf(ss / (float)p.K + p.eps);
+}
+__device__ __forceinline__ float row_rstd(const GemmP& p, int t) {
+    if (p.nss == nullptr) return 1.0f;
+    float v[kNormKMax / kNormBlock];
+    load_row_ss(p, t, true, v);
+    return rstd_of(p, v);
+}
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + expf(-g)); }
 
 template <int EPI>
-__device__ __forceinline__ void epi_store4(const GemmP& p, int t, int col, f32x4 v) {
+__device__ __forceinline__ void epi_store4(const GemmP& p, int t, int col, f32x4 v, float sc) {
+    v *= sc;
     float* o = (float*)p.out + (size_t)t * p.ldo + col;
     if (EPI == EPI_RESID) {
         f32x4 x = *(f32x4*)o;
@@ -64,7 +92,10 @@ __device__ __forceinline__ void epi_store4(const GemmP& p, int t, int col, f32x4
 
 // SwiGLU output as the next GEMM's activation planes: hi = bf16(a) at out,
 // lo = bf16(a - hi) one plane (oplane elements) further
-__device__ __forceinline__ void swiglu_store4(const GemmP& p, int t, int col, f32x4 g, f32x4 u) {
+__device__ __forceinline__ void swiglu_store4(const GemmP& p, int t, int col, f32x4 g, f32x4 u,
+                                              float sc) {
+    g *= sc;
+    u *= sc;
     bf16_t* o = (bf16_t*)p.out + (size_t)t * p.ldo + col;
     uint32_t hi[4], lo[4];
 #pragma unroll
@@ -85,6 +116,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, 2)))
 void k_gemm16(GemmP p) {
     constexpr int NTH = 64 * NW;         // threads per workgroup
     constexpr int NT = NW * NSUB * 16;   // virtual columns per tile
+    constexpr int ROWS_PER_TILE = 16;
     constexpr int KS = KC / 32;          // MFMA k-steps per chunk
     constexpr int LDX = KC + 8;          // padded LDS row (bf16 elements)
     constexpr int PPR = KC / 8;          // 16-byte pieces per staged row
@@ -96,6 +128,7 @@ void k_gemm16(GemmP p) {
     static_assert(EPI != EPI_SWIGLU || NSUB % 2 == 0, "SwiGLU pairs gate/up sub-tiles");
     static_assert(2 * PL * PLANE * 2 <= 160 * 1024, "X staging exceeds LDS");
     __shared__ __attribute__((aligned(16))) bf16_t xs[2][PL * PLANE];
+    __shared__ float rsl[SPLIT ? 1 : MT * ROWS_PER_TILE];  // per-slot RMSNorm factor
 
     const int tile = SPLIT ? blockIdx.x / p.S : blockIdx.x;
     const int split = SPLIT ? blockIdx.x % p.S : 0;
@@ -205,10 +238,30 @@ void k_gemm16(GemmP p) {
     };
 
     const int c_last = c_end - 1;
+    // RMSNorm row factors of the tile's slots (epilogues that scale by
+    // them): loads issued ahead of the pipeline prologue, the factors go to
+    // LDS before the first barrier
+    constexpr int NSL = MT * ROWS_PER_TILE;
+    constexpr int NSPT = SPLIT ? 1 : (NSL + NTH - 1) / NTH;  // slots per thread
+    float ssv[NSPT][kNormKMax / kNormBlock];
+    if constexpr (!SPLIT) {
+#pragma unroll
+        for (int i = 0; i < NSPT; ++i) {
+            const int sl = threadIdx.x + i * NTH;
+            load_row_ss(p, min(sl, p.T - 1), p.nss != nullptr && sl < NSL, ssv[i]);
+        }
+    }
 #pragma unroll
     for (int u = 0; u < PD; ++u) {
         load_x(xr[u], min(c_begin + u, c_last));
         load_w(wr[u], min(c_begin + u, c_last));
+    }
+    if constexpr (!SPLIT) {
+#pragma unroll
+        for (int i = 0; i < NSPT; ++i) {
+            const int sl = threadIdx.x + i * NTH;
+            if (sl < NSL) rsl[sl] = p.nss != nullptr ? rstd_of(p, ssv[i]) : 1.0f;
+        }
     }
     store_x(xr[0], 0);
     __syncthreads();
@@ -232,6 +285,7 @@ void k_gemm16(GemmP p) {
     for (int m = 0; m < MT; ++m) {
         const int t = m * 16 + lr;
         if (!(m < mt_act && t < p.T)) continue;
+        const float sc = SPLIT ? 1.0f : rsl[t];
         if (SPLIT) {
 #pragma unroll
             for (int s = 0; s < NSUB; ++s) {
@@ -243,11 +297,11 @@ void k_gemm16(GemmP p) {
 #pragma unroll
             for (int s = 0; s < NSUB; s += 2)
                 swiglu_store4(p, t, ((tile * NW + wave) * NSUB + s) / 2 * 16 + 4 * lg, acc[s][m],
-                              acc[s + 1][m]);
+                              acc[s + 1][m], sc);
         } else {
 #pragma unroll
             for (int s = 0; s < NSUB; ++s)
-                epi_store4<EPI>(p, t, tile * NT + (wave * NSUB + s) * 16 + 4 * lg, acc[s][m]);
+                epi_store4<EPI>(p, t, tile * NT + (wave * NSUB + s) * 16 + 4 * lg, acc[s][m], sc);
         }
     }
 }
@@ -262,6 +316,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, 2)))
 void k_gemm32(GemmP p) {
     constexpr int NTH = 64 * NW;         // threads per workgroup
     constexpr int NT = NW * NS * 32;     // virtual columns per tile
+    constexpr int ROWS_PER_TILE = 32;
     constexpr int KS = KC / 16;          // MFMA k-steps per chunk
     constexpr int LDX = KC + 8;          // padded LDS row (bf16 elements)
     constexpr int PPR = KC / 8;          // 16-byte pieces per staged row
@@ -272,6 +327,7 @@ void k_gemm32(GemmP p) {
     constexpr int PLANE = MT * 32 * LDX;  // LDS elements per plane
     static_assert(2 * PL * PLANE * 2 <= 160 * 1024, "X staging exceeds LDS");
     __shared__ __attribute__((aligned(16))) bf16_t xs[2][PL * PLANE];
+    __shared__ float rsl[SPLIT ? 1 : MT * ROWS_PER_TILE];  // per-slot RMSNorm factor
 
     const int tile = SPLIT ? blockIdx.x / p.S : blockIdx.x;
     const int split = SPLIT ? blockIdx.x % p.S : 0;
@@ -384,10 +440,30 @@ void k_gemm32(GemmP p) {
     };
 
     const int c_last = c_end - 1;
+    // RMSNorm row factors of the tile's slots (epilogues that scale by
+    // them): loads issued ahead of the pipeline prologue, the factors go to
+    // LDS before the first barrier
+    constexpr int NSL = MT * ROWS_PER_TILE;
+    constexpr int NSPT = SPLIT ? 1 : (NSL + NTH - 1) / NTH;  // slots per thread
+    float ssv[NSPT][kNormKMax / kNormBlock];
+    if constexpr (!SPLIT) {
+#pragma unroll
+        for (int i = 0; i < NSPT; ++i) {
+            const int sl = threadIdx.x + i * NTH;
+            load_row_ss(p, min(sl, p.T - 1), p.nss != nullptr && sl < NSL, ssv[i]);
+        }
+    }
 #pragma unroll
     for (int u = 0; u < PD; ++u) {
         load_x(xr[u], min(c_begin + u, c_last));
         load_w(wr[u], min(c_begin + u, c_last));
+    }
+    if constexpr (!SPLIT) {
+#pragma unroll
+        for (int i = 0; i < NSPT; ++i) {
+            const int sl = threadIdx.x + i * NTH;
+            if (sl < NSL) rsl[sl] = p.nss != nullptr ? rstd_of(p, ssv[i]) : 1.0f;
+        }
     }
     store_x(xr[0], 0);
     __syncthreads();
@@ -412,6 +488,7 @@ void k_gemm32(GemmP p) {
     for (int m = 0; m < MT; ++m) {
         const int t = m * 32 + lc;
         if (t >= p.T) continue;
+        const float sc = SPLIT ? 1.0f : rsl[t];
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
             const int grp = (tile * NW + wave) * NS + s;
@@ -429,12 +506,14 @@ void k_gemm32(GemmP p) {
                 for (int q = 0; q < 2; ++q)
                     swiglu_store4(p, t, grp * 16 + 8 * q + 4 * lh,
                                   f32x4{acc[s][m][4 * q], acc[s][m][4 * q + 1], acc[s][m][4 * q + 2], acc[s][m][4 * q + 3]},
-                                  f32x4{acc[s][m][4 * q + 8], acc[s][m][4 * q + 9], acc[s][m][4 * q + 10], acc[s][m][4 * q + 11]});
+                                  f32x4{acc[s][m][4 * q + 8], acc[s][m][4 * q + 9], acc[s][m][4 * q + 10], acc[s][m][4 * q + 11]},
+                                  sc);
             } else {
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
                     epi_store4<EPI>(p, t, grp * 32 + 8 * q + 4 * lh,
-                                    f32x4{acc[s][m][4 * q], acc[s][m][4 * q + 1], acc[s][m][4 * q + 2], acc[s][m][4 * q + 3]});
+                                    f32x4{acc[s][m][4 * q], acc[s][m][4 * q + 1], acc[s][m][4 * q + 2], acc[s][m][4 * q + 3]},
+                                    sc);
             }
         }
     }
@@ -458,11 +537,11 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(GemmP p) {
             g += *(const f32x4*)(base + s * stride + vg);
             u += *(const f32x4*)(base + s * stride + vg + 16);
         }
-        swiglu_store4(p, t, c, g, u);
+        swiglu_store4(p, t, c, g, u, row_rstd(p, t));
     } else {
         f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
         for (int s = 0; s < p.S; ++s) v += *(const f32x4*)(base + s * stride + c);
-        epi_store4<EPI>(p, t, c, v);
+        epi_store4<EPI>(p, t, c, v, row_rstd(p, t));
     }
 }
 
@@ -737,6 +816,9 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
     p.out = g.out;
     p.ldo = g.ldo;
     p.oplane = (size_t)g.T * g.ldo;  // SwiGLU output planes are [2][T][ldo]
+    p.nss = g.norm_ss;
+    p.nnb = g.norm_nb;
+    p.eps = D.eps;
     if (g.raw) {
         // S partial planes [S][T][N] for a fused consumer to reduce
         hipLaunchKernelGGL(pick<true>(sh, EPI_STORE), dim3(p.tiles * S), dim3(64 * sh.NW), 0, s, p);

@@ -132,6 +132,98 @@ void launch_resid_norm(const Dims& D, int T, const float* part, int S, float* x,
         resid_norm_dispatch<float>(T, part, S, x, (const float*)gamma, (float*)h, D.d, D.eps, s);
 }
 
+// ---------------------------------------------------------------------------
+// bf16 configuration: split-K reduction fused with the residual add and the
+// elementwise half of the next RMSNorm.  x[t] += sum_s part[s][t] (split
+// order, fixed); h[t] = x[t] * gamma as activation planes; and the sum of
+// squares of each 1024-column block of the new x.  The row factor rstd(t)
+// is applied by the consumers of h after their products (it commutes with
+// them), so no workgroup needs a whole row: one workgroup per (slot row,
+// column block), five per row of the 32B model, where one workgroup per row
+// (the fused norm) is bound by what a single CU can pull.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_resid_reduce(const float* part, int S, int T, float* x,
+                                                      const bf16_t* gamma, bf16_t* h, float* ssq,
+                                                      int d, int nsq) {
+    __shared__ float red[4];
+    const int t = blockIdx.x, blk = blockIdx.y;
+    const int k = blk * 256 + threadIdx.x;  // float4 column index
+    const bool act = k < (d >> 2);
+    float4* xr = (float4*)(x + (size_t)t * d);
+    const size_t plane4 = (size_t)T * d / 4;
+    const float4* pr = (const float4*)(part + (size_t)t * d);
+    const float4 xv = act ? xr[k] : float4{0.f, 0.f, 0.f, 0.f};
+    const uint2 gq = act ? *(const uint2*)(gamma + 4 * k) : uint2{0u, 0u};
+    float4 v = float4{0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < S; sp += 8) {
+        float4 b[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+            b[q] = act && sp + q < S ? pr[(sp + q) * plane4 + k] : float4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            v.x += b[q].x; v.y += b[q].y; v.z += b[q].z; v.w += b[q].w;
+        }
+    }
+    float4 r = xv;
+    r.x += v.x; r.y += v.y; r.z += v.z; r.w += v.w;
+    if (act) {
+        xr[k] = r;
+        const size_t o = (size_t)t * d + 4 * k, pl = (size_t)T * d;
+        st_act(h, pl, o + 0, r.x * bf16_to_f32((bf16_t)(gq.x & 0xffffu)));
+        st_act(h, pl, o + 1, r.y * bf16_to_f32((bf16_t)(gq.x >> 16)));
+        st_act(h, pl, o + 2, r.z * bf16_to_f32((bf16_t)(gq.y & 0xffffu)));
+        st_act(h, pl, o + 3, r.w * bf16_to_f32((bf16_t)(gq.y >> 16)));
+    }
+    float ss = act ? r.x * r.x + r.y * r.y + r.z * r.z + r.w * r.w : 0.f;
+    ss = wave_sum(ss);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+    __syncthreads();
+    if (threadIdx.x == 0) ssq[(size_t)t * nsq + blk] = red[0] + red[1] + red[2] + red[3];
+}
+
+void launch_resid_reduce(const Dims& D, int T, const float* part, int S, float* x,
+                         const void* gamma, void* h, float* ssq, int nsq, hipStream_t s) {
+    hipLaunchKernelGGL(k_resid_reduce, dim3(T, nsq), dim3(256), 0, s, part, S, T, x,
+                       (const bf16_t*)gamma, (bf16_t*)h, ssq, D.d, nsq);
+}
+
+// bf16 configuration: embedding gather into x, h = x * gamma (activation
+// planes) and the block sums of squares (the first QKV GEMM's consumer
+// applies rstd); iteration i of a thread covers column block i
+template <int PER>
+__global__ __launch_bounds__(256) void k_embed_ss(const int32_t* tok, const bf16_t* E,
+                                                  const bf16_t* gamma, float* x, bf16_t* h,
+                                                  float* ssq, int d, int nsq, int T) {
+    __shared__ float red[PER][4];
+    const int t = blockIdx.x;
+    const size_t row = (size_t)tok[t] * d;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+        const int k = threadIdx.x + i * 256;
+        float v[4];
+        float ss = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            v[e] = 4 * k < d ? ld(E, row + 4 * k + e) : 0.f;
+            ss += v[e] * v[e];
+        }
+        if (4 * k < d) {
+            *(float4*)(x + (size_t)t * d + 4 * k) = float4{v[0], v[1], v[2], v[3]};
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                st_act(h, (size_t)T * d, (size_t)t * d + 4 * k + e, v[e] * ld(gamma, 4 * k + e));
+        }
+        ss = wave_sum(ss);
+        if ((threadIdx.x & 63) == 0) red[i][threadIdx.x >> 6] = ss;
+    }
+    __syncthreads();
+    if ((int)threadIdx.x < nsq) ssq[(size_t)t * nsq + threadIdx.x] = red[threadIdx.x][0] +
+                                                                  red[threadIdx.x][1] +
+                                                                  red[threadIdx.x][2] +
+                                                                  red[threadIdx.x][3];
+}
+
 // embedding gather fused with the first RMSNorm
 template <typename TA, int PER>
 __global__ __launch_bounds__(256) void k_embed_norm(const int32_t* tok, const TA* E,
@@ -171,7 +263,13 @@ void launch_embed_norm(const Dims& D, const BatchView& bv, const void* embed, co
 #define EN(TA, P) hipLaunchKernelGGL((k_embed_norm<TA, P>), dim3(bv.T), dim3(256), 0, s, sb.tok, \
                                      (const TA*)embed, (const TA*)gamma, sb.x, (TA*)sb.h, D.d, D.eps, bv.T)
     if (D.bf16) {
-        if (per <= 1) EN(bf16_t, 1); else if (per <= 2) EN(bf16_t, 2); else if (per <= 5) EN(bf16_t, 5); else EN(bf16_t, 8);
+        // x, h = x * gamma and the block sums of squares
+        const int nsq = sb.nsq;
+#define ES(P) hipLaunchKernelGGL((k_embed_ss<P>), dim3(bv.T), dim3(256), 0, s, sb.tok, \
+                                 (const bf16_t*)embed, (const bf16_t*)gamma, sb.x, (bf16_t*)sb.h, \
+                                 sb.ssq, D.d, nsq, bv.T)
+        if (nsq <= 1) ES(1); else if (nsq <= 2) ES(2); else if (nsq <= 4) ES(4); else ES(8);
+#undef ES
     } else {
         if (per <= 1) EN(float, 1); else if (per <= 2) EN(float, 2); else if (per <= 5) EN(float, 5); else EN(float, 8);
     }
@@ -189,7 +287,8 @@ template <typename TA>
 __global__ __launch_bounds__(256) void k_qkrope(BatchView bv, const float* qkv, int S,
                                                 const float* cs, TA* qbuf, KVPool kv, int layer,
                                                 const TA* qn, const TA* kn, int hq, int hkv, int hd,
-                                                int qk_norm, float eps) {
+                                                int qk_norm, float eps, const float* nss, int nnb,
+                                                int d) {
     const int wave = (blockIdx.x * 4) + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     const int nh = hq + hkv;
@@ -203,12 +302,27 @@ __global__ __launch_bounds__(256) void k_qkrope(BatchView bv, const float* qkv, 
     // qkv holds S split-K partial planes [S][T][nqkv]; add them in order
     const size_t plane = (size_t)bv.T * nqkv;
     const float* src = qkv + (size_t)t * nqkv + col;
+    // the input's RMSNorm row factor (bf16: the GEMM multiplied x * gamma);
+    // its block sums are requested first
+    float ssb[kNormKMax / kNormBlock];
+#pragma unroll
+    for (int b = 0; b < kNormKMax / kNormBlock; ++b)
+        ssb[b] = nss != nullptr && b < nnb ? nss[(size_t)t * nnb + b] : 0.f;
     float x0 = 0.f, x1 = 0.f;
     if (act)
         for (int sp = 0; sp < S; ++sp) {
             x0 += src[sp * plane + lane];
             x1 += src[sp * plane + lane + half];
         }
+    float rt = 1.0f;
+    if (nss != nullptr) {
+        float ssx = 0.f;
+#pragma unroll
+        for (int b = 0; b < kNormKMax / kNormBlock; ++b) ssx += ssb[b];
+        rt = 1.0f / sqrtf(ssx / (float)d + eps);
+        x0 *= rt;
+        x1 *= rt;
+    }
     if (qk_norm) {
         const float ss = wave_sum(x0 * x0 + x1 * x1);
         const float r = 1.0f / sqrtf(ss / (float)hd + eps);
@@ -244,6 +358,8 @@ __global__ __launch_bounds__(256) void k_qkrope(BatchView bv, const float* qkv, 
         v0 += vs[sp * plane + lane];
         v1 += vs[sp * plane + lane + half];
     }
+    v0 *= rt;
+    v1 *= rt;
     TA* vd = base + kv.v_off(layer, page, g);
     st(vd, (size_t)lane * kPageTokens + off, v0);
     st(vd, (size_t)(lane + half) * kPageTokens + off, v1);
@@ -257,11 +373,11 @@ void launch_qkv_finish(const Dims& D, const BatchView& bv, const SlotBufs& sb, c
     if (D.bf16)
         hipLaunchKernelGGL(k_qkrope<bf16_t>, dim3(blocks), dim3(256), 0, s, bv, part, S, sb.cs,
                            (bf16_t*)sb.qbuf, kv, layer, (const bf16_t*)qn, (const bf16_t*)kn, D.hq,
-                           D.hkv, D.hd, D.qk_norm, D.eps);
+                           D.hkv, D.hd, D.qk_norm, D.eps, sb.ssq, sb.nsq, D.d);
     else
         hipLaunchKernelGGL(k_qkrope<float>, dim3(blocks), dim3(256), 0, s, bv, part, S, sb.cs,
                            (float*)sb.qbuf, kv, layer, (const float*)qn, (const float*)kn, D.hq,
-                           D.hkv, D.hd, D.qk_norm, D.eps);
+                           D.hkv, D.hd, D.qk_norm, D.eps, (const float*)nullptr, 0, D.d);
 }
 
 // ---------------------------------------------------------------------------

@@ -38,10 +38,10 @@ struct Layout {
     size_t st_user, st_prefix, st_L, st_root, st_soff, st_doff, st_sb, st_sj, st_pt, st_items,
         st_ioff, st_flags, st_bytes;
     // slot buffers (byte offsets within the slot)
-    size_t stage, tok, cs, x, h, ffn, qbuf, attn, apart, aml, gpart, gcount, logits, sstat, spart,
+    size_t stage, tok, cs, x, ssq, h, ffn, qbuf, attn, apart, aml, gpart, gcount, logits, sstat, spart,
         spartB, scount, scountB, result, slot_bytes;
     size_t gpart_floats;
-    int gcount_n;
+    int gcount_n, nsq;
     // global region after the slots
     size_t kvw_pages, total;
     int max_pages, max_items, rows_max, Tmax, Bmax;
@@ -127,6 +127,8 @@ Layout plan(const sd_config& c) {
     L.tok = take((size_t)L.Tmax * 4);
     L.cs = take((size_t)L.Tmax * (D.hd / 2) * 2 * 4);
     L.x = take((size_t)L.Tmax * D.d * 4);
+    L.nsq = (D.d + kNormBlock - 1) / kNormBlock;
+    L.ssq = take((size_t)L.Tmax * L.nsq * 4);
     // activations that feed matrix products: two bf16 planes (hi, lo) each
     // in the bf16 configuration, one fp32 plane otherwise
     const size_t ap = D.bf16 ? 2 : 1;
@@ -402,9 +404,28 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
     {
         ProfScope ps(c, SD_K_SMALL, st);
         launch_prepare(D, bv, sb, st);
-        // x = E[tok]; h = RMSNorm(x) with the first layer's pre-attention gain
+        // x = E[tok]; h = RMSNorm(x) with the first layer's pre-attention
+        // gain (bf16: h = x * gain and the block sums of squares)
         launch_embed_norm(D, bv, c->w.embed, c->layers[0].norm1, sb, st);
     }
+    // GEMM input RMSNorm(x) * gamma: h = RMSNorm(x) * gamma (fp32), or
+    // h = x * gamma with the rstd factor applied to the GEMM's outputs (bf16:
+    // the norm's row reduction then needs no single-workgroup pass)
+    auto normed_input = [&](GemmCall& g) {
+        g.X = sb.h;
+        if (D.bf16) {
+            g.norm_ss = sb.ssq;
+            g.norm_nb = sb.nsq;
+        }
+    };
+    // x += partial sums; then h = x * gamma plus the block sums of squares
+    // (bf16) or h = RMSNorm(x) * gamma (fp32)
+    auto residual = [&](int S, const void* gamma) {
+        if (D.bf16)
+            launch_resid_reduce(D, T, sb.gpart, S, sb.x, gamma, sb.h, sb.ssq, sb.nsq, st);
+        else
+            launch_resid_norm(D, T, sb.gpart, S, sb.x, gamma, sb.h, st);
+    };
     for (int l = 0; l < D.L; ++l) {
         const sd_layer_weights& w = c->layers[l];
         const size_t lbase = (size_t)l * c->pl.layer * 2;
@@ -413,7 +434,7 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
             // with QK-norm, RoPE, the query store and the KV append
             ProfScope ps(c, SD_K_QKV, st);
             GemmCall g{};
-            g.X = sb.h;
+            normed_input(g);
             g.Wp = c->wpack + lbase + c->pl.qkv * 2;
             g.W[0] = w.wq; g.W[1] = w.wk; g.W[2] = w.wv;
             g.seg[0] = 0; g.seg[1] = D.nq(); g.seg[2] = D.nq() + D.nkv();
@@ -444,12 +465,12 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
             o.epi = EPI_STORE;
             o.raw = 1;
             const int S = launch_gemm(D, o, sb, st);
-            launch_resid_norm(D, T, sb.gpart, S, sb.x, w.norm2, sb.h, st);
+            residual(S, w.norm2);
         }
         {
             ProfScope ps(c, SD_K_GATEUP, st);
             GemmCall gu{};
-            gu.X = sb.h;
+            normed_input(gu);
             gu.Wp = c->wpack + lbase + c->pl.gu * 2;
             gu.W[0] = w.wg; gu.W[1] = w.wu;
             gu.nseg = 2;
@@ -478,12 +499,12 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
             dn.raw = 1;
             const int S = launch_gemm(D, dn, sb, st);
             const void* gnext = l + 1 < D.L ? c->layers[l + 1].norm1 : c->w.norm_f;
-            launch_resid_norm(D, T, sb.gpart, S, sb.x, gnext, sb.h, st);
+            residual(S, gnext);
         }
     }
     ProfScope ps_lm(c, SD_K_LMHEAD, st);
     GemmCall lm{};
-    lm.X = sb.h;
+    normed_input(lm);
     lm.Wp = c->wpack + c->pl.lm * 2;
     lm.W[0] = c->w.lm_head;
     lm.nseg = 1;
@@ -586,6 +607,8 @@ sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_poo
         b.tok = (int32_t*)(s.base + L.tok);
         b.cs = (float*)(s.base + L.cs);
         b.x = (float*)(s.base + L.x);
+        b.ssq = (float*)(s.base + L.ssq);
+        b.nsq = L.nsq;
         b.h = s.base + L.h;
         b.ffn = s.base + L.ffn;
         b.qbuf = s.base + L.qbuf;

@@ -11,6 +11,8 @@ constexpr int kAttnItemsMax = 1024;  // attention work items per batch (beyond o
 constexpr int kAttnWGsPerCU = 2;     // co-resident attention workgroups per CU (register bound)
 constexpr int kAttnBuffers = 3;      // LDS ring of the attention kernel (buffers - 1 blocks in flight)
 constexpr int kVocabChunks = 16;  // vocab split of the sampler kernels
+constexpr int kNormBlock = 1024;   // columns per sum-of-squares block of x
+constexpr int kNormKMax = 8192;    // widest model dimension the GEMM can normalise on load
 constexpr int kMaxPending = 8;
 
 // Model dimensions as the kernels see them.
@@ -69,9 +71,13 @@ struct SlotBufs {
     int32_t* tok;     // [Tmax]
     float* cs;        // [Tmax][hd/2][2]
     float* x;         // [Tmax][d]
+    float* ssq;       // [Tmax][nsq] sums of squares of x per 1024-column block
+                      // (bf16 configuration: h holds x * gamma and the
+                      // consumers of RMSNorm(x) scale their outputs by rstd)
+    int nsq;
     // activations feeding matrix products; bf16 configuration: [2][T][...]
     // hi and lo planes of the batch's T slots (plane stride T * width)
-    void* h;          // [T][d] normed GEMM input
+    void* h;          // [T][d] GEMM input: RMSNorm(x) * gamma (fp32), x * gamma (bf16)
     void* ffn;        // [T][F] SwiGLU output
     void* qbuf;       // [T][nq] rotated queries
     void* attn;       // [T][nq] attention output
@@ -110,16 +116,28 @@ struct GemmCall {
     int ldo;
     int raw;          // 1: write split-K partial planes [S][T][N] to the slot's
                       //    partial buffer and leave the reduction to the consumer
+    // bf16 configuration, RMSNorm after the product: when norm_ss is set, X
+    // holds x * gamma and each output of slot t is scaled by
+    // rstd(t) = 1 / sqrt(sum_b norm_ss[t][b] / K + eps)
+    const float* norm_ss;
+    int norm_nb;
 };
 // Returns the number of partial planes S (raw mode), else the splits used.
 int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_t s);
+// bf16 configuration: x[t] += sum_s part[s][t] (split order), h = x * gamma
+// (activation planes) and the block sums of squares of the new x; the
+// consumers of h scale by rstd
+void launch_resid_reduce(const Dims& D, int T, const float* part, int S, float* x,
+                         const void* gamma, void* h, float* ssq, int nsq, hipStream_t s);
 // x[t] += sum_s part[s][t] (split order); h[t] = RMSNorm(x[t]) * gamma
 void launch_resid_norm(const Dims& D, int T, const float* part, int S, float* x,
                        const void* gamma, void* h, hipStream_t s);
-// embedding gather into x and h = RMSNorm(x) * gamma
+// embedding gather into x and h = RMSNorm(x) * gamma (fp32 configuration),
+// or into x, h = x * gamma and the block sums of squares (bf16)
 void launch_embed_norm(const Dims& D, const BatchView& bv, const void* embed, const void* gamma,
                        const SlotBufs& sb, hipStream_t s);
 // QKV partial reduction fused with QK-norm, RoPE, query store and KV append
+// (bf16: the summed partials are first scaled by the slot's rstd)
 void launch_qkv_finish(const Dims& D, const BatchView& bv, const SlotBufs& sb, const KVPool& kv,
                        int layer, const float* part, int S, const void* qn, const void* kn,
                        hipStream_t s);
