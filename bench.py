@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--cpu-layers", type=int, default=16,
                     help="decoder layers the CPU-baseline sample runs (extrapolated to all)")
     ap.add_argument("--breakdown", action="store_true", help="time every kernel class")
+    ap.add_argument("--no-greedy", action="store_true",
+                    help="skip the greedy-mode measurement that follows a stochastic run")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 1 GiB device copy (scale reference for HBM byte counters)")
     return ap.parse_args()
@@ -53,7 +55,7 @@ def log(msg):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+        print(json.dumps({"error": "this benchmark measures one GPU; --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     import torch
@@ -176,6 +178,31 @@ def main():
                 "mfma_tflops": round(2.0 * T * 2 * m.d_ffn * m.d_model / gu_avg_s / 1e12, 1),
                 "mfma_frac_bf16": round(2.0 * T * 2 * m.d_ffn * m.d_model / gu_avg_s / 1e12 / BF16_PEAK_TFLOPS, 4)}
 
+    def class_ms(k, steps=3):
+        """Per-step device time of one kernel class (event pair per scope,
+        the empty pair's cost subtracted)."""
+        sv.sd_profile_begin(v.ctx, k, steps * nb * (4 * m.n_layers + 8))
+        for _ in range(steps):
+            step()
+        ms, n = sv.sd_profile_end(v.ctx)
+        return max(ms - n * pair_ms, 1e-6) / steps
+
+    # attention (all layers, KV streamed once per user) and sampler rates
+    kv_read_step = sum(int(p + l + 1) for p, l in zip(w.prefix_len, w.draft_len)) * m.kv_bytes_per_token()
+    attn_ms = class_ms(sv.SD_K_ATTN)
+    samp_bytes = sum(b.T for b in batches) * m.vocab * 4 + int(w.n_users) * m.vocab * 4
+    samp_ms = class_ms(sv.SD_K_SAMPLER)
+    kernels = {
+        "attention": {"achieved": round(kv_read_step / (attn_ms / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                      "unit": "GB/s", "frac": round(kv_read_step / (attn_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                      "bytes_per_step": kv_read_step, "ms_per_step": round(attn_ms, 4),
+                      "note": "paged attention + chunk combine, all layers; bytes = cached and new K/V read once"},
+        "sampler": {"achieved": round(samp_bytes / (samp_ms / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": round(samp_bytes / (samp_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                    "bytes_per_step": samp_bytes, "ms_per_step": round(samp_ms, 4),
+                    "note": "accept/reject + resample kernels; bytes = T x V fp32 logits + one q row per user"},
+    }
+
     breakdown = None
     if args.breakdown:
         breakdown = {}
@@ -212,9 +239,13 @@ def main():
         "step_algorithmic_gb": round(step_bytes / 1e9, 2),
         "step_effective_gbs": round(step_bytes / (ms_step / 1e3) / 1e9, 1),
         "roofline": roofline,
+        "kernels": kernels,
     }
     if breakdown is not None:
         result["breakdown_ms"] = breakdown
+    if args.mode == "stochastic" and not args.no_greedy:
+        result["greedy"] = greedy_run(v, w, batches, dev_in, step_args=(streams, nb), steps=args.steps,
+                                      warmup=args.warmup, torch=torch)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, batches[0], args.cpu_layers, acc_step / verified_step)
     v.close()
@@ -239,6 +270,38 @@ def measured_traffic(workload):
     if hashlib.sha256(open(src, "rb").read()).hexdigest() != h.group(1):
         return None
     return int(m.group(1))
+
+
+def greedy_run(v, w, batches, dev_in, step_args, steps, warmup, torch):
+    """The same workload in greedy mode (accept iff the draft is the
+    target's argmax), with drafts planted to follow the target's own argmax
+    for k_m ~ U{0..l_m} steps; timed like the stochastic run."""
+    streams, nb = step_args
+    plant_greedy_drafts(v, w, batches, dev_in, torch)
+
+    def step():
+        for n in range(nb):
+            d, q, au = dev_in[n]
+            v.verify(n, w.assign, w.draft_len, d, q, "greedy", seed=w.seed, round_=0,
+                     stream=streams[n % len(streams)])
+        acc = 0
+        for n in range(nb):
+            n_acc, _ = v.accept(n, w.n_users)
+            acc += int((n_acc[batches[n].users] + 1).sum())
+        return acc
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    accepted = 0
+    for _ in range(steps):
+        accepted += step()
+    torch.cuda.synchronize()
+    ms_step = 1e3 * (time.perf_counter() - t0) / steps
+    return {"value": round(accepted / steps / (ms_step / 1e3), 2), "unit": "tokens/s",
+            "ms_per_step": round(ms_step, 4), "accepted_per_step": accepted / steps,
+            "drafts": "first k_m drafts follow the target's argmax, k_m ~ U{0..l_m}"}
 
 
 def plant_greedy_drafts(v, w, batches, dev_in, torch):
