@@ -311,9 +311,19 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 // 32x32x16 form.  MT: 32-slot tiles; NS: 32-row weight groups (pairs of
 // 16-row groups) per wave; KC: k per chunk (a multiple of 16); NW: waves per
 // workgroup; PL: activation planes; PD: chunks of prefetch.
-template <int MT, int NS, int KC, int EPI, bool SPLIT, int NW, int PL, int PD>
+// PK (two planes packed, for 32a < T <= 32a + 16): the B operand's columns
+// are (slot, plane) pairs instead of slots, MT = 2a + 1 tiles in one staged
+// plane: tiles 0..a-1 the hi plane of slots 0..32a-1, tile a the hi plane of
+// slots 32a.. in columns 0-15 and their lo plane in columns 16-31, tiles
+// a+1..2a the lo plane of slots 0..32a-1.  That is one tile fewer than two
+// planes of a + 1 tiles each; the epilogue adds each slot's hi and lo sums
+// (same lane of tiles m and m + a + 1, or lanes l and l ^ 16 of tile a).
+template <int MT, int NS, int KC, int EPI, bool SPLIT, int NW, int PL, int PD, bool PK = false>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, 2)))
 void k_gemm32(GemmP p) {
+    static_assert(!PK || (PL == 2 && MT % 2 == 1), "packed planes: two planes, 2a + 1 tiles");
+    constexpr int PLS = PK ? 1 : PL;     // staged (and multiplied) planes
+    constexpr int PA = MT / 2;           // packed: full tiles per plane
     constexpr int NTH = 64 * NW;         // threads per workgroup
     constexpr int NT = NW * NS * 32;     // virtual columns per tile
     constexpr int ROWS_PER_TILE = 32;
@@ -321,12 +331,12 @@ void k_gemm32(GemmP p) {
     constexpr int LDX = KC + 8;          // padded LDS row (bf16 elements)
     constexpr int PPR = KC / 8;          // 16-byte pieces per staged row
     constexpr int NPP = MT * 32 * PPR;   // pieces per staged plane
-    constexpr int NPC = PL * NPP;        // pieces per staged chunk (all planes)
+    constexpr int NPC = PLS * NPP;       // pieces per staged chunk (all planes)
     constexpr int XPT = (NPC + NTH - 1) / NTH;  // X pieces per thread
     constexpr bool XEVEN = NPC % NTH == 0;
     constexpr int PLANE = MT * 32 * LDX;  // LDS elements per plane
-    static_assert(2 * PL * PLANE * 2 <= 160 * 1024, "X staging exceeds LDS");
-    __shared__ __attribute__((aligned(16))) bf16_t xs[2][PL * PLANE];
+    static_assert(2 * PLS * PLANE * 2 <= 160 * 1024, "X staging exceeds LDS");
+    __shared__ __attribute__((aligned(16))) bf16_t xs[2][PLS * PLANE];
     __shared__ float rsl[SPLIT ? 1 : MT * ROWS_PER_TILE];  // per-slot RMSNorm factor
 
     const int tile = SPLIT ? blockIdx.x / p.S : blockIdx.x;
@@ -382,8 +392,15 @@ void k_gemm32(GemmP p) {
 #pragma unroll
     for (int i = 0; i < XPT; ++i) {
         const int idx = min((int)threadIdx.x + i * NTH, NPC - 1);
-        const int pl = idx / NPP, pi = idx % NPP;
-        const int r = min(pi / PPR, p.T - 1), cc = pi % PPR;
+        int pl = idx / NPP, row = (idx % NPP) / PPR;
+        const int cc = idx % PPR;
+        if (PK) {
+            // staged row -> (plane, slot) of the packed layout
+            const int v = row;
+            pl = v < 32 * PA + 16 ? 0 : 1;
+            row = v < 32 * PA + 16 ? v : v < 32 * PA + 32 ? v - 16 : v - 32 * (PA + 1);
+        }
+        const int r = min(row, p.T - 1);
         xoff[i] = (((uint32_t)pl * (uint32_t)p.T + (uint32_t)r) * (uint32_t)p.K + (uint32_t)cc * 8u) * 2u;
     }
     auto load_x = [&](uint4 (&x)[XPT], int c) {
@@ -414,22 +431,22 @@ void k_gemm32(GemmP p) {
     // ahead, and every slot tile of the class is computed (tiles past T
     // multiply clamped copies of row T-1 and are never stored).  MFMAs on one
     // accumulator are MT*NS instructions apart (planes outermost).
-    auto read_x = [&](bf16x8 (&xf)[PL][MT], const bf16_t* xb, int ks) {
+    auto read_x = [&](bf16x8 (&xf)[PLS][MT], const bf16_t* xb, int ks) {
 #pragma unroll
-        for (int pl = 0; pl < PL; ++pl)
+        for (int pl = 0; pl < PLS; ++pl)
 #pragma unroll
             for (int m = 0; m < MT; ++m)
                 xf[pl][m] = *(const bf16x8*)(xb + pl * PLANE + (m * 32 + lc) * LDX + ks * 16 + 8 * lh);
     };
     auto compute = [&](int buf, const bf16x8 (&w)[KS][NS]) {
         const bf16_t* xb = xs[buf];
-        bf16x8 xf[2][PL][MT];
+        bf16x8 xf[2][PLS][MT];
         read_x(xf[0], xb, 0);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             if (ks + 1 < KS) read_x(xf[(ks + 1) & 1], xb, ks + 1);
 #pragma unroll
-            for (int pl = 0; pl < PL; ++pl)
+            for (int pl = 0; pl < PLS; ++pl)
 #pragma unroll
                 for (int m = 0; m < MT; ++m)
 #pragma unroll
@@ -484,10 +501,25 @@ void k_gemm32(GemmP p) {
 
     // Accumulator layout: lane l holds slot t = 32*m + l % 32 and, in
     // registers 4q..4q+3, weight rows 8q + 4*(l/32) + 0..3 of its group.
+    // Packed planes: slot t's sums are those of tile m and tile m + a + 1
+    // (t < 32a), or of lanes l and l ^ 16 of tile a, swapped in by
+    // v_permlane16_swap, which hands each lane the pair (own, partner).
+    if constexpr (PK) {
 #pragma unroll
-    for (int m = 0; m < MT; ++m) {
+        for (int s = 0; s < NS; ++s)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const auto pr = __builtin_amdgcn_permlane16_swap(__float_as_uint(acc[s][PA][e]),
+                                                                 __float_as_uint(acc[s][PA][e]), false, false);
+                acc[s][PA][e] = __uint_as_float(pr[0]) + __uint_as_float(pr[1]);
+#pragma unroll
+                for (int m = 0; m < PA; ++m) acc[s][m][e] += acc[s][m + PA + 1][e];
+            }
+    }
+#pragma unroll
+    for (int m = 0; m < (PK ? PA + 1 : MT); ++m) {
         const int t = m * 32 + lc;
-        if (t >= p.T) continue;
+        if (t >= p.T || (PK && m == PA && lc >= 16)) continue;
         const float sc = SPLIT ? 1.0f : rsl[t];
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
@@ -637,23 +669,29 @@ __global__ void k_gemm_f32(GemmF p) {
 //   * above 224 slots tiles need the register budget of one wave per SIMD
 //     (four waves) and shorter chunks so that a double-buffered two-plane
 //     chunk fits in LDS.
-struct GemmShape { int F, MT, NSUB, KC, NW, PD; };
+struct GemmShape { int F, MT, NSUB, KC, NW, PD, PK; };
 
 constexpr int kT32 = 97;  // first slot count served by the 32x32 form
 
-static GemmShape shape_for(int T, int vcols) {
+static GemmShape shape_for(int T, int vcols, bool raw) {
     const bool wide = vcols % 256 == 0;
+    // packed planes (2a + 1 tiles for 32a < T <= 32a + 16): split-K
+    // partial GEMMs at 65..80 slots (QKV / O / down at T = 80: 29.5 / 23.7
+    // / 53 us against 32.4 / 25.3 / 54 us for the 16x16 form), and every
+    // GEMM at 97..112 slots (gate/up at T = 112: 147-175 us against 167-194)
+    if (wide && raw && T > 64 && T <= 80) return {32, 5, 1, 64, 8, 2, 1};
+    if (wide && T > 96 && T <= 112) return {32, 7, 1, 64, 8, 1, 1};
     if (T < kT32) {
         const int mt = std::max(2, (T + 15) / 16);
-        return wide ? GemmShape{16, mt, 2, 128, 8, 1} : GemmShape{16, mt, 2, 64, 4, 2};
+        return wide ? GemmShape{16, mt, 2, 128, 8, 1, 0} : GemmShape{16, mt, 2, 64, 4, 2, 0};
     }
     const int mt = (T + 31) / 32;
-    if (mt <= 4) return wide ? GemmShape{32, mt, 1, 64, 8, 2} : GemmShape{32, mt, 1, 64, 4, 2};
-    if (mt <= 7) return wide ? GemmShape{32, mt, 1, 64, 8, 1} : GemmShape{32, mt, 1, 64, 4, 1};
-    if (mt <= 8) return {32, 8, 1, 64, 4, 1};
-    if (mt <= 10) return {32, 10, 1, 32, 4, 1};
-    if (mt <= 13) return {32, 13, 1, 16, 4, 1};
-    return {0, 0, 0, 0, 0, 0};
+    if (mt <= 4) return wide ? GemmShape{32, mt, 1, 64, 8, 2, 0} : GemmShape{32, mt, 1, 64, 4, 2, 0};
+    if (mt <= 7) return wide ? GemmShape{32, mt, 1, 64, 8, 1, 0} : GemmShape{32, mt, 1, 64, 4, 1, 0};
+    if (mt <= 8) return {32, 8, 1, 64, 4, 1, 0};
+    if (mt <= 10) return {32, 10, 1, 32, 4, 1, 0};
+    if (mt <= 13) return {32, 13, 1, 16, 4, 1, 0};
+    return {0, 0, 0, 0, 0, 0, 0};
 }
 
 typedef void (*GemmFn)(GemmP);
@@ -661,7 +699,7 @@ typedef void (*ReduceFn)(GemmP);
 
 // Activations always come as two planes (hi, lo); split-K kernels write raw
 // partial planes and the epilogue runs in the reducer.
-template <int F, int MT, int NW, int KC, int PD, bool SPLIT>
+template <int F, int MT, int NW, int KC, int PD, bool SPLIT, bool PK = false>
 static GemmFn pick_epi(int epi) {
     if constexpr (F == 16) {
         if (SPLIT) return k_gemm16<MT, 2, KC, EPI_STORE, true, NW, 2, PD>;
@@ -671,11 +709,11 @@ static GemmFn pick_epi(int epi) {
             default: return k_gemm16<MT, 2, KC, EPI_STORE, false, NW, 2, PD>;
         }
     } else {
-            if (SPLIT) return k_gemm32<MT, 1, KC, EPI_STORE, true, NW, 2, PD>;
+        if (SPLIT) return k_gemm32<MT, 1, KC, EPI_STORE, true, NW, 2, PD, PK>;
         switch (epi) {
-            case EPI_RESID: return k_gemm32<MT, 1, KC, EPI_RESID, false, NW, 2, PD>;
-            case EPI_SWIGLU: return k_gemm32<MT, 1, KC, EPI_SWIGLU, false, NW, 2, PD>;
-            default: return k_gemm32<MT, 1, KC, EPI_STORE, false, NW, 2, PD>;
+            case EPI_RESID: return k_gemm32<MT, 1, KC, EPI_RESID, false, NW, 2, PD, PK>;
+            case EPI_SWIGLU: return k_gemm32<MT, 1, KC, EPI_SWIGLU, false, NW, 2, PD, PK>;
+            default: return k_gemm32<MT, 1, KC, EPI_STORE, false, NW, 2, PD, PK>;
         }
     }
 }
@@ -704,6 +742,11 @@ static GemmFn pick_nw(const GemmShape& sh, int epi) {
 
 template <bool SPLIT>
 static GemmFn pick(const GemmShape& sh, int epi) {
+    if (sh.PK) {
+        if (sh.MT == 5) return SPLIT ? pick_epi<32, 5, 8, 64, 2, true, true>(epi) : nullptr;
+        if (sh.MT == 7) return pick_epi<32, 7, 8, 64, 1, SPLIT, true>(epi);
+        return nullptr;
+    }
     if (sh.F == 32 && sh.MT == 8) return pick_epi<32, 8, 4, 64, 1, SPLIT>(epi);
     if (sh.F == 32 && sh.MT == 10) return pick_epi<32, 10, 4, 32, 1, SPLIT>(epi);
     if (sh.F == 32 && sh.MT == 13) return pick_epi<32, 13, 4, 16, 1, SPLIT>(epi);
@@ -768,7 +811,7 @@ int gemm_counter_count(const Dims&) { return 1; }
 bool gemm_shape_ok(const Dims& D, int T, int K, int N, int epi) {
     if (!D.bf16) return true;
     const int vcols = epi == EPI_SWIGLU ? 2 * N : N;
-    const GemmShape sh = shape_for(T, vcols);
+    const GemmShape sh = shape_for(T, vcols, false);
     if (sh.MT == 0) return false;
     return K % sh.KC == 0 && K % 32 == 0 && vcols % (sh.F * sh.NW * sh.NSUB) == 0;
 }
@@ -793,7 +836,7 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
         return 1;
     }
     const int vcols = g.epi == EPI_SWIGLU ? 2 * g.N : g.N;
-    const GemmShape sh = shape_for(g.T, vcols);
+    const GemmShape sh = shape_for(g.T, vcols, g.raw != 0);
     const int nt = sh.F * sh.NW * sh.NSUB;
     GemmP p;
     p.X = (const bf16_t*)g.X;

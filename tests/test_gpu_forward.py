@@ -196,11 +196,13 @@ def test_determinism_two_runs_bit_identical():
     v.close()
 
 
-@pytest.mark.parametrize("T_target", [17, 70, 150, 250, 300, 416])
+@pytest.mark.parametrize("T_target", [17, 70, 75, 80, 105, 112, 150, 250, 300, 416])
 def test_bf16_every_gemm_tile_class(T_target):
-    """Query-slot totals that select each GEMM tile class (2..26 slot tiles;
-    eight-wave tiles up to 16 slot tiles, four-wave tiles above) and the
-    split-K and unsplit paths, up to the 416-slot maximum."""
+    """Query-slot totals that select each GEMM tile class: the 16x16 form up
+    to 96 slots, the 32x32 form above (eight-wave tiles up to 224 slots,
+    four-wave tiles above), the packed-plane 32x32 tiles (split-K partials
+    at 65..80 slots, every GEMM at 97..112, with and without padding in the
+    mixed tile), split-K and unsplit paths, up to the 416-slot maximum."""
     rng = np.random.default_rng(T_target)
     L, T = [], 0
     while T < T_target:
