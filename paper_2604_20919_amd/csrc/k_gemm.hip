@@ -776,15 +776,17 @@ static int cu_count() {
 // giving 1.25 to 1.75 workgroups per CU, else the smallest giving at least
 // 1.25.  Eight-wave tiles (one workgroup per CU fits in LDS): the largest
 // count keeping the grid within one wave of workgroups, splits of unequal
-// chunk counts allowed (measured on the 32B shapes at T = 80: QKV 40 tiles
-// x 6 = 240 workgroups 27.2 us vs x 5 30.7 us, O 20 x 12 23.9 vs x 8 27.4,
-// down 20 x 12 52.6 vs x 10 57.1; the extra partial sums cost the
-// consumers less than the idle CUs cost the GEMM).
+// chunk counts allowed, at least two chunks per split (measured on the 32B
+// shapes at T = 80: QKV 40 tiles x 6 = 240 workgroups 27.2 us vs x 5
+// 30.7 us, O 20 x 12 23.9 vs x 8 27.4, down 20 x 12 52.6 vs x 10 57.1; the
+// extra partial sums cost the consumers less than the idle CUs cost the
+// GEMM.  On the 1.7B shapes one-chunk splits lose to pipeline start-up and
+// partial-sum traffic: the step goes from 2.99 to 2.77 ms with two).
 static int choose_splits(int tiles, int kchunks, int nw) {
     if (nw == 8) {
         const int hi = cu_count();
         if (tiles * 2 > hi) return 1;
-        return std::max(1, std::min(kchunks, hi / tiles));
+        return std::max(1, std::min(std::max(1, kchunks / 2), hi / tiles));
     }
     const int lo = cu_count() * 5 / 4, hi = cu_count() * 7 / 4;
     if (tiles >= lo) return 1;
