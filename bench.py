@@ -43,6 +43,10 @@ def parse():
     ap.add_argument("--breakdown", action="store_true", help="time every kernel class")
     ap.add_argument("--no-greedy", action="store_true",
                     help="skip the greedy-mode measurement that follows a stochastic run")
+    ap.add_argument("--graph", type=int, default=-1, choices=[-1, 0, 1],
+                    help="1: each batch's pass is replayed from a HIP graph (sd_verify_batch_graph); "
+                         "0: eager launches; -1 (default): graphs for the pipelined multi-batch "
+                         "workload, whose definition asks for them, eager otherwise")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 1 GiB device copy (scale reference for HBM byte counters)")
     return ap.parse_args()
@@ -78,6 +82,8 @@ def main():
 
     w = wl.workload(args.workload)
     m = w.model
+    if args.graph < 0:
+        args.graph = 1 if w.n_batches > 1 else 0
     t0 = time.time()
     dw = DeviceWeights(m, w.seed)
     log(f"weights {dw.nbytes() / 1e9:.1f} GB generated on GPU in {time.time() - t0:.1f}s")
@@ -122,7 +128,7 @@ def main():
         for n in range(nb):
             d, q, au = dev_in[n]
             v.verify(n, w.assign, w.draft_len, d, q, args.mode, seed=w.seed, round_=0,
-                     accept_u=au, stream=streams[n % len(streams)])
+                     accept_u=au, stream=streams[n % len(streams)], graph=bool(args.graph))
         acc = 0
         for n in range(nb):
             n_acc, _ = v.accept(n, w.n_users)
@@ -232,7 +238,8 @@ def main():
         "data": "synthetic (random-init weights N(0,0.02), synthetic KV N(0,1), synthetic draft q)",
         "config": {"workload": args.workload, "model": m.name, "mode": args.mode,
                    "users": int(w.n_users), "batches": nb, "verified_tokens_per_step": verified_step,
-                   "prefix_tokens": kv_tokens},
+                   "prefix_tokens": kv_tokens, "hip_graph": bool(args.graph),
+                   "streams": len(streams)},
         "verified_tokens_per_s": round(verified_step / (ms_step / 1e3), 1),
         "accepted_per_step": acc_step,
         "step_hbm_floor_ms": round(step_bytes / (HBM_PEAK_GBS * 1e9) * 1e3, 3),
@@ -245,7 +252,7 @@ def main():
         result["breakdown_ms"] = breakdown
     if args.mode == "stochastic" and not args.no_greedy:
         result["greedy"] = greedy_run(v, w, batches, dev_in, step_args=(streams, nb), steps=args.steps,
-                                      warmup=args.warmup, torch=torch)
+                                      warmup=args.warmup, torch=torch, graph=bool(args.graph))
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, batches[0], args.cpu_layers, acc_step / verified_step)
     v.close()
@@ -272,7 +279,7 @@ def measured_traffic(workload):
     return int(m.group(1))
 
 
-def greedy_run(v, w, batches, dev_in, step_args, steps, warmup, torch):
+def greedy_run(v, w, batches, dev_in, step_args, steps, warmup, torch, graph):
     """The same workload in greedy mode (accept iff the draft is the
     target's argmax), with drafts planted to follow the target's own argmax
     for k_m ~ U{0..l_m} steps; timed like the stochastic run."""
@@ -283,7 +290,7 @@ def greedy_run(v, w, batches, dev_in, step_args, steps, warmup, torch):
         for n in range(nb):
             d, q, au = dev_in[n]
             v.verify(n, w.assign, w.draft_len, d, q, "greedy", seed=w.seed, round_=0,
-                     stream=streams[n % len(streams)])
+                     stream=streams[n % len(streams)], graph=graph)
         acc = 0
         for n in range(nb):
             n_acc, _ = v.accept(n, w.n_users)

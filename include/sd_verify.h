@@ -205,6 +205,31 @@ sd_status sd_verify_batch(sd_ctx* ctx, int32_t batch, int32_t n_users, const int
                           sd_stream stream);
 
 /*
+ * sd_verify_batch with the device work of the pass replayed from a HIP graph.
+ * Same arguments, validation, errors and completion (sd_accept) as
+ * sd_verify_batch; `stream` must not be NULL (the null stream cannot be
+ * captured).  The batch's workspace slot (batch % max_pending) keeps one
+ * graph: the first call captures the pass (staging upload, every kernel,
+ * result download) on `stream`, instantiates it and launches it; a later
+ * call whose launch signature is unchanged -- the same users with the same
+ * l_m and i_m, mode, seed, round, input pointers and stream -- only re-plans
+ * the host side (page reservation, staged tables, which the graph's upload
+ * reads from the slot's pinned staging buffer at launch time) and launches
+ * the graph once.  Any other signature re-captures (so a serving loop whose
+ * i_m advance every round re-captures every round; repeated verification of
+ * an unchanged batch replays).  The graph holds no memset nodes.  If the
+ * caller is itself capturing `stream`, the launches are enqueued into the
+ * caller's capture instead.  While a profiling window (sd_profile_begin) is
+ * open the pass runs eagerly.  Graphs are released by sd_verify_destroy.
+ * Errors as sd_verify_batch, plus SD_EINVAL for a NULL stream and SD_EHIP if
+ * capture or instantiation fails (nothing is left pending then).
+ */
+sd_status sd_verify_batch_graph(sd_ctx* ctx, int32_t batch, int32_t n_users, const int32_t* assign,
+                                const int32_t* draft_len, const int32_t* draft_tokens,
+                                const float* q, int32_t mode, uint64_t seed, uint64_t round,
+                                const float* accept_u, sd_stream stream);
+
+/*
  * Wait for batch `batch` and return its decisions (Sec. II-A steps 2-3):
  *   n_accepted: host [M] (M of the sd_verify_batch call); entry m of every
  *               batch user receives a_m, the number of leading drafts accepted

@@ -41,6 +41,12 @@ struct GemmP {
     const bf16_t* X;
     const bf16_t* Wp;  // packed weights: [vcols/16][K/32][64 lanes][8]
     int K, KT, T, S, kchunks, tiles;  // KT = K / 32 fragments per 16-row group
+    // Work split: a wave unit is the row block one wave multiplies (NSUB
+    // 16-row groups, or NS 32-row groups); G units in total.  Each k split
+    // has WPS workgroups; workgroup w of a split takes units
+    // [w*G/WPS, (w+1)*G/WPS), one per wave, so G need not be a multiple of
+    // the waves per workgroup (waves past the range load nothing).
+    int G, WPS;
     float* part;     // [S][T][vcols] when S > 1
     int vcols;
     void* out;
@@ -111,15 +117,21 @@ __device__ __forceinline__ void swiglu_store4(const GemmP& p, int t, int col, f3
 // 16x16x32 form.  MT: 16-slot tiles; NSUB: 16-row weight groups per wave;
 // KC: k per chunk (a multiple of 32); NW: waves per workgroup; PL:
 // activation planes; PD: chunks of prefetch.
-template <int MT, int NSUB, int KC, int EPI, bool SPLIT, int NW, int PL, int PD>
+// XPAD: bf16 elements of padding per staged row.  With 16 (a row stride of
+// an odd multiple of 32 bytes) the B-fragment reads of 32 lanes (16 rows at
+// two k offsets) hit distinct banks of the 128-bank LDS, and the staging
+// stores are ordered so that the rows written together sit 16/R rows apart
+// (R rows per 32 lanes), which also spreads them over every bank.  With 8
+// (stride 272 or 144 bytes) rows 0 and 15 of a read share banks.
+template <int MT, int NSUB, int KC, int EPI, bool SPLIT, int NW, int PL, int PD, int XPAD = 16>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, 2)))
 void k_gemm16(GemmP p) {
     constexpr int NTH = 64 * NW;         // threads per workgroup
-    constexpr int NT = NW * NSUB * 16;   // virtual columns per tile
     constexpr int ROWS_PER_TILE = 16;
     constexpr int KS = KC / 32;          // MFMA k-steps per chunk
-    constexpr int LDX = KC + 8;          // padded LDS row (bf16 elements)
+    constexpr int LDX = KC + XPAD;       // padded LDS row (bf16 elements)
     constexpr int PPR = KC / 8;          // 16-byte pieces per staged row
+    constexpr int RPP = PPR >= 32 ? 1 : 32 / PPR;  // staged rows per 32 lanes
     constexpr int NPP = MT * 16 * PPR;   // pieces per staged plane
     constexpr int NPC = PL * NPP;        // pieces per staged chunk (all planes)
     constexpr int XPT = (NPC + NTH - 1) / NTH;  // X pieces per thread
@@ -130,23 +142,29 @@ void k_gemm16(GemmP p) {
     __shared__ __attribute__((aligned(16))) bf16_t xs[2][PL * PLANE];
     __shared__ float rsl[SPLIT ? 1 : MT * ROWS_PER_TILE];  // per-slot RMSNorm factor
 
-    const int tile = SPLIT ? blockIdx.x / p.S : blockIdx.x;
+    // k split of this workgroup (consecutive workgroups take consecutive
+    // splits, so with S a divisor of 8 every XCD works on one k range) and
+    // its range of wave units
     const int split = SPLIT ? blockIdx.x % p.S : 0;
+    const int wgi = SPLIT ? blockIdx.x / p.S : blockIdx.x;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int lr = lane & 15, lg = lane >> 4;
     const int mt_act = (p.T + 15) >> 4;
 
     // Buffer resources: one uniform resource per operand, fixed 32-bit
-    // per-lane offsets, uniform chunk offsets.  Out-of-range reads return 0.
+    // per-lane offsets, uniform chunk offsets.  Out-of-range reads return 0
+    // (and fetch nothing: a wave without a unit points past the buffer).
     const int wv = __builtin_amdgcn_readfirstlane(wave);
+    const int unit = wgi * p.G / p.WPS + wv;
+    const bool has_unit = unit < (wgi + 1) * p.G / p.WPS;
     const uint64_t wbytes = (uint64_t)p.vcols * (uint64_t)p.K * 2u;
     const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
         (void*)p.Wp, (short)0, (int)(wbytes > 0x7fffffffu ? 0x7fffffffu : wbytes), 0x00020000);
     uint32_t woff[NSUB];
 #pragma unroll
     for (int s = 0; s < NSUB; ++s) {
-        const uint32_t vs = (uint32_t)((tile * NW + wv) * NSUB + s);  // 16-row group
-        woff[s] = vs * (uint32_t)p.KT * 1024u + (uint32_t)lane * 16u;
+        const uint32_t vs = (uint32_t)(unit * NSUB + s);  // 16-row group
+        woff[s] = has_unit ? vs * (uint32_t)p.KT * 1024u + (uint32_t)lane * 16u : 0x80000000u;
     }
     const __amdgpu_buffer_rsrc_t xres =
         __builtin_amdgcn_make_buffer_rsrc((void*)p.X, (short)0, PL * p.T * p.K * 2, 0x00020000);
@@ -174,11 +192,17 @@ void k_gemm16(GemmP p) {
     uint4 xr[NB][XPT];
     bf16x8 wr[NB][KS][NSUB];
     uint32_t xoff[XPT];
+    // staging order q -> LDS row (a permutation within each block of 16
+    // rows; the identity for XPAD != 16)
+    auto staged_row = [](int q) {
+        if constexpr (XPAD != 16 || RPP == 1) return q;
+        else return (q & ~15) | ((q % RPP) * (16 / RPP)) | ((q / RPP) % (16 / RPP));
+    };
 #pragma unroll
     for (int i = 0; i < XPT; ++i) {
         const int idx = min((int)threadIdx.x + i * NTH, NPC - 1);
         const int pl = idx / NPP, pi = idx % NPP;
-        const int r = min(pi / PPR, p.T - 1), cc = pi % PPR;
+        const int r = min(staged_row(pi / PPR), p.T - 1), cc = pi % PPR;
         xoff[i] = (((uint32_t)pl * (uint32_t)p.T + (uint32_t)r) * (uint32_t)p.K + (uint32_t)cc * 8u) * 2u;
     }
     auto load_x = [&](uint4 (&x)[XPT], int c) {
@@ -193,7 +217,7 @@ void k_gemm16(GemmP p) {
             const int idx = threadIdx.x + i * NTH;
             const int pl = idx / NPP, pi = idx % NPP;
             if (XEVEN || idx < NPC)
-                *(uint4*)(&xs[buf][pl * PLANE + (pi / PPR) * LDX + (pi % PPR) * 8]) = x[i];
+                *(uint4*)(&xs[buf][pl * PLANE + staged_row(pi / PPR) * LDX + (pi % PPR) * 8]) = x[i];
         }
     };
     auto load_w = [&](bf16x8 (&w)[KS][NSUB], int c) {
@@ -284,24 +308,23 @@ void k_gemm16(GemmP p) {
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
         const int t = m * 16 + lr;
-        if (!(m < mt_act && t < p.T)) continue;
+        if (!(has_unit && m < mt_act && t < p.T)) continue;
         const float sc = SPLIT ? 1.0f : rsl[t];
         if (SPLIT) {
 #pragma unroll
             for (int s = 0; s < NSUB; ++s) {
-                const int v = tile * NT + (wave * NSUB + s) * 16 + 4 * lg;
+                const int v = (unit * NSUB + s) * 16 + 4 * lg;
                 *(f32x4*)(p.part + ((size_t)split * p.T + t) * p.vcols + v) = acc[s][m];
             }
         } else if (EPI == EPI_SWIGLU) {
             // groups 2j / 2j+1 hold gate / up rows 16j..16j+15
 #pragma unroll
             for (int s = 0; s < NSUB; s += 2)
-                swiglu_store4(p, t, ((tile * NW + wave) * NSUB + s) / 2 * 16 + 4 * lg, acc[s][m],
-                              acc[s + 1][m], sc);
+                swiglu_store4(p, t, (unit * NSUB + s) / 2 * 16 + 4 * lg, acc[s][m], acc[s + 1][m], sc);
         } else {
 #pragma unroll
             for (int s = 0; s < NSUB; ++s)
-                epi_store4<EPI>(p, t, tile * NT + (wave * NSUB + s) * 16 + 4 * lg, acc[s][m], sc);
+                epi_store4<EPI>(p, t, (unit * NSUB + s) * 16 + 4 * lg, acc[s][m], sc);
         }
     }
 }
@@ -325,7 +348,6 @@ void k_gemm32(GemmP p) {
     constexpr int PLS = PK ? 1 : PL;     // staged (and multiplied) planes
     constexpr int PA = MT / 2;           // packed: full tiles per plane
     constexpr int NTH = 64 * NW;         // threads per workgroup
-    constexpr int NT = NW * NS * 32;     // virtual columns per tile
     constexpr int ROWS_PER_TILE = 32;
     constexpr int KS = KC / 16;          // MFMA k-steps per chunk
     constexpr int LDX = KC + 8;          // padded LDS row (bf16 elements)
@@ -339,14 +361,17 @@ void k_gemm32(GemmP p) {
     __shared__ __attribute__((aligned(16))) bf16_t xs[2][PLS * PLANE];
     __shared__ float rsl[SPLIT ? 1 : MT * ROWS_PER_TILE];  // per-slot RMSNorm factor
 
-    const int tile = SPLIT ? blockIdx.x / p.S : blockIdx.x;
     const int split = SPLIT ? blockIdx.x % p.S : 0;
+    const int wgi = SPLIT ? blockIdx.x / p.S : blockIdx.x;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int lc = lane & 31, lh = lane >> 5;
 
     // Buffer resources: one uniform resource per operand, fixed 32-bit
-    // per-lane offsets, uniform chunk offsets.  Out-of-range reads return 0.
+    // per-lane offsets, uniform chunk offsets.  Out-of-range reads return 0
+    // (and fetch nothing: a wave without a unit points past the buffer).
     const int wv = __builtin_amdgcn_readfirstlane(wave);
+    const int unit = wgi * p.G / p.WPS + wv;
+    const bool has_unit = unit < (wgi + 1) * p.G / p.WPS;
     const uint64_t wbytes = (uint64_t)p.vcols * (uint64_t)p.K * 2u;
     const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
         (void*)p.Wp, (short)0, (int)(wbytes > 0x7fffffffu ? 0x7fffffffu : wbytes), 0x00020000);
@@ -358,8 +383,9 @@ void k_gemm32(GemmP p) {
     uint32_t woff[NS];
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-        const uint32_t g16 = (uint32_t)(((tile * NW + wv) * NS + s) * 2 + (lc >> 4));
-        woff[s] = g16 * (uint32_t)p.KT * 1024u + (uint32_t)((lane & 15) + 16 * lh) * 16u;
+        const uint32_t g16 = (uint32_t)((unit * NS + s) * 2 + (lc >> 4));
+        woff[s] = has_unit ? g16 * (uint32_t)p.KT * 1024u + (uint32_t)((lane & 15) + 16 * lh) * 16u
+                           : 0x80000000u;
     }
     const __amdgpu_buffer_rsrc_t xres =
         __builtin_amdgcn_make_buffer_rsrc((void*)p.X, (short)0, PL * p.T * p.K * 2, 0x00020000);
@@ -519,11 +545,11 @@ void k_gemm32(GemmP p) {
 #pragma unroll
     for (int m = 0; m < (PK ? PA + 1 : MT); ++m) {
         const int t = m * 32 + lc;
-        if (t >= p.T || (PK && m == PA && lc >= 16)) continue;
+        if (!has_unit || t >= p.T || (PK && m == PA && lc >= 16)) continue;
         const float sc = SPLIT ? 1.0f : rsl[t];
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
-            const int grp = (tile * NW + wave) * NS + s;
+            const int grp = unit * NS + s;
             if (SPLIT) {
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
@@ -856,6 +882,8 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
         S = t;
     }
     p.S = S;
+    p.G = p.tiles * sh.NW;
+    p.WPS = p.tiles;
     p.part = sb.gpart;
     p.out = g.out;
     p.ldo = g.ldo;

@@ -194,6 +194,10 @@ struct Slot {
     int32_t* result_host = nullptr;  // pinned
     char* base = nullptr;        // device slot base
     SlotBufs bufs{};
+    // graph of the slot's last captured pass and the launch signature it
+    // was captured for (sd_verify_batch_graph)
+    hipGraphExec_t gexec = nullptr;
+    std::vector<int64_t> gkey;
 };
 
 }  // namespace
@@ -680,6 +684,7 @@ sd_status sd_verify_destroy(sd_ctx* c) {
             (void)hipEventSynchronize(s.done);
             (void)hipEventDestroy(s.done);
         }
+        if (s.gexec) (void)hipGraphExecDestroy(s.gexec);
         if (s.stage_host) (void)hipHostFree(s.stage_host);
         if (s.result_host) (void)hipHostFree(s.result_host);
     }
@@ -760,11 +765,89 @@ sd_status sd_kv_read(sd_ctx* c, int32_t user, int32_t layer, int32_t pos0, int32
     return kv_copy(c, user, layer, pos0, n, k, v, stream, 0);
 }
 
+// Device work of one pass: staging upload, forward + sampler (or the
+// sampler alone on caller logits), result download.  No allocation, no
+// memset: the whole sequence can be captured into a graph.
+static sd_status enqueue_pass(sd_ctx* c, Slot& s, const BatchView& bv, const float* logits,
+                              hipStream_t st) {
+    sd_status rs = hip_status(hipMemcpyAsync(s.base + c->lay.stage, s.stage_host, c->lay.st_bytes,
+                                             hipMemcpyHostToDevice, st));
+    if (rs == SD_OK) {
+        if (logits) {
+            launch_prepare(c->D, bv, s.bufs, st);
+            launch_sampler(c->D, bv, s.bufs, logits, st);
+            rs = hip_status(hipGetLastError());
+        } else {
+            rs = enqueue_forward(c, s, bv, st);
+            if (rs == SD_OK) {
+                ProfScope ps(c, SD_K_SAMPLER, st);
+                launch_sampler(c->D, bv, s.bufs, s.bufs.logits, st);
+                rs = hip_status(hipGetLastError());
+            }
+        }
+    }
+    if (rs == SD_OK)
+        rs = hip_status(hipMemcpyAsync(s.result_host, s.bufs.result,
+                                       (size_t)(2 * c->lay.Bmax + 4) * 4, hipMemcpyDeviceToHost, st));
+    return rs;
+}
+
+// Everything the launch shapes and kernel arguments of a pass depend on,
+// apart from the staged tables (which the graph's upload re-reads from the
+// pinned staging buffer at every launch).
+static std::vector<int64_t> launch_key(sd_ctx* c, const Slot& s, const BatchView& bv,
+                                       hipStream_t st) {
+    std::vector<int64_t> k = {bv.B, bv.T, bv.nd, bv.mode, (int64_t)bv.seed, (int64_t)bv.round,
+                              bv.n_items, bv.rows_max, (int64_t)(intptr_t)bv.drafts,
+                              (int64_t)(intptr_t)bv.q, (int64_t)(intptr_t)bv.accept_u,
+                              (int64_t)(intptr_t)st};
+    for (int b = 0; b < s.B; ++b) {
+        k.push_back(s.users[b]);
+        k.push_back(s.L[b]);
+        k.push_back(c->users[s.users[b]].prefix);
+    }
+    return k;
+}
+
+// Graph path: replay the slot's graph when the signature matches, else
+// capture the pass on `st` (thread-local capture mode), instantiate it and
+// launch it.  A stream the caller is already capturing gets the plain
+// launches (they become part of the caller's graph).
+static sd_status enqueue_graph(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t st) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    SD_HIP(hipStreamIsCapturing(st, &cs));
+    if (cs != hipStreamCaptureStatusNone) return enqueue_pass(c, s, bv, nullptr, st);
+    std::vector<int64_t> key = launch_key(c, s, bv, st);
+    if (!s.gexec || s.gkey != key) {
+        if (s.gexec) {
+            (void)hipGraphExecDestroy(s.gexec);
+            s.gexec = nullptr;
+            s.gkey.clear();
+        }
+        SD_HIP(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
+        const sd_status rs = enqueue_pass(c, s, bv, nullptr, st);
+        hipGraph_t g = nullptr;
+        const hipError_t e = hipStreamEndCapture(st, &g);
+        if (rs != SD_OK || e != hipSuccess || !g) {
+            if (g) (void)hipGraphDestroy(g);
+            return rs != SD_OK ? rs : SD_EHIP;
+        }
+        hipGraphExec_t ex = nullptr;
+        const hipError_t ei = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+        (void)hipGraphDestroy(g);
+        if (ei != hipSuccess) return SD_EHIP;
+        s.gexec = ex;
+        s.gkey = std::move(key);
+    }
+    return hip_status(hipGraphLaunch(s.gexec, st));
+}
+
 static sd_status submit(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t* assign,
                         const int32_t* draft_len, const int32_t* draft_tokens, const float* q,
                         const float* logits, int32_t mode, uint64_t seed, uint64_t round,
-                        const float* accept_u, sd_stream stream) {
+                        const float* accept_u, sd_stream stream, bool graph = false) {
     if (!c) return SD_EINVAL;
+    if (graph && (stream == nullptr || logits != nullptr)) return SD_EINVAL;
     if (mode != SD_GREEDY && mode != SD_STOCHASTIC && mode != SD_FORCE) return SD_EINVAL;
     if (!draft_tokens || (mode == SD_STOCHASTIC && !q)) return SD_EINVAL;
     const bool sample_only = logits != nullptr;
@@ -810,26 +893,9 @@ static sd_status submit(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t
     bv.q = q;
     bv.accept_u = accept_u;
     hipStream_t st = (hipStream_t)stream;
-    hipError_t e = hipMemcpyAsync(s.base + c->lay.stage, s.stage_host, c->lay.st_bytes,
-                                  hipMemcpyHostToDevice, st);
-    sd_status rs = hip_status(e);
-    if (rs == SD_OK) {
-        if (sample_only) {
-            launch_prepare(c->D, bv, s.bufs, st);
-            launch_sampler(c->D, bv, s.bufs, logits, st);
-            rs = hip_status(hipGetLastError());
-        } else {
-            rs = enqueue_forward(c, s, bv, st);
-            if (rs == SD_OK) {
-                ProfScope ps(c, SD_K_SAMPLER, st);
-                launch_sampler(c->D, bv, s.bufs, s.bufs.logits, st);
-                rs = hip_status(hipGetLastError());
-            }
-        }
-    }
-    if (rs == SD_OK)
-        rs = hip_status(hipMemcpyAsync(s.result_host, s.bufs.result,
-                                       (size_t)(2 * c->lay.Bmax + 4) * 4, hipMemcpyDeviceToHost, st));
+    // an open profiling window records events between launches: eager path
+    sd_status rs = graph && c->prof_class == 0 ? enqueue_graph(c, s, bv, st)
+                                               : enqueue_pass(c, s, bv, logits, st);
     if (rs == SD_OK) rs = hip_status(hipEventRecord(s.done, st));
     if (rs != SD_OK) {
         if (!sample_only)
@@ -851,6 +917,14 @@ sd_status sd_verify_batch(sd_ctx* c, int32_t batch, int32_t n_users, const int32
                           sd_stream stream) {
     return submit(c, batch, n_users, assign, draft_len, draft_tokens, q, nullptr, mode, seed, round,
                   accept_u, stream);
+}
+
+sd_status sd_verify_batch_graph(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t* assign,
+                                const int32_t* draft_len, const int32_t* draft_tokens, const float* q,
+                                int32_t mode, uint64_t seed, uint64_t round, const float* accept_u,
+                                sd_stream stream) {
+    return submit(c, batch, n_users, assign, draft_len, draft_tokens, q, nullptr, mode, seed, round,
+                  accept_u, stream, true);
 }
 
 sd_status sd_sample_logits(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t* assign,

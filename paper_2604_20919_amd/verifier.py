@@ -71,9 +71,12 @@ class Verifier:
 
     # --- batches ---
     def verify(self, batch: int, assign: Sequence[int], draft_len: Sequence[int], drafts, q,
-               mode="stochastic", seed: int = 0, round_: int = 0, accept_u=None, stream=None):
-        sv.sd_verify_batch(self.ctx, batch, assign, draft_len, drafts, q, mode, seed, round_,
-                           accept_u, stream)
+               mode="stochastic", seed: int = 0, round_: int = 0, accept_u=None, stream=None,
+               graph: bool = False):
+        """graph: replay the pass from a HIP graph (sd_verify_batch_graph);
+        needs a non-null stream."""
+        fn = sv.sd_verify_batch_graph if graph else sv.sd_verify_batch
+        fn(self.ctx, batch, assign, draft_len, drafts, q, mode, seed, round_, accept_u, stream)
 
     def sample(self, batch: int, assign, draft_len, drafts, q, logits, mode="stochastic",
                seed: int = 0, round_: int = 0, accept_u=None, stream=None):
