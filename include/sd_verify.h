@@ -230,6 +230,39 @@ sd_status sd_verify_batch_graph(sd_ctx* ctx, int32_t batch, int32_t n_users, con
                                 const float* accept_u, sd_stream stream);
 
 /*
+ * One decode step of a drafting model (Sec. II-A step 1 and eq. 13: each
+ * device generates its l_m drafts one token at a time and sends each with
+ * its probability; here the drafting model runs in its own context on the
+ * GPU).  For every user m with assign[m] == batch (ascending m) the forward
+ * covers one query slot, the root token at position i_m; its key and value
+ * are written into the user's pages.  The token is then drawn from the
+ * slot's distribution p = softmax(z) at temperature 1 -- exponential race
+ * keyed by (seed, round, user, slot 0) in SD_STOCHASTIC mode, argmax
+ * (lowest index on ties) in SD_GREEDY -- which is the bonus draw of
+ * sd_verify_batch with l_m = 0.
+ *   probs: device fp32 [rows][vocab], or NULL.  Receives p of each user's
+ *          slot, evaluated with the same expression the race uses, so the
+ *          drawn token is a draw from exactly these rows; pass them as
+ *          sd_verify_batch's q.
+ *   probs_row: host int32 [n_users] or NULL: the row of `probs` that
+ *          receives user m's distribution (entries of users outside the
+ *          batch are ignored; the caller guarantees the rows exist and are
+ *          distinct).  NULL: row b for the b-th batch user.  A drafting loop
+ *          points step j of user m at row draft_off[m] + j - 1 of the q array
+ *          it will pass to sd_verify_batch.  Negative rows: SD_EINVAL.
+ * Complete with sd_accept(batch, n_accepted, out_token, commit): every user
+ * gets a_m = 0 and out_token = the drawn token; commit = 1 advances the user
+ * by one position (i_m += 1, root := token), ready for the next step.
+ * Draws of one call are keyed by (seed, round): give every step of a
+ * drafting loop its own round value.  SD_FORCE is rejected (SD_EINVAL).
+ * SD_EINVAL also for probs_row without probs.  Other errors as
+ * sd_verify_batch (max_batch_tokens bounds the batch's user count here).
+ */
+sd_status sd_draft_batch(sd_ctx* ctx, int32_t batch, int32_t n_users, const int32_t* assign,
+                         int32_t mode, uint64_t seed, uint64_t round, float* probs,
+                         const int32_t* probs_row, sd_stream stream);
+
+/*
  * Wait for batch `batch` and return its decisions (Sec. II-A steps 2-3):
  *   n_accepted: host [M] (M of the sd_verify_batch call); entry m of every
  *               batch user receives a_m, the number of leading drafts accepted

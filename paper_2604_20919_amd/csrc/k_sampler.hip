@@ -214,6 +214,28 @@ __global__ __launch_bounds__(256) void k_samp_b2(SampP p, int chunks) {
     p.result[p.bmax + b] = tok;
 }
 
+// Decode-step output: the target distribution p of every slot, written
+// with the expression phase B's race evaluates, so a token drawn by the
+// race is a draw from exactly these rows.  One thread per four entries.
+__global__ __launch_bounds__(256) void k_probs(BatchView bv, const float* logits, const float* sstat,
+                                               float* probs, int V) {
+    const int t = blockIdx.y;
+    const int k = (blockIdx.x * 256 + threadIdx.x) * 4;
+    if (k >= V) return;
+    const float M = sstat[(size_t)t * 4 + 0], S = sstat[(size_t)t * 4 + 1];
+    const float* z = logits + (size_t)t * V;
+    float* o = probs + (size_t)bv.prow[bv.slot_b[t]] * V;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        if (k + e < V) o[k + e] = expf(z[k + e] - M) / S;
+}
+
+void launch_probs(const Dims& D, const BatchView& bv, const SlotBufs& sb, const float* logits,
+                  float* probs, hipStream_t s) {
+    const int blocks = ((D.V + 3) / 4 + 255) / 256;
+    hipLaunchKernelGGL(k_probs, dim3(blocks, bv.T), dim3(256), 0, s, bv, logits, sb.sstat, probs, D.V);
+}
+
 void launch_sampler(const Dims& D, const BatchView& bv, const SlotBufs& sb, const float* logits,
                     hipStream_t s) {
     SampP p;

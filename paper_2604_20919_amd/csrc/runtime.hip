@@ -36,7 +36,7 @@ int ceil_div(long a, long b) { return (int)((a + b - 1) / b); }
 struct Layout {
     // staging block (int32 offsets within the block)
     size_t st_user, st_prefix, st_L, st_root, st_soff, st_doff, st_sb, st_sj, st_pt, st_items,
-        st_ioff, st_flags, st_bytes;
+        st_ioff, st_flags, st_prow, st_bytes;
     // slot buffers (byte offsets within the slot)
     size_t stage, tok, cs, x, ssq, h, ffn, qbuf, attn, apart, aml, gpart, gcount, logits, sstat, spart,
         spartB, scount, scountB, result, slot_bytes;
@@ -119,6 +119,7 @@ Layout plan(const sd_config& c) {
     L.st_items = take_i((size_t)L.max_items * 4);
     L.st_ioff = take_i(L.Bmax + 1);
     L.st_flags = take_i(4);
+    L.st_prow = take_i(L.Bmax);
     L.st_bytes = o;
     // slot
     size_t s = 0;
@@ -189,6 +190,7 @@ struct Slot {
     int B = 0, T = 0, nd = 0;
     std::vector<int> users;  // global ids in batch order
     std::vector<int> L;
+    std::vector<int> prow;   // decode steps: destination row of each user's probabilities
     hipEvent_t done = nullptr;
     char* stage_host = nullptr;  // pinned
     int32_t* result_host = nullptr;  // pinned
@@ -270,25 +272,27 @@ BatchView make_view(sd_ctx* c, Slot& s) {
     v.items = (const int4*)(st + L.st_items);
     v.item_off = (const int32_t*)(st + L.st_ioff);
     v.flags = (int32_t*)(st + L.st_flags);
+    v.prow = (const int32_t*)(st + L.st_prow);
     v.max_pages = L.max_pages;
     return v;
 }
 
 // Collect the users of batch `batch` and validate every argument that does
 // not need the device.  Fills users / Ls / T / nd.
+// draft_len == NULL: a decode step, every batch user contributes its root
+// alone (l_m = 0, one query slot).
 sd_status collect_batch(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t* assign,
                         const int32_t* draft_len, bool need_active, std::vector<int>& users,
                         std::vector<int>& Ls, int& T, int& nd) {
-    if (batch < 0 || n_users < 1 || n_users > c->cfg.max_users || !assign || !draft_len)
-        return SD_EINVAL;
+    if (batch < 0 || n_users < 1 || n_users > c->cfg.max_users || !assign) return SD_EINVAL;
     users.clear();
     Ls.clear();
     T = 0;
     nd = 0;
     for (int m = 0; m < n_users; ++m) {
         if (assign[m] != batch) continue;
-        const int L = draft_len[m];
-        if (L < 1 || L > c->cfg.max_draft) return SD_EINVAL;
+        const int L = draft_len ? draft_len[m] : 0;
+        if (draft_len && (L < 1 || L > c->cfg.max_draft)) return SD_EINVAL;
         const User& u = c->users[m];
         if (need_active) {
             if (!u.active) return SD_EINVAL;
@@ -380,6 +384,8 @@ void build_stage(sd_ctx* c, Slot& s, int mode, bool with_items, int* n_items, in
         ioff[b + 1] = ni;
     }
     flags[0] = flags[1] = flags[2] = flags[3] = 0;
+    int32_t* prow = (int32_t*)(st + L.st_prow);
+    for (int b = 0; b < s.B; ++b) prow[b] = s.prow.empty() ? b : s.prow[b];
     *n_items = ni;
     *rows_max = (maxL + 1) * c->D.G();
 }
@@ -769,7 +775,7 @@ sd_status sd_kv_read(sd_ctx* c, int32_t user, int32_t layer, int32_t pos0, int32
 // sampler alone on caller logits), result download.  No allocation, no
 // memset: the whole sequence can be captured into a graph.
 static sd_status enqueue_pass(sd_ctx* c, Slot& s, const BatchView& bv, const float* logits,
-                              hipStream_t st) {
+                              hipStream_t st, float* probs = nullptr) {
     sd_status rs = hip_status(hipMemcpyAsync(s.base + c->lay.stage, s.stage_host, c->lay.st_bytes,
                                              hipMemcpyHostToDevice, st));
     if (rs == SD_OK) {
@@ -782,6 +788,7 @@ static sd_status enqueue_pass(sd_ctx* c, Slot& s, const BatchView& bv, const flo
             if (rs == SD_OK) {
                 ProfScope ps(c, SD_K_SAMPLER, st);
                 launch_sampler(c->D, bv, s.bufs, s.bufs.logits, st);
+                if (probs) launch_probs(c->D, bv, s.bufs, s.bufs.logits, probs, st);
                 rs = hip_status(hipGetLastError());
             }
         }
@@ -842,14 +849,17 @@ static sd_status enqueue_graph(sd_ctx* c, Slot& s, const BatchView& bv, hipStrea
     return hip_status(hipGraphLaunch(s.gexec, st));
 }
 
+// draft_len == NULL: decode step of sd_draft_batch (no drafts, one slot per
+// user); probs, if set, receives softmax of each slot's logits.
 static sd_status submit(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t* assign,
                         const int32_t* draft_len, const int32_t* draft_tokens, const float* q,
                         const float* logits, int32_t mode, uint64_t seed, uint64_t round,
-                        const float* accept_u, sd_stream stream, bool graph = false) {
+                        const float* accept_u, sd_stream stream, bool graph = false,
+                        float* probs = nullptr, const int32_t* probs_row = nullptr) {
     if (!c) return SD_EINVAL;
     if (graph && (stream == nullptr || logits != nullptr)) return SD_EINVAL;
     if (mode != SD_GREEDY && mode != SD_STOCHASTIC && mode != SD_FORCE) return SD_EINVAL;
-    if (!draft_tokens || (mode == SD_STOCHASTIC && !q)) return SD_EINVAL;
+    if (draft_len && (!draft_tokens || (mode == SD_STOCHASTIC && !q))) return SD_EINVAL;
     const bool sample_only = logits != nullptr;
     if (batch < 0) return SD_EINVAL;
     Slot& s = c->slots[batch % c->cfg.max_pending];
@@ -871,8 +881,19 @@ static sd_status submit(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t
             reserve_to(c, u, pages_for(u.prefix + Ls[b] + 1));
         }
     }
+    if (probs_row) {
+        for (int m : users)
+            if (probs_row[m] < 0) {
+                if (!sample_only)
+                    for (int m2 : users) release_to(c, c->users[m2], pages_for(c->users[m2].prefix));
+                return SD_EINVAL;
+            }
+    }
     s.users = users;
     s.L = Ls;
+    s.prow.clear();
+    if (probs_row)
+        for (int m : users) s.prow.push_back(probs_row[m]);
     s.B = (int)users.size();
     s.T = T;
     s.nd = nd;
@@ -895,7 +916,7 @@ static sd_status submit(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t
     hipStream_t st = (hipStream_t)stream;
     // an open profiling window records events between launches: eager path
     sd_status rs = graph && c->prof_class == 0 ? enqueue_graph(c, s, bv, st)
-                                               : enqueue_pass(c, s, bv, logits, st);
+                                               : enqueue_pass(c, s, bv, logits, st, probs);
     if (rs == SD_OK) rs = hip_status(hipEventRecord(s.done, st));
     if (rs != SD_OK) {
         if (!sample_only)
@@ -925,6 +946,14 @@ sd_status sd_verify_batch_graph(sd_ctx* c, int32_t batch, int32_t n_users, const
                                 sd_stream stream) {
     return submit(c, batch, n_users, assign, draft_len, draft_tokens, q, nullptr, mode, seed, round,
                   accept_u, stream, true);
+}
+
+sd_status sd_draft_batch(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t* assign,
+                         int32_t mode, uint64_t seed, uint64_t round, float* probs,
+                         const int32_t* probs_row, sd_stream stream) {
+    if (mode == SD_FORCE || (probs_row && !probs)) return SD_EINVAL;
+    return submit(c, batch, n_users, assign, nullptr, nullptr, nullptr, nullptr, mode, seed, round,
+                  nullptr, stream, false, probs, probs_row);
 }
 
 sd_status sd_sample_logits(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t* assign,

@@ -64,6 +64,7 @@ struct BatchView {
     const float* q;            // device input [nd][V]
     const float* accept_u;     // device input [nd] or null
     int32_t* flags;            // [1] device error bits, zeroed by the staging copy
+    const int32_t* prow;       // [B] decode steps: output row of each user's probabilities
 };
 
 // Workspace buffers of one batch slot.
@@ -148,6 +149,10 @@ int gemm_counter_count(const Dims& D);
 
 void launch_sampler(const Dims& D, const BatchView& bv, const SlotBufs& sb, const float* logits,
                     hipStream_t s);
+// probs[t][k] = exp(z[t][k] - m_t) / S_t from the sampler's per-slot
+// statistics (the same expression the race uses for p)
+void launch_probs(const Dims& D, const BatchView& bv, const SlotBufs& sb, const float* logits,
+                  float* probs, hipStream_t s);
 
 void launch_kv_copy(const Dims& D, const KVPool& kv, const int32_t* pages_dev, int layer,
                     int pos0, int n, const void* k, const void* v, int to_pool, hipStream_t s);

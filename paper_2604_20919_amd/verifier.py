@@ -78,6 +78,12 @@ class Verifier:
         fn = sv.sd_verify_batch_graph if graph else sv.sd_verify_batch
         fn(self.ctx, batch, assign, draft_len, drafts, q, mode, seed, round_, accept_u, stream)
 
+    def draft(self, batch: int, assign: Sequence[int], mode="stochastic", seed: int = 0,
+              round_: int = 0, probs=None, probs_row=None, stream=None):
+        """One decode step of the users of `batch` (sd_draft_batch); complete
+        with accept(batch, n_users, commit=True)."""
+        sv.sd_draft_batch(self.ctx, batch, assign, mode, seed, round_, probs, probs_row, stream)
+
     def sample(self, batch: int, assign, draft_len, drafts, q, logits, mode="stochastic",
                seed: int = 0, round_: int = 0, accept_u=None, stream=None):
         sv.sd_sample_logits(self.ctx, batch, assign, draft_len, drafts, q, logits, mode, seed,

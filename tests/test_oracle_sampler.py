@@ -248,3 +248,25 @@ def test_draws_depend_on_user_not_batch_position():
     res2 = oracle.sample("stochastic", users[perm], np.full(B, L), lg, dp, qp, seed=2, round_=5)
     assert np.array_equal(res2["n_acc"], res["n_acc"][perm])
     assert np.array_equal(res2["token"], res["token"][perm])
+
+
+def test_decode_step_draws_from_p():
+    """l_m = 0 (a drafting model's decode step): no accept trial, and the
+    emitted token follows p of the single slot; greedy takes its argmax
+    (lowest index on ties), zero-probability tokens are never drawn."""
+    rng = np.random.default_rng(23)
+    V, B = 7, 30000
+    p, _ = _tables(rng, 0, V, zero_p=[2])
+    logits = np.tile(_logits(p), (B, 1))
+    empty_q = np.zeros((0, V), np.float32)
+    res = oracle.sample("stochastic", np.arange(B), np.zeros(B), logits, np.zeros(0, np.int32),
+                        empty_q, seed=5, round_=1)
+    assert np.all(res["n_acc"] == 0)
+    ok, pv = _chi2_ok(np.bincount(res["token"], minlength=V), p[0])
+    assert ok, pv
+    # other rounds and seeds give other draws from the same law
+    res2 = oracle.sample("stochastic", np.arange(B), np.zeros(B), logits, np.zeros(0, np.int32),
+                         empty_q, seed=5, round_=2)
+    assert (res2["token"] != res["token"]).mean() > 0.5
+    g = oracle.sample("greedy", np.arange(3), np.zeros(3), logits[:3], np.zeros(0, np.int32), empty_q)
+    assert np.all(g["token"] == int(np.argmax(p[0])))
