@@ -308,12 +308,29 @@ __global__ __launch_bounds__(256) void k_qkrope(BatchView bv, const float* qkv, 
 #pragma unroll
     for (int b = 0; b < kNormKMax / kNormBlock; ++b)
         ssb[b] = nss != nullptr && b < nnb ? nss[(size_t)t * nnb + b] : 0.f;
-    float x0 = 0.f, x1 = 0.f;
-    if (act)
-        for (int sp = 0; sp < S; ++sp) {
-            x0 += src[sp * plane + lane];
-            x1 += src[sp * plane + lane + half];
+    // partial planes added in split order, eight planes' loads in flight at
+    // a time (key heads also fetch their value columns in the same batch)
+    const float* vs = qkv + (size_t)t * nqkv + (size_t)(hq + hkv) * hd + (size_t)(is_q ? 0 : h - hq) * hd;
+    float x0 = 0.f, x1 = 0.f, v0 = 0.f, v1 = 0.f;
+    for (int sp = 0; sp < S; sp += 8) {
+        float a0[8], a1[8], b0[8], b1[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const bool ok = act && sp + u < S;
+            const size_t o = (size_t)(sp + u) * plane + lane;
+            a0[u] = ok ? src[o] : 0.f;
+            a1[u] = ok ? src[o + half] : 0.f;
+            b0[u] = ok && !is_q ? vs[o] : 0.f;
+            b1[u] = ok && !is_q ? vs[o + half] : 0.f;
         }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            x0 += a0[u];
+            x1 += a1[u];
+            v0 += b0[u];
+            v1 += b1[u];
+        }
+    }
     float rt = 1.0f;
     if (nss != nullptr) {
         float ssx = 0.f;
@@ -352,12 +369,6 @@ __global__ __launch_bounds__(256) void k_qkrope(BatchView bv, const float* qkv, 
     TA* kd = base + kv.k_off(layer, page, g) + (size_t)off * hd;
     st(kd, lane, y0);
     st(kd, lane + half, y1);
-    const float* vs = qkv + (size_t)t * nqkv + (size_t)(hq + hkv) * hd + (size_t)g * hd;
-    float v0 = 0.f, v1 = 0.f;
-    for (int sp = 0; sp < S; ++sp) {
-        v0 += vs[sp * plane + lane];
-        v1 += vs[sp * plane + lane + half];
-    }
     v0 *= rt;
     v1 *= rt;
     TA* vd = base + kv.v_off(layer, page, g);
