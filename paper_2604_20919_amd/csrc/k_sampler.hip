@@ -19,6 +19,7 @@
 #include "sdv_internal.h"
 
 namespace sdv {
+static_assert(kVocabChunks <= 64, "chunk partials are merged by one wave");
 
 struct SampP {
     BatchView bv;
@@ -49,11 +50,34 @@ __global__ __launch_bounds__(256) void k_samp_a1(SampP p) {
     const int k0 = c * p.cw, k1 = min(p.V, k0 + p.cw);
     float m = -INFINITY, s = 0.f, bv = -INFINITY;
     int bi = 0x7fffffff;
-    for (int k = k0 + threadIdx.x; k < k1; k += 256) {
-        const float v = z[k];
+    auto add = [&](float v, int k) {
         if (v > bv) { bv = v; bi = k; }  // increasing k per thread: first max kept
         if (v > m) { s = (m == -INFINITY ? 0.f : s * expf(m - v)) + 1.f; m = v; }
         else if (v != -INFINITY) s += expf(v - m);
+    };
+    if ((p.V & 3) == 0) {
+        // four float4 loads per thread in flight, then the elements in
+        // increasing k order (chunk bounds are multiples of 4)
+        for (int k4 = k0 + 4 * threadIdx.x; k4 < k1; k4 += 4 * 1024) {
+            float4 v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int k = k4 + u * 1024;
+                v[u] = k < k1 ? *(const float4*)(z + k) : float4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int k = k4 + u * 1024;
+                if (k < k1) {
+                    add(v[u].x, k);
+                    add(v[u].y, k + 1);
+                    add(v[u].z, k + 2);
+                    add(v[u].w, k + 3);
+                }
+            }
+        }
+    } else {
+        for (int k = k0 + threadIdx.x; k < k1; k += 256) add(z[k], k);
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
@@ -79,16 +103,30 @@ __global__ __launch_bounds__(256) void k_samp_a1(SampP p) {
 // A2: one thread per slot: merge the chunk partials in chunk order and take
 // the slot's accept decision for the draft that follows it
 __global__ __launch_bounds__(256) void k_samp_a2(SampP p, int chunks) {
-    const int t = blockIdx.x * 256 + threadIdx.x;
+    const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
     const BatchView& bv = p.bv;
     if (t >= bv.T) return;
+    // lane i holds chunk i's partial; a fixed butterfly merges them (ties of
+    // the argmax to the lowest index, so the result is the chunk-order one)
     float M = -INFINITY, S = 0.f, BV = -INFINITY;
-    int BI = 0;
-    for (int i = 0; i < chunks; ++i) {
-        const float* e = p.spartA + ((size_t)t * kVocabChunks + i) * 4;
-        merge_ms(M, S, e[0], e[1]);
-        if (e[2] > BV) { BV = e[2]; BI = __float_as_int(e[3]); }
+    int BI = 0x7fffffff;
+    if (lane < chunks) {
+        const float4 e = *(const float4*)(p.spartA + ((size_t)t * kVocabChunks + lane) * 4);
+        M = e.x; S = e.y; BV = e.z; BI = __float_as_int(e.w);
     }
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const float m2 = __shfl_xor(M, o, 64), s2 = __shfl_xor(S, o, 64);
+        const float v2 = __shfl_xor(BV, o, 64);
+        const int i2 = __shfl_xor(BI, o, 64);
+        // both partners combine the pair in the same (lower lane first) order
+        if (lane & o) { float mt = M, st = S; M = m2; S = s2; merge_ms(M, S, mt, st); }
+        else merge_ms(M, S, m2, s2);
+        if (v2 > BV || (v2 == BV && i2 < BI)) { BV = v2; BI = i2; }
+    }
+    if (BI == 0x7fffffff) BI = 0;  // a row of -inf logits only
+    if (lane != 0) return;
     const int b = bv.slot_b[t], j = bv.slot_j[t];
     float acc = 0.f;
     if (j < bv.L[b]) {
@@ -192,24 +230,34 @@ __global__ __launch_bounds__(256) void k_samp_b1(SampP p) {
 // slot (greedy / force), or the race winner merged over chunks in chunk
 // order (ties to the lowest index)
 __global__ __launch_bounds__(256) void k_samp_b2(SampP p, int chunks) {
-    const int b = blockIdx.x * 256 + threadIdx.x;
+    const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
     const BatchView& bv = p.bv;
-    if (b == 0) p.result[2 * p.bmax] = *bv.flags;
+    if (b == 0 && lane == 0) p.result[2 * p.bmax] = *bv.flags;
     if (b >= bv.B) return;
     const int a = leading_accepts(p, b);
     int tok;
     if (bv.mode != 1) {
         tok = __float_as_int(p.sstat[(size_t)(bv.slot_off[b] + a) * 4 + 2]);
     } else {
+        // lane i holds chunk i's two race winners; the best key wins, ties to
+        // the lowest token index (the chunk-order result)
         float BR = -1.f, BP = -1.f;
-        int IR = 0, IP = 0;
-        for (int i = 0; i < chunks; ++i) {
-            const float* e = p.spartB + ((size_t)b * kVocabChunks + i) * 4;
-            if (e[0] > BR) { BR = e[0]; IR = __float_as_int(e[1]); }
-            if (e[2] > BP) { BP = e[2]; IP = __float_as_int(e[3]); }
+        int IR = 0x7fffffff, IP = 0x7fffffff;
+        if (lane < chunks) {
+            const float4 e = *(const float4*)(p.spartB + ((size_t)b * kVocabChunks + lane) * 4);
+            BR = e.x; IR = __float_as_int(e.y); BP = e.z; IP = __float_as_int(e.w);
+        }
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const float r2 = __shfl_xor(BR, o, 64), p2 = __shfl_xor(BP, o, 64);
+            const int ir2 = __shfl_xor(IR, o, 64), ip2 = __shfl_xor(IP, o, 64);
+            if (r2 > BR || (r2 == BR && ir2 < IR)) { BR = r2; IR = ir2; }
+            if (p2 > BP || (p2 == BP && ip2 < IP)) { BP = p2; IP = ip2; }
         }
         tok = (a < bv.L[b] && BR > 0.f) ? IR : IP;
     }
+    if (lane != 0) return;
     p.result[b] = a;
     p.result[p.bmax + b] = tok;
 }
@@ -252,9 +300,9 @@ void launch_sampler(const Dims& D, const BatchView& bv, const SlotBufs& sb, cons
     p.bmax = sb.bmax;
     const int chunks = (D.V + p.cw - 1) / p.cw;
     hipLaunchKernelGGL(k_samp_a1, dim3(bv.T, chunks), dim3(256), 0, s, p);
-    hipLaunchKernelGGL(k_samp_a2, dim3((bv.T + 255) / 256), dim3(256), 0, s, p, chunks);
+    hipLaunchKernelGGL(k_samp_a2, dim3((bv.T + 3) / 4), dim3(256), 0, s, p, chunks);
     if (bv.mode == 1) hipLaunchKernelGGL(k_samp_b1, dim3(bv.B, chunks), dim3(256), 0, s, p);
-    hipLaunchKernelGGL(k_samp_b2, dim3((bv.B + 255) / 256), dim3(256), 0, s, p, chunks);
+    hipLaunchKernelGGL(k_samp_b2, dim3((bv.B + 3) / 4), dim3(256), 0, s, p, chunks);
 }
 
 }  // namespace sdv

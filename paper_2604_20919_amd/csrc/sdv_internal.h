@@ -10,7 +10,7 @@ constexpr int kPageTokens = 16;   // tokens per KV page
 constexpr int kAttnItemsMax = 1024;  // attention work items per batch (beyond one per (user, KV head))
 constexpr int kAttnWGsPerCU = 2;     // co-resident attention workgroups per CU (register bound)
 constexpr int kAttnBuffers = 3;      // LDS ring of the attention kernel (buffers - 1 blocks in flight)
-constexpr int kVocabChunks = 16;  // vocab split of the sampler kernels
+constexpr int kVocabChunks = 64;  // vocab split of the sampler kernels (at most 64: one wave merges)
 constexpr int kNormBlock = 1024;   // columns per sum-of-squares block of x
 constexpr int kNormKMax = 8192;    // widest model dimension the GEMM can normalise on load
 constexpr int kMaxPending = 8;
