@@ -47,6 +47,9 @@ def parse():
                     help="1: each batch's pass is replayed from a HIP graph (sd_verify_batch_graph); "
                          "0: eager launches; -1 (default): graphs for the pipelined multi-batch "
                          "workload, whose definition asks for them, eager otherwise")
+    ap.add_argument("--q-topk", type=int, default=0,
+                    help="K > 0: draft rows sent as sparse payloads (top-K tokens plus a uniform "
+                         "remainder, drafts redrawn from them) and verified by sd_verify_batch_sparse")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 1 GiB device copy (scale reference for HBM byte counters)")
     return ap.parse_args()
@@ -119,6 +122,12 @@ def main():
     kv_tokens = int(w.prefix_len.sum())
     log(f"cached KV of {kv_tokens} tokens written in {time.time() - t0:.1f}s")
 
+    sparse = None
+    if args.q_topk > 0:
+        sparse = []
+        for b in batches:
+            sr = wl.sparsify(b, args.q_topk, w.seed)   # redraws b.drafts from the sparse rows
+            sparse.append(tuple(torch.from_numpy(a).cuda() for a in (sr.idx, sr.val, sr.rest)))
     dev_in = [batch_to_device(b) for b in batches]
     if args.mode == "greedy":
         plant_greedy_drafts(v, w, batches, dev_in, torch)
@@ -127,6 +136,10 @@ def main():
     def step():
         for n in range(nb):
             d, q, au = dev_in[n]
+            if sparse is not None and args.mode == "stochastic":
+                v.verify_sparse(n, w.assign, w.draft_len, d, *sparse[n], args.mode, seed=w.seed,
+                                round_=0, accept_u=au, stream=streams[n % len(streams)])
+                continue
             v.verify(n, w.assign, w.draft_len, d, q, args.mode, seed=w.seed, round_=0,
                      accept_u=au, stream=streams[n % len(streams)], graph=bool(args.graph))
         acc = 0
@@ -196,7 +209,12 @@ def main():
     # attention (all layers, KV streamed once per user) and sampler rates
     kv_read_step = sum(int(p + l + 1) for p, l in zip(w.prefix_len, w.draft_len)) * m.kv_bytes_per_token()
     attn_ms = class_ms(sv.SD_K_ATTN)
-    samp_bytes = sum(b.T for b in batches) * m.vocab * 4 + int(w.n_users) * m.vocab * 4
+    nd_all = int(sum(int(b.draft_len.sum()) for b in batches))
+    if sparse is not None:
+        # logits once; every sparse row's K entries (the accept lookups) and remainders
+        samp_bytes = sum(b.T for b in batches) * m.vocab * 4 + nd_all * (args.q_topk * 8 + 4)
+    else:
+        samp_bytes = sum(b.T for b in batches) * m.vocab * 4 + int(w.n_users) * m.vocab * 4
     samp_ms = class_ms(sv.SD_K_SAMPLER)
     kernels = {
         "attention": {"achieved": round(kv_read_step / (attn_ms / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
@@ -206,7 +224,8 @@ def main():
         "sampler": {"achieved": round(samp_bytes / (samp_ms / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(samp_bytes / (samp_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
                     "bytes_per_step": samp_bytes, "ms_per_step": round(samp_ms, 4),
-                    "note": "accept/reject + resample kernels; bytes = T x V fp32 logits + one q row per user"},
+                    "note": ("accept/reject + resample kernels; bytes = T x V fp32 logits + "
+                             + ("the sparse rows" if sparse is not None else "one q row per user"))},
     }
 
     breakdown = None
@@ -238,7 +257,11 @@ def main():
         "data": "synthetic (random-init weights N(0,0.02), synthetic KV N(0,1), synthetic draft q)",
         "config": {"workload": args.workload, "model": m.name, "mode": args.mode,
                    "users": int(w.n_users), "batches": nb, "verified_tokens_per_step": verified_step,
-                   "prefix_tokens": kv_tokens, "hip_graph": bool(args.graph),
+                   "prefix_tokens": kv_tokens, "hip_graph": bool(args.graph) and sparse is None,
+                   "q_payload": (f"sparse top-{args.q_topk} + remainder" if sparse is not None
+                                 else "dense fp32 rows"),
+                   "q_payload_bytes_per_step": (nd_all * (args.q_topk * 8 + 4) if sparse is not None
+                                                else nd_all * m.vocab * 4),
                    "streams": len(streams)},
         "verified_tokens_per_s": round(verified_step / (ms_step / 1e3), 1),
         "accepted_per_step": acc_step,

@@ -230,6 +230,32 @@ sd_status sd_verify_batch_graph(sd_ctx* ctx, int32_t batch, int32_t n_users, con
                                 const float* accept_u, sd_stream stream);
 
 /*
+ * sd_verify_batch with sparse draft distributions, the compact payload of
+ * Sec. II-A (drafted tokens plus a little probability information per draft).
+ * Draft row r (the batch's drafts in order, as for q) is given by q_k token
+ * ids q_idx[r][0..q_k-1] (device int32 [sum l_m][q_k], distinct, in
+ * 0..vocab-1), their probabilities q_val[r][.] (device fp32 [sum l_m][q_k])
+ * and the probability q_rest[r] (device fp32 [sum l_m]) that every token not
+ * listed carries:  q_r(k) = q_val[r][i] if k == q_idx[r][i], else q_rest[r].
+ * Verification is exact for drafts drawn from that distribution (a device
+ * that drafts from its top-q_k tokens plus a uniform remainder, say): the
+ * accept ratio uses q_r(d) and the residual at the stop slot uses q_r over
+ * the whole vocabulary, exactly as with the equivalent dense row, and the
+ * decisions equal those of sd_verify_batch given that dense row.  The rows
+ * are read, not checked: they must describe a distribution (the caller's
+ * contract, as for dense q).  The sparse rows matter only in SD_STOCHASTIC
+ * mode.  Completion and other rules as sd_verify_batch.
+ * Errors: SD_EINVAL (q_k outside 1..4096, a NULL row pointer, or the
+ * sd_verify_batch conditions), SD_ENOTIMPL (vocab above 262144).
+ */
+sd_status sd_verify_batch_sparse(sd_ctx* ctx, int32_t batch, int32_t n_users,
+                                 const int32_t* assign, const int32_t* draft_len,
+                                 const int32_t* draft_tokens, const int32_t* q_idx,
+                                 const float* q_val, const float* q_rest, int32_t q_k,
+                                 int32_t mode, uint64_t seed, uint64_t round,
+                                 const float* accept_u, sd_stream stream);
+
+/*
  * One decode step of a drafting model (Sec. II-A step 1 and eq. 13: each
  * device generates its l_m drafts one token at a time and sends each with
  * its probability; here the drafting model runs in its own context on the

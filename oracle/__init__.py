@@ -280,6 +280,18 @@ def prefill(m: wl.ModelShape, weights: WeightSource, tokens, kv_bf16: Optional[b
 # sampler
 # ----------------------------------------------------------------------------
 
+def expand_sparse_q(idx, val, rest, V: int) -> np.ndarray:
+    """Dense rows of sparse draft distributions: q_r(k) = val[r][i] where
+    k = idx[r][i], else rest[r] (the compact payload of drafted tokens plus a
+    little probability information, DiP-SD Sec. II-A).  The accept/resample
+    step is defined on these dense rows; nothing else changes."""
+    idx = np.asarray(idx)
+    q = np.repeat(np.asarray(rest, np.float32)[:, None], V, axis=1)
+    rows = np.arange(idx.shape[0])[:, None]
+    q[rows, idx] = np.asarray(val, np.float32)
+    return q
+
+
 def sample(mode, users, draft_len, logits, drafts, q, accept_u=None, seed: int = 0,
            round_: int = 0):
     """Verify decisions for a batch: returns dict with n_acc, token, and the

@@ -126,8 +126,19 @@ __global__ __launch_bounds__(256) void k_samp_a2(SampP p, int chunks) {
         if (v2 > BV || (v2 == BV && i2 < BI)) { BV = v2; BI = i2; }
     }
     if (BI == 0x7fffffff) BI = 0;  // a row of -inf logits only
-    if (lane != 0) return;
     const int b = bv.slot_b[t], j = bv.slot_j[t];
+    // sparse q: q(d) of the draft that follows this slot, looked up by the
+    // whole wave (token ids of a row are distinct, so at most one lane hits)
+    float qsp = -1.f;
+    if (bv.qk > 0 && bv.mode == 1 && j < bv.L[b]) {
+        const int di = bv.draft_off[b] + j;
+        const int d = bv.drafts[di];
+        for (int e = lane; e < bv.qk; e += 64)
+            if (bv.q_idx[(size_t)di * bv.qk + e] == d) qsp = bv.q_val[(size_t)di * bv.qk + e];
+        qsp = wave_max(qsp);
+        if (qsp < 0.f) qsp = bv.q_rest[di];
+    }
+    if (lane != 0) return;
     float acc = 0.f;
     if (j < bv.L[b]) {
         const int di = bv.draft_off[b] + j;
@@ -137,7 +148,7 @@ __global__ __launch_bounds__(256) void k_samp_a2(SampP p, int chunks) {
         else if (bv.mode == 2) acc = 1.f;
         else {
             const float pd = expf(p.logits[(size_t)t * p.V + d] - M) / S;
-            const float qd = bv.q[(size_t)di * p.V + d];
+            const float qd = bv.qk > 0 ? qsp : bv.q[(size_t)di * p.V + d];
             const float r = pd / qd;
             float u;
             if (bv.accept_u) u = bv.accept_u[di];
@@ -164,9 +175,11 @@ __device__ __forceinline__ int leading_accepts(const SampP& p, int b) {
 // B1 (stochastic): per (user, vocab chunk): best race keys of the residual
 // max(0, p - q) at the stop slot and of p itself (the bonus draw, and the
 // fallback when the residual is empty); both use the same unit exponentials
+template <bool SPARSE>
 __global__ __launch_bounds__(256) void k_samp_b1(SampP p) {
     __shared__ float sk[2][4];
     __shared__ int sidx[2][4];
+    __shared__ float qloc[SPARSE ? kSparseChunkMax : 1];  // sparse q over this chunk
     const int b = blockIdx.x, c = blockIdx.y;
     const BatchView& bv = p.bv;
     const int Lb = bv.L[b];
@@ -176,9 +189,26 @@ __global__ __launch_bounds__(256) void k_samp_b1(SampP p) {
     const float M = st4[0], S = st4[1];
     const float* z = p.logits + (size_t)row * p.V;
     const bool resid = a < Lb;
-    const float* qr = resid ? bv.q + (size_t)(bv.draft_off[b] + a) * p.V : nullptr;
-    const uint64_t user = (uint64_t)bv.user_id[b];
     const int k0 = c * p.cw, k1 = min(p.V, k0 + p.cw);
+    const float* qr = nullptr;
+    if (SPARSE) {
+        // the stop slot's q on [k0, k1): the remainder probability, then the
+        // listed tokens that fall into the chunk
+        if (resid) {
+            const size_t di = (size_t)bv.draft_off[b] + a;
+            const float rest = bv.q_rest[di];
+            for (int k = threadIdx.x; k < k1 - k0; k += 256) qloc[k] = rest;
+            __syncthreads();
+            for (int e = threadIdx.x; e < bv.qk; e += 256) {
+                const int tk = bv.q_idx[di * bv.qk + e];
+                if (tk >= k0 && tk < k1) qloc[tk - k0] = bv.q_val[di * bv.qk + e];
+            }
+            __syncthreads();
+        }
+    } else {
+        qr = resid ? bv.q + (size_t)(bv.draft_off[b] + a) * p.V : nullptr;
+    }
+    const uint64_t user = (uint64_t)bv.user_id[b];
     float br = -1.f, bp = -1.f;
     int ir = 0x7fffffff, ip = 0x7fffffff;
     for (int k4 = k0 + 4 * threadIdx.x; k4 < k1; k4 += 4 * 256) {
@@ -196,7 +226,7 @@ __global__ __launch_bounds__(256) void k_samp_b1(SampP p) {
                 if (kp > bp) { bp = kp; ip = k; }
             }
             if (resid) {
-                const float wk = fmaxf(pk - qr[k], 0.f);
+                const float wk = fmaxf(pk - (SPARSE ? qloc[k - k0] : qr[k]), 0.f);
                 if (wk > 0.f) {
                     const float kr = wk / E;
                     if (kr > br) { br = kr; ir = k; }
@@ -301,7 +331,12 @@ void launch_sampler(const Dims& D, const BatchView& bv, const SlotBufs& sb, cons
     const int chunks = (D.V + p.cw - 1) / p.cw;
     hipLaunchKernelGGL(k_samp_a1, dim3(bv.T, chunks), dim3(256), 0, s, p);
     hipLaunchKernelGGL(k_samp_a2, dim3((bv.T + 3) / 4), dim3(256), 0, s, p, chunks);
-    if (bv.mode == 1) hipLaunchKernelGGL(k_samp_b1, dim3(bv.B, chunks), dim3(256), 0, s, p);
+    if (bv.mode == 1) {
+        if (bv.qk > 0)
+            hipLaunchKernelGGL(k_samp_b1<true>, dim3(bv.B, chunks), dim3(256), 0, s, p);
+        else
+            hipLaunchKernelGGL(k_samp_b1<false>, dim3(bv.B, chunks), dim3(256), 0, s, p);
+    }
     hipLaunchKernelGGL(k_samp_b2, dim3((bv.B + 3) / 4), dim3(256), 0, s, p, chunks);
 }
 

@@ -851,15 +851,25 @@ static sd_status enqueue_graph(sd_ctx* c, Slot& s, const BatchView& bv, hipStrea
 
 // draft_len == NULL: decode step of sd_draft_batch (no drafts, one slot per
 // user); probs, if set, receives softmax of each slot's logits.
+// Sparse draft distributions of sd_verify_batch_sparse (k == 0: dense q).
+struct SparseQ {
+    const int32_t* idx = nullptr;
+    const float* val = nullptr;
+    const float* rest = nullptr;
+    int32_t k = 0;
+};
+
 static sd_status submit(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t* assign,
                         const int32_t* draft_len, const int32_t* draft_tokens, const float* q,
                         const float* logits, int32_t mode, uint64_t seed, uint64_t round,
                         const float* accept_u, sd_stream stream, bool graph = false,
-                        float* probs = nullptr, const int32_t* probs_row = nullptr) {
+                        float* probs = nullptr, const int32_t* probs_row = nullptr,
+                        SparseQ sq = SparseQ{}) {
     if (!c) return SD_EINVAL;
     if (graph && (stream == nullptr || logits != nullptr)) return SD_EINVAL;
     if (mode != SD_GREEDY && mode != SD_STOCHASTIC && mode != SD_FORCE) return SD_EINVAL;
-    if (draft_len && (!draft_tokens || (mode == SD_STOCHASTIC && !q))) return SD_EINVAL;
+    const bool need_q = mode == SD_STOCHASTIC && sq.k == 0;
+    if (draft_len && (!draft_tokens || (need_q && !q))) return SD_EINVAL;
     const bool sample_only = logits != nullptr;
     if (batch < 0) return SD_EINVAL;
     Slot& s = c->slots[batch % c->cfg.max_pending];
@@ -913,6 +923,10 @@ static sd_status submit(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t
     bv.drafts = draft_tokens;
     bv.q = q;
     bv.accept_u = accept_u;
+    bv.q_idx = sq.idx;
+    bv.q_val = sq.val;
+    bv.q_rest = sq.rest;
+    bv.qk = sq.k;
     hipStream_t st = (hipStream_t)stream;
     // an open profiling window records events between launches: eager path
     sd_status rs = graph && c->prof_class == 0 ? enqueue_graph(c, s, bv, st)
@@ -946,6 +960,24 @@ sd_status sd_verify_batch_graph(sd_ctx* c, int32_t batch, int32_t n_users, const
                                 sd_stream stream) {
     return submit(c, batch, n_users, assign, draft_len, draft_tokens, q, nullptr, mode, seed, round,
                   accept_u, stream, true);
+}
+
+sd_status sd_verify_batch_sparse(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t* assign,
+                                 const int32_t* draft_len, const int32_t* draft_tokens,
+                                 const int32_t* q_idx, const float* q_val, const float* q_rest,
+                                 int32_t q_k, int32_t mode, uint64_t seed, uint64_t round,
+                                 const float* accept_u, sd_stream stream) {
+    if (!c || q_k < 1 || q_k > kSparseKMax || !q_idx || !q_val || !q_rest) return SD_EINVAL;
+    // the race kernel holds one vocab chunk of q in LDS
+    const int cw = ((c->D.V + kVocabChunks - 1) / kVocabChunks + 3) & ~3;
+    if (cw > kSparseChunkMax) return SD_ENOTIMPL;
+    SparseQ sq;
+    sq.idx = q_idx;
+    sq.val = q_val;
+    sq.rest = q_rest;
+    sq.k = q_k;
+    return submit(c, batch, n_users, assign, draft_len, draft_tokens, nullptr, nullptr, mode, seed,
+                  round, accept_u, stream, false, nullptr, nullptr, sq);
 }
 
 sd_status sd_draft_batch(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t* assign,

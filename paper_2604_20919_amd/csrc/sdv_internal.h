@@ -14,6 +14,8 @@ constexpr int kVocabChunks = 64;  // vocab split of the sampler kernels (at most
 constexpr int kNormBlock = 1024;   // columns per sum-of-squares block of x
 constexpr int kNormKMax = 8192;    // widest model dimension the GEMM can normalise on load
 constexpr int kMaxPending = 8;
+constexpr int kSparseChunkMax = 4096;  // largest vocab chunk of the sparse-q race (vocab <= 64 * 4096)
+constexpr int kSparseKMax = 4096;      // most listed tokens per sparse draft row
 
 // Model dimensions as the kernels see them.
 struct Dims {
@@ -63,6 +65,13 @@ struct BatchView {
     const int32_t* drafts;     // device input [nd]
     const float* q;            // device input [nd][V]
     const float* accept_u;     // device input [nd] or null
+    // sparse draft distributions (qk > 0; q is then unused): row r lists qk
+    // tokens q_idx[r][.] with probabilities q_val[r][.]; every other token
+    // has probability q_rest[r]
+    const int32_t* q_idx;      // device input [nd][qk]
+    const float* q_val;        // device input [nd][qk]
+    const float* q_rest;       // device input [nd]
+    int qk;
     int32_t* flags;            // [1] device error bits, zeroed by the staging copy
     const int32_t* prow;       // [B] decode steps: output row of each user's probabilities
 };

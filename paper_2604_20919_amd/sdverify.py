@@ -24,7 +24,7 @@ MODES = {"greedy": SD_GREEDY, "stochastic": SD_STOCHASTIC, "force": SD_FORCE}
 
 EXPORTS = ("sd_verify_query_sizes", "sd_verify_init", "sd_verify_destroy", "sd_user_reset",
            "sd_user_release", "sd_user_state", "sd_kv_write", "sd_kv_read", "sd_verify_batch",
-           "sd_verify_batch_graph", "sd_draft_batch", "sd_accept", "sd_sample_logits", "sd_debug_logits", "sd_profile_begin", "sd_profile_end",
+           "sd_verify_batch_graph", "sd_verify_batch_sparse", "sd_draft_batch", "sd_accept", "sd_sample_logits", "sd_debug_logits", "sd_profile_begin", "sd_profile_end",
            "sd_status_str")
 SD_K_QKV, SD_K_ATTN, SD_K_O, SD_K_GATEUP, SD_K_DOWN, SD_K_LMHEAD, SD_K_SAMPLER, SD_K_SMALL = range(1, 9)
 
@@ -77,6 +77,8 @@ def lib() -> ctypes.CDLL:
         L.sd_verify_batch.argtypes = [vp, i32, i32, vp, vp, vp, vp, i32, u64, u64, vp, vp]
         L.sd_verify_batch_graph.argtypes = [vp, i32, i32, vp, vp, vp, vp, i32, u64, u64, vp, vp]
         L.sd_draft_batch.argtypes = [vp, i32, i32, vp, i32, u64, u64, vp, vp, vp]
+        L.sd_verify_batch_sparse.argtypes = [vp, i32, i32, vp, vp, vp, vp, vp, vp, i32, i32, u64, u64,
+                                             vp, vp]
         L.sd_accept.argtypes = [vp, i32, vp, vp, i32]
         L.sd_sample_logits.argtypes = [vp, i32, i32, vp, vp, vp, vp, vp, i32, u64, u64, vp, vp]
         L.sd_debug_logits.argtypes = [vp, i32, vp, vp]
@@ -185,6 +187,18 @@ def sd_verify_batch_graph(ctx: int, batch: int, assign: Sequence[int], draft_len
     _check("sd_verify_batch_graph", lib().sd_verify_batch_graph(
         ctx, batch, a.size, a.ctypes.data, L.ctypes.data, _dev(draft_tokens), _dev(q), mode,
         int(seed), int(round_), _dev(accept_u), _stream(stream)))
+
+
+def sd_verify_batch_sparse(ctx: int, batch: int, assign: Sequence[int], draft_len: Sequence[int],
+                           draft_tokens, q_idx, q_val, q_rest, mode, seed: int = 0, round_: int = 0,
+                           accept_u=None, stream=None) -> None:
+    """q_idx int32 [nd][K], q_val fp32 [nd][K], q_rest fp32 [nd] (device)."""
+    a, L = _host_i32(assign), _host_i32(draft_len)
+    mode = MODES[mode] if isinstance(mode, str) else int(mode)
+    k = int(q_idx.shape[1]) if hasattr(q_idx, "shape") else 0
+    _check("sd_verify_batch_sparse", lib().sd_verify_batch_sparse(
+        ctx, batch, a.size, a.ctypes.data, L.ctypes.data, _dev(draft_tokens), _dev(q_idx), _dev(q_val),
+        _dev(q_rest), k, mode, int(seed), int(round_), _dev(accept_u), _stream(stream)))
 
 
 def sd_draft_batch(ctx: int, batch: int, assign: Sequence[int], mode, seed: int = 0,

@@ -78,6 +78,13 @@ class Verifier:
         fn = sv.sd_verify_batch_graph if graph else sv.sd_verify_batch
         fn(self.ctx, batch, assign, draft_len, drafts, q, mode, seed, round_, accept_u, stream)
 
+    def verify_sparse(self, batch: int, assign: Sequence[int], draft_len: Sequence[int], drafts,
+                      q_idx, q_val, q_rest, mode="stochastic", seed: int = 0, round_: int = 0,
+                      accept_u=None, stream=None):
+        """Verification with sparse draft rows (sd_verify_batch_sparse)."""
+        sv.sd_verify_batch_sparse(self.ctx, batch, assign, draft_len, drafts, q_idx, q_val, q_rest,
+                                  mode, seed, round_, accept_u, stream)
+
     def draft(self, batch: int, assign: Sequence[int], mode="stochastic", seed: int = 0,
               round_: int = 0, probs=None, probs_row=None, stream=None):
         """One decode step of the users of `batch` (sd_draft_batch); complete

@@ -270,3 +270,45 @@ def test_decode_step_draws_from_p():
     assert (res2["token"] != res["token"]).mean() > 0.5
     g = oracle.sample("greedy", np.arange(3), np.zeros(3), logits[:3], np.zeros(0, np.int32), empty_q)
     assert np.all(g["token"] == int(np.argmax(p[0])))
+
+
+def _sparse_rows(q, K):
+    """Top-K of each dense row plus a uniform remainder (test tables)."""
+    V = q.shape[1]
+    idx = np.argsort(-q, axis=1, kind="stable")[:, :K]
+    val = np.take_along_axis(q, idx, axis=1)
+    rest = (1.0 - val.sum(1)) / (V - K)
+    return idx.astype(np.int32), val.astype(np.float32), rest.astype(np.float32)
+
+
+def test_sparse_rows_expand_to_their_definition():
+    rng = np.random.default_rng(29)
+    V, K = 9, 3
+    _, q = _tables(rng, 4, V)
+    idx, val, rest = _sparse_rows(q, K)
+    dense = oracle.expand_sparse_q(idx, val, rest, V)
+    for r in range(q.shape[0]):
+        for k in range(V):
+            hit = np.nonzero(idx[r] == k)[0]
+            want = val[r, hit[0]] if hit.size else rest[r]
+            assert dense[r, k] == want
+        assert abs(dense[r].astype(np.float64).sum() - 1.0) < 1e-6
+
+
+def test_sparse_draft_rows_keep_the_target_distribution():
+    """Drafts drawn from top-K-plus-remainder rows and verified against
+    those rows: the first emitted token still follows p (the speculative
+    sampling law holds for any draft distribution given exactly)."""
+    rng = np.random.default_rng(31)
+    L, V, K, B = 2, 8, 3, 30000
+    p, q = _tables(rng, L, V)
+    idx, val, rest = _sparse_rows(q, K)
+    qs = oracle.expand_sparse_q(idx, val, rest, V).astype(np.float64)
+    qs /= qs.sum(1, keepdims=True)
+    logits, qq, drafts = _batch(p, qs, B, rng)
+    # the rows as the verifier receives them (unnormalised float32 values)
+    qq = np.tile(oracle.expand_sparse_q(idx, val, rest, V), (B, 1))
+    res = oracle.sample("stochastic", np.arange(B), np.full(B, L), logits, drafts, qq, seed=12)
+    first = [e[0] for e in _emitted(res, drafts, L)]
+    ok, pv = _chi2_ok(np.bincount(first, minlength=V), p[0])
+    assert ok, pv

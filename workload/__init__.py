@@ -367,3 +367,49 @@ def custom_workload(model: str, prefix_len: List[int], draft_len: List[int], see
                     np.asarray(draft_len, np.int32), a, int(a.max()) + 1 if n else 1,
                     q_sigma=q_sigma, q_mix=q_mix, q_sigma_b=1.0, accept_u_input=accept_u_input,
                     kv=kv, seed=seed)
+
+
+S_SPARSE_U = 0x700A  # stream of the uniforms that redraw drafts from sparse rows
+
+
+@dataclasses.dataclass
+class SparseRows:
+    idx: np.ndarray    # int32 [nd][K]  listed tokens, distinct
+    val: np.ndarray    # fp32 [nd][K]   their probabilities
+    rest: np.ndarray   # fp32 [nd]      probability of every other token
+
+
+def sparsify(b: Batch, K: int, seed: int) -> SparseRows:
+    """Input construction for the sparse-payload variant: each dense draft
+    row of `b` becomes its K most likely tokens (ties to the lower id) with
+    their probabilities plus a uniform remainder (1 - sum) / (V - K), and the
+    drafts are redrawn from those sparse rows (inverse CDF on a seeded
+    uniform per draft, listed tokens first in increasing id, then the other
+    tokens in increasing id), so the drafts follow the distribution the
+    verification is given.  `b.drafts` is replaced in place."""
+    nd, V = b.q.shape
+    assert 1 <= K < V
+    idx = np.empty((nd, K), np.int32)
+    val = np.empty((nd, K), np.float32)
+    rest = np.empty(nd, np.float32)
+    u = np.empty(max(nd, 1), np.float32)
+    lib().wl_fill_uniform_f32(_ptr(u), int(max(nd, 1)), seed, S_SPARSE_U, 0, 0.0, 1.0)
+    for r in range(nd):
+        row = b.q[r].astype(np.float64)
+        top = np.lexsort((np.arange(V), -row))[:K]
+        top = np.sort(top)
+        idx[r] = top
+        val[r] = b.q[r, top]
+        listed = float(np.sum(val[r].astype(np.float64)))
+        rest[r] = np.float32(max(1.0 - listed, 0.0) / (V - K))
+        # inverse CDF over (listed tokens by id, then the others by id)
+        x = float(u[r])
+        cum = np.cumsum(val[r].astype(np.float64))
+        if x < cum[-1]:
+            d = int(top[np.searchsorted(cum, x, side="right")])
+        else:
+            j = min(int((x - cum[-1]) / max(float(rest[r]), 1e-300)), V - K - 1)
+            others = np.setdiff1d(np.arange(V), top, assume_unique=True)
+            d = int(others[j])
+        b.drafts[r] = d
+    return SparseRows(idx, val, rest)
