@@ -1,0 +1,126 @@
+"""Host runtime behind the C ABI on a live context: argument validation
+(every rejected call returns its code and changes nothing), the pending /
+accept state machine, device-detected bad tokens, and the page pool (no
+page is lost across committed rounds, trims and releases)."""
+import numpy as np
+import pytest
+import torch
+
+import workload as wl
+from gpu_harness import layer_ptrs, load_synthetic_kv
+from paper_2604_20919_amd import sdverify as sv
+from paper_2604_20919_amd.verifier import Verifier
+from workload.device import DeviceWeights, batch_to_device
+
+pytestmark = pytest.mark.gpu
+
+
+def _verifier(w, dw, n_pages, max_ctx=256, max_draft=4, max_batch_tokens=32):
+    return Verifier(w.model, layer_ptrs(dw), n_pages=n_pages, max_users=w.n_users,
+                    max_draft=max_draft, max_batch_users=w.n_users,
+                    max_batch_tokens=max_batch_tokens, max_ctx=max_ctx, max_pending=2)
+
+
+def _code(fn):
+    try:
+        fn()
+    except sv.SdError as e:
+        return e.status
+    return sv.SD_OK
+
+
+def test_validation_and_state_machine():
+    w = wl.custom_workload("tiny-bf16", [20, 33, 5], [2, 3, 1], seed=71)
+    dw = DeviceWeights(w.model, w.seed)
+    # room for 12 slots: the valid batch has 9, the oversized one 15 (rejected
+    # on the host before anything reads the 6-entry draft buffer)
+    v = _verifier(w, dw, n_pages=64, max_batch_tokens=12)
+    load_synthetic_kv(v, w)
+    b = w.batch(0)
+    d, q, au = batch_to_device(b)
+    states = [v.user_state(u) for u in range(3)]
+    L = np.array(w.draft_len)
+    bad_calls = {
+        "draft length 0": lambda: v.verify(0, w.assign, np.array([2, 0, 1]), d, q),
+        "draft length above max": lambda: v.verify(0, w.assign, np.array([2, 5, 1]), d, q),
+        "empty batch": lambda: v.verify(1, w.assign, L, d, q),
+        "negative batch": lambda: v.verify(-1, w.assign, L, d, q),
+        "no drafts pointer": lambda: v.verify(0, w.assign, L, None, q),
+        "no q in stochastic mode": lambda: v.verify(0, w.assign, L, d, None, "stochastic"),
+        "too many slots": lambda: v.verify(0, w.assign, np.array([4, 4, 4]), d, q),
+    }
+    for name, call in bad_calls.items():
+        assert _code(call) == sv.SD_EINVAL, name
+    assert [v.user_state(u) for u in range(3)] == states
+    # a user that was never started
+    w4 = wl.custom_workload("tiny-bf16", [20, 33, 5, 9], [2, 3, 1, 1], seed=71)
+    v4 = _verifier(w4, dw, n_pages=64, max_batch_tokens=12)
+    load_synthetic_kv(v4, w4, users=[0, 1, 2])
+    b4 = w4.batch(0)
+    d4, q4, _ = batch_to_device(b4)
+    assert _code(lambda: v4.verify(0, w4.assign, w4.draft_len, d4, q4)) == sv.SD_EINVAL
+    v4.close()
+    # greedy mode needs no q
+    v.verify(0, w.assign, L, d, None, "greedy")
+    # pending: a second verify of the slot, a reset of a pending user and an
+    # accept of another batch are refused
+    assert _code(lambda: v.verify(0, w.assign, L, d, q)) == sv.SD_ESTATE
+    assert _code(lambda: v.reset_user(1, 10, 0)) == sv.SD_ESTATE
+    assert _code(lambda: v.accept(2, 3)) == sv.SD_ESTATE
+    n1, t1 = v.accept(0, 3)
+    assert _code(lambda: v.accept(0, 3)) == sv.SD_ESTATE
+    assert [v.user_state(u) for u in range(3)] == states  # commit = 0
+    v.close()
+
+
+def test_bad_token_is_reported_by_the_device_and_not_committed():
+    w = wl.custom_workload("tiny-bf16", [20, 33], [2, 3], seed=72)
+    dw = DeviceWeights(w.model, w.seed)
+    v = _verifier(w, dw, n_pages=64)
+    load_synthetic_kv(v, w)
+    b = w.batch(0)
+    d, q, _ = batch_to_device(b)
+    d[1] = w.model.vocab + 5
+    before = [v.user_state(u) for u in range(2)]
+    v.verify(0, w.assign, w.draft_len, d, q)
+    assert _code(lambda: v.accept(0, 2, commit=True)) == sv.SD_EDEVICE
+    assert [v.user_state(u) for u in range(2)] == before
+    # the slot is free again and a good batch goes through
+    d[1] = 7
+    v.verify(0, w.assign, w.draft_len, d, q)
+    v.accept(0, 2, commit=True)
+    v.close()
+
+
+def test_page_pool_accounting():
+    """A pool sized to the last page: committed rounds grow the users, the
+    draft slots' extra pages are trimmed back at accept, and after the users
+    are released one new user can take every page again (nothing leaked)."""
+    prefix, L = [30, 47], [3, 4]
+    w = wl.custom_workload("tiny-bf16", prefix, L, seed=73)
+    dw = DeviceWeights(w.model, w.seed)
+    rounds = 5
+    final = [p + rounds * (l + 1) for p, l in zip(prefix, L)]
+    n_pages = sum((f + 15) // 16 for f in final)
+    v = _verifier(w, dw, n_pages=n_pages, max_ctx=n_pages * 16)
+    load_synthetic_kv(v, w)
+    b = w.batch(0)
+    d, q, _ = batch_to_device(b)
+    # force mode accepts every draft: i_m grows by l_m + 1 per round
+    for r in range(rounds):
+        v.verify(0, w.assign, w.draft_len, d, q, "force")
+        v.accept(0, 2, commit=True)
+    assert [v.user_state(u)[0] for u in range(2)] == final
+    # no page is left: one more token for user 0 beyond its last page fails
+    full0 = ((final[0] + 15) // 16) * 16
+    assert _code(lambda: v.reset_user(0, full0 + 1, 1)) == sv.SD_ENOMEM
+    assert v.user_state(0)[0] == final[0]
+    # a verify that would need a new page is refused with nothing reserved
+    if final[0] + L[0] + 1 > full0 or final[1] + L[1] + 1 > ((final[1] + 15) // 16) * 16:
+        assert _code(lambda: v.verify(0, w.assign, w.draft_len, d, q)) == sv.SD_ENOMEM
+    # release everything: a single user can now hold the whole pool
+    for u in range(2):
+        sv.sd_user_release(v.ctx, u)
+    v.reset_user(0, n_pages * 16 - 2, 3)
+    assert _code(lambda: v.reset_user(1, 1, 3)) == sv.SD_ENOMEM
+    v.close()
