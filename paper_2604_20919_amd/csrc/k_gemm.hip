@@ -701,7 +701,9 @@ __global__ void k_gemm_f32(GemmF p) {
 //     computes 96 slots (gate/up 113 vs 119 us in the full step);
 //   * above, the 32x32 form wins by its MFMA rate: gate/up at T = 128 / 176
 //     / 240 takes 141 / 188 / 390 us against 181 / 237 / 509 us;
-//   * above 224 slots tiles need the register budget of one wave per SIMD
+//   * 225..256 slots: eight waves with 32-k chunks (gate/up at T = 240
+//     292 us against 392 us for four waves with 64-k chunks);
+//   * above 256 slots tiles need the register budget of one wave per SIMD
 //     (four waves) and shorter chunks so that a double-buffered two-plane
 //     chunk fits in LDS.
 struct GemmShape { int F, MT, NSUB, KC, NW, PD, PK; };
@@ -723,7 +725,11 @@ static GemmShape shape_for(int T, int vcols, bool raw) {
     const int mt = (T + 31) / 32;
     if (mt <= 4) return wide ? GemmShape{32, mt, 1, 64, 8, 2, 0} : GemmShape{32, mt, 1, 64, 4, 2, 0};
     if (mt <= 7) return wide ? GemmShape{32, mt, 1, 64, 8, 1, 0} : GemmShape{32, mt, 1, 64, 4, 1, 0};
-    if (mt <= 8) return {32, 8, 1, 64, 4, 1, 0};
+    // 225..256 slots: eight waves with 32-k chunks (double-buffered staging
+    // of 2 x 256 rows then fits one workgroup of 256 weight rows per CU);
+    // same-box probe at T = 240: gate/up 292 vs 392 us, QKV 63 vs 99, O 51
+    // vs 93, down 143 vs 210 us against four waves with 64-k chunks
+    if (mt <= 8) return wide ? GemmShape{32, 8, 1, 32, 8, 1, 0} : GemmShape{32, 8, 1, 64, 4, 1, 0};
     if (mt <= 10) return {32, 10, 1, 32, 4, 1, 0};
     if (mt <= 13) return {32, 13, 1, 16, 4, 1, 0};
     return {0, 0, 0, 0, 0, 0, 0};
@@ -782,7 +788,8 @@ static GemmFn pick(const GemmShape& sh, int epi) {
         if (sh.MT == 7) return pick_epi<32, 7, 8, 64, 1, SPLIT, true>(epi);
         return nullptr;
     }
-    if (sh.F == 32 && sh.MT == 8) return pick_epi<32, 8, 4, 64, 1, SPLIT>(epi);
+    if (sh.F == 32 && sh.MT == 8)
+        return sh.NW == 8 ? pick_epi<32, 8, 8, 32, 1, SPLIT>(epi) : pick_epi<32, 8, 4, 64, 1, SPLIT>(epi);
     if (sh.F == 32 && sh.MT == 10) return pick_epi<32, 10, 4, 32, 1, SPLIT>(epi);
     if (sh.F == 32 && sh.MT == 13) return pick_epi<32, 13, 4, 16, 1, SPLIT>(epi);
     return sh.NW == 8 ? pick_nw<8, SPLIT>(sh, epi) : pick_nw<4, SPLIT>(sh, epi);
