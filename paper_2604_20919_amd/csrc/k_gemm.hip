@@ -706,11 +706,15 @@ __global__ void k_gemm_f32(GemmF p) {
 //   * above 256 slots tiles need the register budget of one wave per SIMD
 //     (four waves) and shorter chunks so that a double-buffered two-plane
 //     chunk fits in LDS.
-struct GemmShape { int F, MT, NSUB, KC, NW, PD, PK; };
+// FILL: choose the k splits to fill one wave of workgroups (the eight-wave
+// rule of choose_splits) even for four-wave tiles.
+struct GemmShape { int F, MT, NSUB, KC, NW, PD, PK, FILL = 0; };
 
 constexpr int kT32 = 97;  // first slot count served by the 32x32 form
 
-static GemmShape shape_for(int T, int vcols, bool raw) {
+static int cu_count();
+
+static GemmShape shape_for(int T, int vcols, bool raw, int K) {
     const bool wide = vcols % 256 == 0;
     // packed planes (2a + 1 tiles for 32a < T <= 32a + 16): split-K
     // partial GEMMs at 65..80 slots (QKV / O / down at T = 80: 29.5 / 23.7
@@ -720,6 +724,16 @@ static GemmShape shape_for(int T, int vcols, bool raw) {
     if (wide && T > 96 && T <= 112) return {32, 7, 1, 64, 8, 1, 1};
     if (T < kT32) {
         const int mt = std::max(2, (T + 15) / 16);
+        // split-K partial GEMMs with few weight rows (the Qwen3-1.7B shapes):
+        // when eight-wave tiles with at least two 128-k chunks per split
+        // cannot fill 90% of the CUs, four-wave tiles with 64-k chunks give
+        // twice the workgroups (QKV / O / down at T = 60: 7.9 / 6.5 / 9.4 us
+        // against 10.2 / 8.9 / 11.6 us)
+        if (raw && wide) {
+            const int tiles8 = vcols / 256;
+            const int s8 = std::min(std::max(1, K / 128 / 2), std::max(1, cu_count() / tiles8));
+            if (10 * tiles8 * s8 < 9 * cu_count()) return GemmShape{16, mt, 2, 64, 4, 2, 0, 1};
+        }
         return wide ? GemmShape{16, mt, 2, 128, 8, 1, 0} : GemmShape{16, mt, 2, 64, 4, 2, 0};
     }
     const int mt = (T + 31) / 32;
@@ -803,7 +817,7 @@ static ReduceFn pick_reduce(int epi) {
     }
 }
 
-static int cu_count() {
+static int cu_count() {  // cached
     static int n = 0;
     if (n == 0) {
         int dev = 0;
@@ -855,7 +869,7 @@ int gemm_counter_count(const Dims&) { return 1; }
 bool gemm_shape_ok(const Dims& D, int T, int K, int N, int epi) {
     if (!D.bf16) return true;
     const int vcols = epi == EPI_SWIGLU ? 2 * N : N;
-    const GemmShape sh = shape_for(T, vcols, false);
+    const GemmShape sh = shape_for(T, vcols, false, K);
     if (sh.MT == 0) return false;
     return K % sh.KC == 0 && K % 32 == 0 && vcols % (sh.F * sh.NW * sh.NSUB) == 0;
 }
@@ -880,7 +894,7 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
         return 1;
     }
     const int vcols = g.epi == EPI_SWIGLU ? 2 * g.N : g.N;
-    const GemmShape sh = shape_for(g.T, vcols, g.raw != 0);
+    const GemmShape sh = shape_for(g.T, vcols, g.raw != 0, g.K);
     const int nt = sh.F * sh.NW * sh.NSUB;
     GemmP p;
     p.X = (const bf16_t*)g.X;
@@ -891,7 +905,7 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
     p.kchunks = g.K / sh.KC;
     p.vcols = vcols;
     p.tiles = p.vcols / nt;
-    int S = choose_splits(p.tiles, p.kchunks, sh.NW);
+    int S = choose_splits(p.tiles, p.kchunks, sh.FILL ? 8 : sh.NW);
     while (S > 1 && (size_t)S * g.T * p.vcols > sb.gpart_floats) {
         int t = S - 1;
         while (t > 1 && p.kchunks % t) --t;
