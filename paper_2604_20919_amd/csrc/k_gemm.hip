@@ -897,7 +897,6 @@ size_t gemm_partial_floats(const Dims& D, int Tmax) {
     return (size_t)Tmax * std::max<size_t>(widest * 2, (size_t)65536);
 }
 
-int gemm_counter_count(const Dims&) { return 1; }
 
 bool gemm_shape_ok(const Dims& D, int T, int K, int N, int epi) {
     if (!D.bf16) return true;

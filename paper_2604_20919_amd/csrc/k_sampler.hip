@@ -28,8 +28,6 @@ struct SampP {
     float* sstat;         // [T][4]
     float* spartA;        // [T][kVocabChunks][4]
     float* spartB;        // [B][kVocabChunks][4]
-    int32_t* cntA;        // [T]
-    int32_t* cntB;        // [B]
     int32_t* result;      // n_acc [Bmax], token [Bmax], flags
     int bmax;
 };
@@ -324,8 +322,6 @@ void launch_sampler(const Dims& D, const BatchView& bv, const SlotBufs& sb, cons
     p.sstat = sb.sstat;
     p.spartA = sb.spart;
     p.spartB = sb.spartB;
-    p.cntA = sb.scount;
-    p.cntB = sb.scountB;
     p.result = sb.result;
     p.bmax = sb.bmax;
     const int chunks = (D.V + p.cw - 1) / p.cw;

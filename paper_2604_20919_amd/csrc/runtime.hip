@@ -38,10 +38,10 @@ struct Layout {
     size_t st_user, st_prefix, st_L, st_root, st_soff, st_doff, st_sb, st_sj, st_pt, st_items,
         st_ioff, st_flags, st_prow, st_bytes;
     // slot buffers (byte offsets within the slot)
-    size_t stage, tok, cs, x, ssq, h, ffn, qbuf, attn, apart, aml, gpart, gcount, logits, sstat, spart,
-        spartB, scount, scountB, result, slot_bytes;
+    size_t stage, tok, cs, x, ssq, h, ffn, qbuf, attn, apart, aml, gpart, logits, sstat, spart,
+        spartB, result, slot_bytes;
     size_t gpart_floats;
-    int gcount_n, nsq;
+    int nsq;
     // global region after the slots
     size_t kvw_pages, total;
     int max_pages, max_items, rows_max, Tmax, Bmax;
@@ -142,14 +142,10 @@ Layout plan(const sd_config& c) {
     L.aml = take(nparts * 2 * 4);
     L.gpart_floats = gemm_partial_floats(D, L.Tmax);
     L.gpart = take(std::max<size_t>(L.gpart_floats, 1) * 4);
-    L.gcount_n = gemm_counter_count(D);
-    L.gcount = take((size_t)L.gcount_n * 4);
     L.logits = take((size_t)L.Tmax * D.V * 4);
     L.sstat = take((size_t)L.Tmax * 4 * 4);
     L.spart = take((size_t)L.Tmax * kVocabChunks * 4 * 4);
     L.spartB = take((size_t)L.Bmax * kVocabChunks * 4 * 4);
-    L.scount = take((size_t)L.Tmax * 4);
-    L.scountB = take((size_t)L.Bmax * 4);
     L.result = take((size_t)(2 * L.Bmax + 4) * 4);
     L.slot_bytes = s;
     L.kvw_pages = L.slot_bytes * (size_t)c.max_pending;
@@ -627,22 +623,12 @@ sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_poo
         b.aml = (float*)(s.base + L.aml);
         b.gpart = (float*)(s.base + L.gpart);
         b.gpart_floats = L.gpart_floats;
-        b.gcount = (int32_t*)(s.base + L.gcount);
-        b.gcount_n = L.gcount_n;
         b.logits = (float*)(s.base + L.logits);
         b.sstat = (float*)(s.base + L.sstat);
         b.spart = (float*)(s.base + L.spart);
         b.spartB = (float*)(s.base + L.spartB);
-        b.scount = (int32_t*)(s.base + L.scount);
-        b.scountB = (int32_t*)(s.base + L.scountB);
         b.result = (int32_t*)(s.base + L.result);
         b.bmax = L.Bmax;
-        if (ok) {
-            // arrival counters start at zero and are reset by their last user
-            ok &= hipMemset(b.gcount, 0, (size_t)L.gcount_n * 4) == hipSuccess;
-            ok &= hipMemset(b.scount, 0, (size_t)L.Tmax * 4) == hipSuccess;
-            ok &= hipMemset(b.scountB, 0, (size_t)L.Bmax * 4) == hipSuccess;
-        }
     }
     ok = ok && hipHostMalloc((void**)&c->kvw_host, (size_t)L.max_pages * 4, hipHostMallocDefault) ==
                    hipSuccess;

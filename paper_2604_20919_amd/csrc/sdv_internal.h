@@ -9,7 +9,7 @@ namespace sdv {
 constexpr int kPageTokens = 16;   // tokens per KV page
 constexpr int kAttnItemsMax = 1024;  // attention work items per batch (beyond one per (user, KV head))
 constexpr int kAttnWGsPerCU = 2;     // co-resident attention workgroups per CU (register bound)
-constexpr int kAttnBuffers = 3;      // LDS ring of the attention kernel (buffers - 1 blocks in flight)
+constexpr int kAttnBuffers = 2;      // LDS ring of the attention kernel (buffers - 1 blocks in flight)
 constexpr int kVocabChunks = 64;  // vocab split of the sampler kernels (at most 64: one wave merges)
 constexpr int kNormBlock = 1024;   // columns per sum-of-squares block of x
 constexpr int kNormKMax = 8192;    // widest model dimension the GEMM can normalise on load
@@ -95,14 +95,10 @@ struct SlotBufs {
     float* aml;       // [max_items][rows_max][2]
     float* gpart;     // GEMM split-K partials
     size_t gpart_floats;
-    int32_t* gcount;  // GEMM tile counters
-    int gcount_n;
     float* logits;    // [Tmax][V]
     float* sstat;     // [Tmax][4] per-slot max, sum, argmax, accept
     float* spart;     // [Tmax * kVocabChunks][4] phase-A vocab-chunk partials
     float* spartB;    // [Bmax * kVocabChunks][4] phase-B partials
-    int32_t* scount;  // [Tmax] phase-A arrival counters
-    int32_t* scountB; // [Bmax] phase-B arrival counters
     int32_t* result;  // [2*Bmax + 4]: n_acc, token, flags
     int bmax;
 };
@@ -154,7 +150,6 @@ void launch_qkv_finish(const Dims& D, const BatchView& bv, const SlotBufs& sb, c
 size_t gemm_partial_floats(const Dims& D, int Tmax);
 void launch_pack(const void* s0, const void* s1, const void* s2, int seg1, int seg2, int mode,
                  int K, int vrows, void* dst, hipStream_t s);
-int gemm_counter_count(const Dims& D);
 
 void launch_sampler(const Dims& D, const BatchView& bv, const SlotBufs& sb, const float* logits,
                     hipStream_t s);
