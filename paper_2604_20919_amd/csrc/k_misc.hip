@@ -132,6 +132,20 @@ void launch_resid_norm(const Dims& D, int T, const float* part, int S, float* x,
         resid_norm_dispatch<float>(T, part, S, x, (const float*)gamma, (float*)h, D.d, D.eps, s);
 }
 
+// four values as bf16 (8 bytes); the activation planes hi = bf16(v),
+// lo = bf16(v - hi) of four consecutive columns
+__device__ __forceinline__ uint2 pack_bf16x4(const float (&v)[4]) {
+    return uint2{(uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16),
+                 (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16)};
+}
+__device__ __forceinline__ void st_act4(bf16_t* p, size_t plane, size_t i, const float (&v)[4]) {
+    float lo[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) lo[e] = v[e] - bf16_to_f32(f32_to_bf16(v[e]));
+    *(uint2*)(p + i) = pack_bf16x4(v);
+    *(uint2*)(p + plane + i) = pack_bf16x4(lo);
+}
+
 // ---------------------------------------------------------------------------
 // bf16 configuration: split-K reduction fused with the residual add and the
 // elementwise half of the next RMSNorm.  x[t] += sum_s part[s][t] (split
@@ -154,14 +168,16 @@ __global__ __launch_bounds__(256) void k_resid_reduce(const float* part, int S, 
     const float4* pr = (const float4*)(part + (size_t)t * d);
     const float4 xv = act ? xr[k] : float4{0.f, 0.f, 0.f, 0.f};
     const uint2 gq = act ? *(const uint2*)(gamma + 4 * k) : uint2{0u, 0u};
+    // partial planes added in split order, sixteen planes' loads in flight
+    // (one memory round trip for the split counts the GEMMs choose)
     float4 v = float4{0.f, 0.f, 0.f, 0.f};
-    for (int sp = 0; sp < S; sp += 8) {
-        float4 b[8];
+    for (int sp = 0; sp < S; sp += 16) {
+        float4 b[16];
 #pragma unroll
-        for (int q = 0; q < 8; ++q)
+        for (int q = 0; q < 16; ++q)
             b[q] = act && sp + q < S ? pr[(sp + q) * plane4 + k] : float4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
+        for (int q = 0; q < 16; ++q) {
             v.x += b[q].x; v.y += b[q].y; v.z += b[q].z; v.w += b[q].w;
         }
     }
@@ -170,10 +186,9 @@ __global__ __launch_bounds__(256) void k_resid_reduce(const float* part, int S, 
     if (act) {
         xr[k] = r;
         const size_t o = (size_t)t * d + 4 * k, pl = (size_t)T * d;
-        st_act(h, pl, o + 0, r.x * bf16_to_f32((bf16_t)(gq.x & 0xffffu)));
-        st_act(h, pl, o + 1, r.y * bf16_to_f32((bf16_t)(gq.x >> 16)));
-        st_act(h, pl, o + 2, r.z * bf16_to_f32((bf16_t)(gq.y & 0xffffu)));
-        st_act(h, pl, o + 3, r.w * bf16_to_f32((bf16_t)(gq.y >> 16)));
+        const float hv[4] = {r.x * bf16_to_f32((bf16_t)(gq.x & 0xffffu)), r.y * bf16_to_f32((bf16_t)(gq.x >> 16)),
+                             r.z * bf16_to_f32((bf16_t)(gq.y & 0xffffu)), r.w * bf16_to_f32((bf16_t)(gq.y >> 16))};
+        st_act4(h, pl, o, hv);
     }
     float ss = act ? r.x * r.x + r.y * r.y + r.z * r.z + r.w * r.w : 0.f;
     ss = wave_sum(ss);
@@ -277,9 +292,9 @@ void launch_embed_norm(const Dims& D, const BatchView& bv, const void* embed, co
 }
 
 // ---------------------------------------------------------------------------
-// QK-norm + rotate-half RoPE + KV append.  One wave per (slot, head) where
-// heads 0..hq-1 are query heads and hq..hq+hkv-1 are KV heads.  Lane a < hd/2
-// owns the rotation pair (a, a + hd/2).  Query heads go to qbuf; key heads
+// QK-norm + rotate-half RoPE + KV append (fp32 configuration).  One wave
+// per (slot, head) where heads 0..hq-1 are query heads and hq..hq+hkv-1 are
+// KV heads.  Lane a < hd/2 owns the rotation pair (a, a + hd/2).  Query heads go to qbuf; key heads
 // go (normed, rotated) into the K block of the slot's page and the matching
 // value row (unrotated) into the V^T block.
 // ---------------------------------------------------------------------------
@@ -376,19 +391,133 @@ __global__ __launch_bounds__(256) void k_qkrope(BatchView bv, const float* qkv, 
     st(vd, (size_t)(lane + half) * kPageTokens + off, v1);
 }
 
+// bf16 configuration (head_dim 128): the same steps with 16 lanes per head
+// and four heads of one slot per wave.  Lane l of a head owns dims 4l..4l+3
+// and their rotation partners 64+4l..64+4l+3, so every partial-plane read is
+// a 16-byte load (a wave reads 1 KB per instruction instead of 256 B) and
+// the query and key rows leave as 8-byte stores.  One wave per workgroup,
+// so that few waves (small batches) still spread over the CUs.
+__global__ __launch_bounds__(64) void k_qkrope_bf16(BatchView bv, const float* qkv, int S,
+                                                     const float* cs, bf16_t* qbuf, KVPool kv,
+                                                     int layer, const bf16_t* qn, const bf16_t* kn,
+                                                     int hq, int hkv, int qk_norm, float eps,
+                                                     const float* nss, int nnb, int d) {
+    constexpr int HD = 128, HALF = 64;
+    const int wave = blockIdx.x;
+    const int lane = threadIdx.x, l = lane & 15;
+    const int nh = hq + hkv, ng = (nh + 3) >> 2;  // head groups of four per slot
+    const int t = wave / ng;
+    if (t >= bv.T) return;
+    const int h = (wave % ng) * 4 + (lane >> 4);
+    const bool act = h < nh;
+    const bool is_q = h < hq;
+    const int nqkv = (hq + 2 * hkv) * HD;
+    const size_t plane = (size_t)bv.T * nqkv;
+    const int col = (is_q ? h * HD : hq * HD + (h - hq) * HD) + 4 * l;
+    const float* src = qkv + (size_t)t * nqkv + col;
+    const float* vs = qkv + (size_t)t * nqkv + (size_t)(hq + hkv) * HD + (size_t)(is_q ? 0 : h - hq) * HD + 4 * l;
+    float ssb[kNormKMax / kNormBlock];
+#pragma unroll
+    for (int b = 0; b < kNormKMax / kNormBlock; ++b)
+        ssb[b] = nss != nullptr && b < nnb ? nss[(size_t)t * nnb + b] : 0.f;
+    // partial planes added in split order, eight planes' loads in flight
+    f32x4 xa = f32x4{0.f, 0.f, 0.f, 0.f}, xb = xa, va = xa, vb = xa;
+    for (int sp = 0; sp < S; sp += 8) {
+        f32x4 a0[8], a1[8], b0[8], b1[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const bool ok = act && sp + u < S;
+            const size_t o = (size_t)(sp + u) * plane;
+            const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
+            a0[u] = ok ? *(const f32x4*)(src + o) : z;
+            a1[u] = ok ? *(const f32x4*)(src + o + HALF) : z;
+            b0[u] = ok && !is_q ? *(const f32x4*)(vs + o) : z;
+            b1[u] = ok && !is_q ? *(const f32x4*)(vs + o + HALF) : z;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            xa += a0[u];
+            xb += a1[u];
+            va += b0[u];
+            vb += b1[u];
+        }
+    }
+    float rt = 1.0f;
+    if (nss != nullptr) {
+        float ssx = 0.f;
+#pragma unroll
+        for (int b = 0; b < kNormKMax / kNormBlock; ++b) ssx += ssb[b];
+        rt = 1.0f / sqrtf(ssx / (float)d + eps);
+        xa *= rt;
+        xb *= rt;
+    }
+    if (qk_norm) {
+        float ss = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ss += xa[e] * xa[e] + xb[e] * xb[e];
+#pragma unroll
+        for (int o = 8; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 16);
+        const float r = 1.0f / sqrtf(ss / (float)HD + eps);
+        const bf16_t* g = is_q ? qn : kn;
+        if (act) {
+            const uint2 ga = *(const uint2*)(g + 4 * l), gb = *(const uint2*)(g + HALF + 4 * l);
+            const uint32_t gw[4] = {ga.x, ga.y, gb.x, gb.y};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t wa = gw[e >> 1], wb = gw[2 + (e >> 1)];
+                xa[e] = xa[e] * r * bf16_to_f32((bf16_t)((e & 1) ? wa >> 16 : wa & 0xffffu));
+                xb[e] = xb[e] * r * bf16_to_f32((bf16_t)((e & 1) ? wb >> 16 : wb & 0xffffu));
+            }
+        }
+    }
+    if (!act) return;
+    const f32x4 c0 = *(const f32x4*)(cs + ((size_t)t * HALF + 4 * l) * 2);
+    const f32x4 c1 = *(const f32x4*)(cs + ((size_t)t * HALF + 4 * l) * 2 + 4);
+    const float cv[4] = {c0[0], c0[2], c1[0], c1[2]}, sv[4] = {c0[1], c0[3], c1[1], c1[3]};
+    float ya[4], yb[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        ya[e] = xa[e] * cv[e] - xb[e] * sv[e];
+        yb[e] = xb[e] * cv[e] + xa[e] * sv[e];
+    }
+    if (is_q) {
+        const size_t q0 = ((size_t)t * hq + h) * HD + 4 * l, pl = (size_t)bv.T * hq * HD;
+        st_act4(qbuf, pl, q0, ya);
+        st_act4(qbuf, pl, q0 + HALF, yb);
+        return;
+    }
+    const int g = h - hq;
+    const int b = bv.slot_b[t];
+    const int pos = bv.prefix[b] + bv.slot_j[t];
+    const int page = bv.page_table[(size_t)b * bv.max_pages + pos / kPageTokens];
+    const int off = pos % kPageTokens;
+    bf16_t* base = (bf16_t*)kv.base;
+    bf16_t* kd = base + kv.k_off(layer, page, g) + (size_t)off * HD + 4 * l;
+    *(uint2*)kd = pack_bf16x4(ya);
+    *(uint2*)(kd + HALF) = pack_bf16x4(yb);
+    bf16_t* vd = base + kv.v_off(layer, page, g);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        vd[(size_t)(4 * l + e) * kPageTokens + off] = f32_to_bf16(va[e] * rt);
+        vd[(size_t)(HALF + 4 * l + e) * kPageTokens + off] = f32_to_bf16(vb[e] * rt);
+    }
+}
+
 void launch_qkv_finish(const Dims& D, const BatchView& bv, const SlotBufs& sb, const KVPool& kv,
                        int layer, const float* part, int S, const void* qn, const void* kn,
                        hipStream_t s) {
-    const int waves = bv.T * (D.hq + D.hkv);
-    const int blocks = (waves + 3) / 4;
-    if (D.bf16)
-        hipLaunchKernelGGL(k_qkrope<bf16_t>, dim3(blocks), dim3(256), 0, s, bv, part, S, sb.cs,
+    if (D.bf16) {
+        // head_dim 128 (checked at init): four heads per wave
+        const int waves = bv.T * ((D.hq + D.hkv + 3) / 4);
+        hipLaunchKernelGGL(k_qkrope_bf16, dim3(waves), dim3(64), 0, s, bv, part, S, sb.cs,
                            (bf16_t*)sb.qbuf, kv, layer, (const bf16_t*)qn, (const bf16_t*)kn, D.hq,
-                           D.hkv, D.hd, D.qk_norm, D.eps, sb.ssq, sb.nsq, D.d);
-    else
-        hipLaunchKernelGGL(k_qkrope<float>, dim3(blocks), dim3(256), 0, s, bv, part, S, sb.cs,
-                           (float*)sb.qbuf, kv, layer, (const float*)qn, (const float*)kn, D.hq,
-                           D.hkv, D.hd, D.qk_norm, D.eps, (const float*)nullptr, 0, D.d);
+                           D.hkv, D.qk_norm, D.eps, sb.ssq, sb.nsq, D.d);
+        return;
+    }
+    const int waves = bv.T * (D.hq + D.hkv);
+    hipLaunchKernelGGL(k_qkrope<float>, dim3((waves + 3) / 4), dim3(256), 0, s, bv, part, S, sb.cs,
+                       (float*)sb.qbuf, kv, layer, (const float*)qn, (const float*)kn, D.hq, D.hkv,
+                       D.hd, D.qk_norm, D.eps, (const float*)nullptr, 0, D.d);
 }
 
 // ---------------------------------------------------------------------------
