@@ -197,6 +197,22 @@ def main():
                 "mfma_tflops": round(2.0 * T * 2 * m.d_ffn * m.d_model / gu_avg_s / 1e12, 1),
                 "mfma_frac_bf16": round(2.0 * T * 2 * m.d_ffn * m.d_model / gu_avg_s / 1e12 / BF16_PEAK_TFLOPS, 4)}
 
+    # achievable peaks of this GPU (library calibration kernels): a read-only
+    # stream and a copy of 1 GiB (4x the last-level cache), and a bf16 MFMA
+    # loop with no memory traffic
+    cal_buf = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    cal_sink = torch.empty(4, dtype=torch.float32, device="cuda")
+    cs0 = streams[0].cuda_stream
+    achievable = {"hbm_read_gbs": round(sv.sd_calib_hbm(cal_buf.data_ptr(), cal_buf.numel(), 1, 10, cs0), 1),
+                  "hbm_copy_gbs": round(sv.sd_calib_hbm(cal_buf.data_ptr(), cal_buf.numel(), 0, 10, cs0), 1),
+                  "mfma_bf16_tflops": round(sv.sd_calib_mfma(cal_sink.data_ptr(), 2048, cs0), 1),
+                  "note": "sd_calib_hbm (1 GiB read-only stream; copy = bytes read + written) and "
+                          "sd_calib_mfma (32x32x16 bf16 MFMA chains on every SIMD)"}
+    del cal_buf, cal_sink
+    hbm_ach = achievable["hbm_read_gbs"]
+    roofline["frac_of_achievable"] = round(achieved / hbm_ach, 4)
+    roofline["mfma_frac_of_achievable"] = round(roofline["mfma_tflops"] / achievable["mfma_bf16_tflops"], 4)
+
     def class_ms(k, steps=3):
         """Per-step device time of one kernel class (event pair per scope,
         the empty pair's cost subtracted)."""
@@ -220,9 +236,11 @@ def main():
         "attention": {"achieved": round(kv_read_step / (attn_ms / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
                       "unit": "GB/s", "frac": round(kv_read_step / (attn_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
                       "bytes_per_step": kv_read_step, "ms_per_step": round(attn_ms, 4),
+                      "frac_of_achievable": round(kv_read_step / (attn_ms / 1e3) / 1e9 / hbm_ach, 4),
                       "note": "paged attention + chunk combine, all layers; bytes = cached and new K/V read once"},
         "sampler": {"achieved": round(samp_bytes / (samp_ms / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(samp_bytes / (samp_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                    "frac_of_achievable": round(samp_bytes / (samp_ms / 1e3) / 1e9 / hbm_ach, 4),
                     "bytes_per_step": samp_bytes, "ms_per_step": round(samp_ms, 4),
                     "note": ("accept/reject + resample kernels; bytes = T x V fp32 logits + "
                              + ("the sparse rows" if sparse is not None else "one q row per user"))},
@@ -270,6 +288,7 @@ def main():
         "step_effective_gbs": round(step_bytes / (ms_step / 1e3) / 1e9, 1),
         "roofline": roofline,
         "kernels": kernels,
+        "achievable": achievable,
     }
     if breakdown is not None:
         result["breakdown_ms"] = breakdown

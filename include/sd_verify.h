@@ -339,6 +339,32 @@ sd_status sd_profile_begin(sd_ctx* ctx, int32_t kclass, int32_t max_launches);
  * milliseconds and their count; stops profiling.  SD_ESTATE if not active. */
 sd_status sd_profile_end(sd_ctx* ctx, double* total_ms, int32_t* launches);
 
+/*
+ * Achievable peaks of this GPU, for quoting kernel rates against what the
+ * chip delivers as well as against its published peaks.  Measurement
+ * helpers only: no context is needed and nothing of the verification state
+ * is touched.  Both calls are synchronous (they wait for their own events on
+ * `stream`) and allocate no device memory.
+ *
+ * sd_calib_hbm: HBM bandwidth over the caller's device buffer `buf` (16-byte
+ * aligned, `bytes` >= 1 MiB and a multiple of 32; its contents are
+ * overwritten).  mode 0: device-to-device copy of the first half onto the
+ * second; mode 1: read-only stream of the whole buffer.  One warm-up, then
+ * `reps` (>= 1) timed launches; *gbs = bytes read plus bytes written per
+ * second / 1e9.
+ *
+ * sd_calib_mfma: dense bf16 matrix-core rate: every SIMD runs independent
+ * chains of v_mfma_f32_32x32x16_bf16 (2*32*32*16 FLOPs each) for `iters`
+ * (>= 1) rounds with no memory traffic; *tflops = FLOPs per second / 1e12.
+ * `sink` is a device float the kernel may write.
+ *
+ * Errors: SD_EINVAL (bad arguments), SD_ENODEV (current device is not
+ * gfx950), SD_EHIP.
+ */
+sd_status sd_calib_hbm(void* buf, size_t bytes, int32_t mode, int32_t reps, double* gbs,
+                       sd_stream stream);
+sd_status sd_calib_mfma(float* sink, int32_t iters, double* tflops, sd_stream stream);
+
 /* Static description of a status code. */
 const char* sd_status_str(sd_status s);
 

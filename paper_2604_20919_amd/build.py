@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libsdverify.so")
 BUILD = os.path.join(HERE, "_build")
-SOURCES = ["runtime.hip", "k_misc.hip", "k_gemm.hip", "k_attn.hip", "k_sampler.hip"]
+SOURCES = ["runtime.hip", "k_misc.hip", "k_gemm.hip", "k_attn.hip", "k_sampler.hip", "calib.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          # compiler-generated packed fp32 ops are kept out of every kernel
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

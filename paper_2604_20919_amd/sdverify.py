@@ -25,7 +25,7 @@ MODES = {"greedy": SD_GREEDY, "stochastic": SD_STOCHASTIC, "force": SD_FORCE}
 EXPORTS = ("sd_verify_query_sizes", "sd_verify_init", "sd_verify_destroy", "sd_user_reset",
            "sd_user_release", "sd_user_state", "sd_kv_write", "sd_kv_read", "sd_verify_batch",
            "sd_verify_batch_graph", "sd_verify_batch_sparse", "sd_draft_batch", "sd_accept", "sd_sample_logits", "sd_debug_logits", "sd_profile_begin", "sd_profile_end",
-           "sd_status_str")
+           "sd_calib_hbm", "sd_calib_mfma", "sd_status_str")
 SD_K_QKV, SD_K_ATTN, SD_K_O, SD_K_GATEUP, SD_K_DOWN, SD_K_LMHEAD, SD_K_SAMPLER, SD_K_SMALL = range(1, 9)
 
 
@@ -84,6 +84,8 @@ def lib() -> ctypes.CDLL:
         L.sd_debug_logits.argtypes = [vp, i32, vp, vp]
         L.sd_profile_begin.argtypes = [vp, i32, i32]
         L.sd_profile_end.argtypes = [vp, P(ctypes.c_double), P(i32)]
+        L.sd_calib_hbm.argtypes = [vp, ctypes.c_size_t, i32, i32, P(ctypes.c_double), vp]
+        L.sd_calib_mfma.argtypes = [vp, i32, P(ctypes.c_double), vp]
         for name in EXPORTS:
             if name != "sd_status_str":
                 getattr(L, name).restype = i32
@@ -242,6 +244,21 @@ def sd_profile_end(ctx: int):
     ms, n = ctypes.c_double(), ctypes.c_int32()
     _check("sd_profile_end", lib().sd_profile_end(ctx, ctypes.byref(ms), ctypes.byref(n)))
     return ms.value, n.value
+
+
+def sd_calib_hbm(buf_ptr: int, nbytes: int, mode: int, reps: int, stream: int = 0) -> float:
+    """Achieved GB/s (bytes read + written) of a copy (mode 0) or read-only
+    stream (mode 1) over the caller's device buffer."""
+    gbs = ctypes.c_double()
+    _check("sd_calib_hbm", lib().sd_calib_hbm(buf_ptr, nbytes, mode, reps, ctypes.byref(gbs), stream))
+    return gbs.value
+
+
+def sd_calib_mfma(sink_ptr: int, iters: int, stream: int = 0) -> float:
+    """Achieved dense bf16 MFMA TFLOP/s of a register-only MFMA loop."""
+    tf = ctypes.c_double()
+    _check("sd_calib_mfma", lib().sd_calib_mfma(sink_ptr, iters, ctypes.byref(tf), stream))
+    return tf.value
 
 
 def make_config(n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, vocab, qk_norm, dtype,

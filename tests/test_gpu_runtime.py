@@ -124,3 +124,29 @@ def test_page_pool_accounting():
     v.reset_user(0, n_pages * 16 - 2, 3)
     assert _code(lambda: v.reset_user(1, 1, 3)) == sv.SD_ENOMEM
     v.close()
+
+
+def test_calibration_peaks():
+    """The achievable-peak helpers reject bad arguments and measure rates in
+    a plausible range for one MI355X (HBM3E at 8 TB/s, 2.5 PFLOP/s bf16)."""
+    buf = torch.empty(1 << 26, dtype=torch.uint8, device="cuda")
+    sink = torch.empty(4, dtype=torch.float32, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    for args in ((buf.data_ptr(), 1000, 1, 1), (buf.data_ptr(), buf.numel(), 2, 1),
+                 (buf.data_ptr(), buf.numel(), 1, 0), (buf.data_ptr() + 8, buf.numel() - 32, 1, 1)):
+        with pytest.raises(sv.SdError) as ei:
+            sv.sd_calib_hbm(*args, stream=s)
+        assert ei.value.status == sv.SD_EINVAL
+    with pytest.raises(sv.SdError) as ei:
+        sv.sd_calib_mfma(sink.data_ptr(), 0, s)
+    assert ei.value.status == sv.SD_EINVAL
+    # copy leaves the first half unchanged and duplicates it into the second
+    buf.view(torch.int32)[: buf.numel() // 8].copy_(torch.arange(buf.numel() // 8, dtype=torch.int32))
+    copy = sv.sd_calib_hbm(buf.data_ptr(), buf.numel(), 0, 2, s)
+    torch.cuda.synchronize()
+    half = buf.view(torch.int32).view(2, -1)
+    assert torch.equal(half[0], half[1])
+    read = sv.sd_calib_hbm(buf.data_ptr(), buf.numel(), 1, 4, s)
+    mfma = sv.sd_calib_mfma(sink.data_ptr(), 256, s)
+    assert 200.0 < copy < 20000.0 and 200.0 < read < 20000.0, (copy, read)
+    assert 50.0 < mfma < 2600.0, mfma
