@@ -95,6 +95,7 @@ __device__ __forceinline__ float row_sum4(float v) {
 template <int NBUF>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_attn_bf16(AttnP p) {
     constexpr int PD = NBUF - 1;  // blocks in flight
+    static_assert(NBUF >= 2 && NBUF <= 4, "the ring's tail waits cover up to three blocks in flight");
     __shared__ __attribute__((aligned(16))) uint4 kvs[NBUF][1024];
     // The batch metadata is read-only while the kernel runs: reading it
     // through the constant address space gives scalar loads, which keep the
@@ -243,12 +244,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         };
 
         // Ring pipeline over NBUF LDS buffers.  Iteration k waits for its own
-        // loads of block k (the 4*(PD-1) loads of blocks k+1..k+PD-1 may stay
-        // in flight) and its LDS reads, then a barrier makes every wave's
-        // loads of block k visible and retires every wave's reads of block
-        // k-1, whose buffer then receives block k+PD.  Block indices are clamped so every
-        // iteration issues exactly four loads (the counts above stay exact);
-        // the tail re-reads the last block.
+        // loads of block k (the loads of the blocks issued after it may stay
+        // in flight: 4*(PD-1), or 4*(last-k) in the tail) and its LDS reads,
+        // then a barrier makes every wave's loads of block k visible and
+        // retires every wave's reads of block k-1, whose buffer then
+        // receives block k+PD while there is one.  Loads retire in issue
+        // order, so the counts are exact; the prologue clamps its block
+        // indices (a chunk shorter than PD blocks re-reads its last one,
+        // which only makes the waits stricter).
         const int last = nblk - 1;
 #pragma unroll
         for (int u = 0; u < PD; ++u) issue(min(u, last), u);
@@ -257,9 +260,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
             for (int u = 0; u < NBUF; ++u) {
                 const int k = k0 + u;
                 if (k >= nblk) break;
-                wait_vm<4 * (PD - 1), true>();
-                barrier_nofence();
-                issue(min(k + PD, last), (u + PD) % NBUF);
+                if (k + PD <= last) {
+                    wait_vm<4 * (PD - 1), true>();
+                    barrier_nofence();
+                    issue(k + PD, (u + PD) % NBUF);
+                } else {
+                    // tail: blocks k..last are the only ones in flight
+                    if (last - k >= 2) wait_vm<8, true>();
+                    else if (last - k == 1) wait_vm<4, true>();
+                    else wait_vm<0, true>();
+                    barrier_nofence();
+                }
                 compute(u, k);
             }
         }
