@@ -85,7 +85,9 @@ typedef struct sd_config {
 } sd_config;
 
 /* Device pointers of one decoder layer, each row-major [out][in] so that
- * y = W x; element type sd_config.dtype. */
+ * y = W x; element type sd_config.dtype.  The gain vectors (norm1, norm2,
+ * qnorm, knorm and sd_weights.norm_f) must be 8-byte aligned: they are read
+ * four bf16 at a time (sd_verify_init returns SD_EINVAL otherwise). */
 typedef struct sd_layer_weights {
     const void* wq;     /* [n_q_heads*head_dim][d_model] */
     const void* wk;     /* [n_kv_heads*head_dim][d_model] */

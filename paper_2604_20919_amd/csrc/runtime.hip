@@ -572,7 +572,12 @@ sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_poo
             !lw.norm2)
             return SD_EINVAL;
         if (cfg->qk_norm && (!lw.qnorm || !lw.knorm)) return SD_EINVAL;
+        // gains are read four elements (8 bytes in bf16) at a time
+        uintptr_t g = (uintptr_t)lw.norm1 | (uintptr_t)lw.norm2;
+        if (cfg->qk_norm) g |= (uintptr_t)lw.qnorm | (uintptr_t)lw.knorm;
+        if (g & 7) return SD_EINVAL;
     }
+    if ((uintptr_t)w->norm_f & 7) return SD_EINVAL;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return SD_ENODEV;
     hipDeviceProp_t prop;

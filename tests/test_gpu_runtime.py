@@ -150,3 +150,23 @@ def test_calibration_peaks():
     mfma = sv.sd_calib_mfma(sink.data_ptr(), 256, s)
     assert 200.0 < copy < 20000.0 and 200.0 < read < 20000.0, (copy, read)
     assert 50.0 < mfma < 2600.0, mfma
+
+
+def test_misaligned_gain_pointers_are_rejected():
+    """Gain vectors are read four bf16 at a time; init refuses a gain pointer
+    that is not 8-byte aligned (layer norms, QK norms, final norm)."""
+    w = wl.custom_workload("tiny-bf16", [20, 33], [2, 3], seed=74)
+    dw = DeviceWeights(w.model, w.seed)
+    for field in ("norm1", "qnorm", "norm_f"):
+        ptrs = layer_ptrs(dw)
+        if field == "norm_f":
+            ptrs["norm_f"] += 2
+        else:
+            ptrs["layers"][1][field] += 2
+        with pytest.raises(sv.SdError) as ei:
+            Verifier(w.model, ptrs, n_pages=16, max_users=w.n_users, max_draft=4, max_batch_users=w.n_users,
+                     max_batch_tokens=16, max_ctx=64, max_pending=1)
+        assert ei.value.status == sv.SD_EINVAL, field
+    # the aligned pointers still initialise
+    Verifier(w.model, layer_ptrs(dw), n_pages=16, max_users=w.n_users, max_draft=4,
+             max_batch_users=w.n_users, max_batch_tokens=16, max_ctx=64, max_pending=1).close()
