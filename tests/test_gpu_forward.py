@@ -196,27 +196,37 @@ def test_determinism_two_runs_bit_identical():
     v.close()
 
 
-@pytest.mark.parametrize("T_target", [17, 70, 75, 80, 105, 112, 150, 250, 300, 416])
+@pytest.mark.parametrize("T_target", [17, 64, 65, 70, 75, 80, 96, 97, 105, 112, 113, 150, 224, 225, 250,
+                                      256, 257, 300, 320, 321, 416])
 def test_bf16_every_gemm_tile_class(T_target):
-    """Query-slot totals that select each GEMM tile class: the 16x16 form up
-    to 96 slots, the 32x32 form above (eight-wave tiles up to 224 slots,
-    four-wave tiles above), the packed-plane 32x32 tiles (split-K partials
-    at 65..80 slots, every GEMM at 97..112, with and without padding in the
-    mixed tile), split-K and unsplit paths, up to the 416-slot maximum."""
+    """Query-slot totals that select each GEMM tile class, and both sides of
+    every boundary between them: the 16x16 form up to 96 slots, the 32x32
+    form above (eight-wave tiles up to 256 slots, four-wave tiles above;
+    32-k chunks at 225..320 slots, 16-k chunks above 320), the
+    packed-plane 32x32 tiles (split-K partials at 65..80 slots, every GEMM
+    at 97..112, with and without padding in the mixed tile), split-K and
+    unsplit paths, up to the 416-slot maximum."""
     rng = np.random.default_rng(T_target)
     L, T = [], 0
     while T < T_target:
-        l = int(min(rng.integers(1, 13), T_target - T - 1)) if T_target - T > 1 else 0
-        if l < 1:
-            break
+        rem = T_target - T
+        if rem == 1:
+            # one slot left: an earlier user drafts one more token
+            j = next(i for i, x in enumerate(L) if x < 12)
+            L[j] += 1
+            T += 1
+            continue
+        l = int(min(rng.integers(1, 13), rem - 1))
         L.append(l)
         T += l + 1
+    assert T == T_target
     prefix = [int(p) for p in rng.integers(0, 200, size=len(L))]
     w = wl.custom_workload("tiny-bf16", prefix, L, seed=40 + T_target, q_sigma=1.0)
     dw = DeviceWeights(w.model, w.seed, gamma="uniform")
     v = make_verifier(w, dw)
     load_synthetic_kv(v, w)
     b = w.batch(0)
+    assert b.T == T_target
     ws = oracle.WeightSource(w.model, w.seed, "uniform")
     gpu = run_gpu(v, w, 0, b, "stochastic", seed=2, round_=3)
     rl, ref = run_oracle(w, b, "stochastic", seed=2, round_=3, weights=ws)
