@@ -38,9 +38,13 @@ Searches:
     equal size are interchangeable, so their lengths are enumerated as
     non-increasing sequences.
 
-Parity status: pinned to the throughputs the paper prints for its
-homogeneous experiments (Sec. V-B) and to closed forms (eq. 1's geometric
-sum, the autoregressive baseline); see tests/test_scheduler.py.
+Parity status: pinned to the throughputs and speedups the paper prints for
+its homogeneous experiments (Sec. V-B, kept with their citations in
+tests/golden/dipsd_printed_values.json) and to closed forms (eq. 1's
+geometric sum, the autoregressive baseline); see tests/test_scheduler.py.
+The heterogeneous experiments (Sec. V-B-2) are not pinned: the per-user
+values of their three cases cannot be recovered unambiguously from the
+text.
 """
 from __future__ import annotations
 
@@ -250,6 +254,25 @@ def homogeneous_global(sysm: System) -> Tuple[float, int, tuple, tuple]:
         if r > best[0]:
             best = (r, N, sizes, lens)
     return best
+
+
+def ad_greedy_batching(sysm: System) -> Tuple[float, list]:
+    """Sec. V-A's "AD w/ greedy batching" baseline: users sorted by prefix
+    length, longest first, are packed into batches in that order, a new
+    batch starting whenever the next user would break the memory bound
+    (eq. 19-21); every batch then decodes one token per user per forward
+    (no drafts: G^v(b, F^v(1, I_n))), the batches one after another.
+    Returns (tokens per second, batches)."""
+    order = sorted(range(sysm.M), key=lambda m: -sysm.prefix[m])
+    batches, cur = [], []
+    for m in order:
+        if cur and not memory_ok(sysm, len(cur) + 1, max(sysm.prefix[x] for x in cur + [m])):
+            batches.append(cur)
+            cur = []
+        cur.append(m)
+    batches.append(cur)
+    ms = sum(t_verify(sysm, len(b), 1, max(sysm.prefix[x] for x in b)) for b in batches)
+    return 1000.0 * sysm.M / ms, batches
 
 
 def autoregressive(sysm: System) -> float:
