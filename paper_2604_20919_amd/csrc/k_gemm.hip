@@ -767,7 +767,10 @@ static GemmShape shape_for(int T, int vcols, bool raw, int K) {
             const int s8 = std::min(std::max(1, K / 128 / 2), std::max(1, cu_count() / tiles8));
             if (10 * tiles8 * s8 < 9 * cu_count()) return GemmShape{16, mt, 2, 64, 4, 2, 0, 1};
         }
-        return wide ? GemmShape{16, mt, 2, 128, 8, 1, 0} : GemmShape{16, mt, 2, 64, 4, 2, 0};
+        // the lm_head (151936 rows: not a multiple of 256) takes the
+        // eight-wave tiles too; its last workgroup has fewer units
+        if (wide || (!raw && vcols % 32 == 0)) return GemmShape{16, mt, 2, 128, 8, 1, 0};
+        return GemmShape{16, mt, 2, 64, 4, 2, 0};
     }
     const int mt = (T + 31) / 32;
     if (mt <= 4) return wide ? GemmShape{32, mt, 1, 64, 8, 2, 0} : GemmShape{32, mt, 1, 64, 4, 2, 0};
@@ -898,14 +901,6 @@ size_t gemm_partial_floats(const Dims& D, int Tmax) {
 }
 
 
-bool gemm_shape_ok(const Dims& D, int T, int K, int N, int epi) {
-    if (!D.bf16) return true;
-    const int vcols = epi == EPI_SWIGLU ? 2 * N : N;
-    const GemmShape sh = shape_for(T, vcols, false, K);
-    if (sh.MT == 0) return false;
-    return K % sh.KC == 0 && K % 32 == 0 && vcols % (sh.F * sh.NW * sh.NSUB) == 0;
-}
-
 int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_t s) {
     if (!D.bf16) {
         GemmF p;
@@ -927,7 +922,7 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
     }
     const int vcols = g.epi == EPI_SWIGLU ? 2 * g.N : g.N;
     const GemmShape sh = shape_for(g.T, vcols, g.raw != 0, g.K);
-    const int nt = sh.F * sh.NW * sh.NSUB;
+    const int unit_rows = sh.F * sh.NSUB;  // weight rows of one wave
     GemmP p;
     p.X = (const bf16_t*)g.X;
     p.Wp = (const bf16_t*)g.Wp;
@@ -936,7 +931,10 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
     p.T = g.T;
     p.kchunks = g.K / sh.KC;
     p.vcols = vcols;
-    p.tiles = p.vcols / nt;
+    // workgroups of NW waves; a last partial workgroup when the row count is
+    // not a multiple of NW units (its surplus waves load and store nothing)
+    const int units = p.vcols / unit_rows;
+    p.tiles = (units + sh.NW - 1) / sh.NW;
     int S = choose_splits(p.tiles, p.kchunks, sh.FILL ? 8 : sh.NW);
     while (S > 1 && (size_t)S * g.T * p.vcols > sb.gpart_floats) {
         int t = S - 1;
@@ -944,7 +942,7 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
         S = t;
     }
     p.S = S;
-    p.G = p.tiles * sh.NW;
+    p.G = units;
     p.WPS = p.tiles;
     p.part = sb.gpart;
     p.out = g.out;

@@ -21,7 +21,6 @@
 using namespace sdv;
 
 namespace sdv {
-bool gemm_shape_ok(const Dims& D, int T, int K, int N, int epi);
 }
 
 namespace {
