@@ -298,34 +298,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 }
 
 // Merge the partials of the chunks of (b, g) for one query row in chunk
-// order; one wave per (slot, query head).  Chunks are taken eight at a time
-// with all their loads issued before the merge (online maximum: the running
-// sums are rescaled when a group raises it).
-template <typename TA>
+// order; half a wave per (slot, query head), lane l of it holding dims
+// 4l..4l+3 (16-byte partial loads, 8-byte stores of the two output planes).
+// Chunks are taken eight at a time with all their loads issued before the
+// merge (online maximum: the running sums are rescaled when a group raises
+// it).
 __global__ __launch_bounds__(256) void k_attn_combine(BatchView bv, const float* apart,
-                                                      const float* aml, TA* out, int hq, int hkv,
-                                                      int hd) {
-    const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
-    const int t = wave / hq, h = wave % hq;
+                                                      const float* aml, bf16_t* out, int hq, int hkv) {
+    const int rid = blockIdx.x * 8 + (threadIdx.x >> 5);  // (slot, query head)
+    const int l = threadIdx.x & 31;
+    const int t = rid / hq, h = rid % hq;
     if (t >= bv.T) return;
     const int G = hq / hkv, g = h / G, hh = h % G;
     const int b = bv.slot_b[t], j = bv.slot_j[t];
     const int row = j * G + hh;
     const int i0 = bv.item_off[b], nch = (bv.item_off[b + 1] - i0) / hkv;
     const int p0 = i0 + g * nch, p1 = p0 + nch;
-    const bool hi_ok = lane + 64 < hd;
-    float M = -INFINITY, Ls = 0.f, acc0 = 0.f, acc1 = 0.f;
+    float M = -INFINITY, Ls = 0.f;
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int pg = p0; pg < p1; pg += 8) {
-        float mi[8], li[8], a0[8], a1[8];
+        float mi[8], li[8];
+        f32x4 a[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const bool ok = pg + u < p1;
             const size_t pr = (size_t)(ok ? pg + u : p0) * bv.rows_max + row;
             mi[u] = ok ? aml[pr * 2] : -INFINITY;
             li[u] = ok ? aml[pr * 2 + 1] : 0.f;
-            a0[u] = ok && lane < hd ? apart[pr * hd + lane] : 0.f;
-            a1[u] = ok && hi_ok ? apart[pr * hd + lane + 64] : 0.f;
+            a[u] = ok ? *(const f32x4*)(apart + pr * HD + 4 * l) : f32x4{0.f, 0.f, 0.f, 0.f};
         }
         float mg = M;
 #pragma unroll
@@ -333,22 +333,19 @@ __global__ __launch_bounds__(256) void k_attn_combine(BatchView bv, const float*
         if (mg == -INFINITY) continue;  // no key of these chunks is visible to the row
         const float sc = exp2f(M - mg);  // 0 while M is still -inf
         Ls *= sc;
-        acc0 *= sc;
-        acc1 *= sc;
+        acc *= sc;
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             if (mi[u] == -INFINITY) continue;
             const float w = exp2f(mi[u] - mg);
             Ls += li[u] * w;
-            acc0 += a0[u] * w;
-            acc1 += a1[u] * w;
+            acc += a[u] * w;
         }
         M = mg;
     }
     const float inv = 1.0f / Ls;
-    const size_t o0 = ((size_t)t * hq + h) * hd, pl = (size_t)bv.T * hq * hd;
-    if (lane < hd) st_act(out, pl, o0 + lane, acc0 * inv);
-    if (hi_ok) st_act(out, pl, o0 + lane + 64, acc1 * inv);
+    const float o[4] = {acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv};
+    st_act4(out, (size_t)bv.T * hq * HD, ((size_t)t * hq + h) * HD + 4 * l, o);
 }
 
 // fp32 path: one wave per (slot, query head); lanes split head_dim
@@ -407,8 +404,9 @@ void launch_attention(const Dims& D, const BatchView& bv, const SlotBufs& sb, co
     p.apart = sb.apart;
     p.aml = sb.aml;
     hipLaunchKernelGGL(k_attn_bf16<kAttnBuffers>, dim3(bv.n_items), dim3(256), 0, s, p);
-    hipLaunchKernelGGL(k_attn_combine<bf16_t>, dim3(blocks), dim3(256), 0, s, bv, sb.apart, sb.aml,
-                       (bf16_t*)sb.attn, D.hq, D.hkv, D.hd);
+    // half a wave per (slot, query head)
+    hipLaunchKernelGGL(k_attn_combine, dim3((bv.T * D.hq + 7) / 8), dim3(256), 0, s, bv, sb.apart,
+                       sb.aml, (bf16_t*)sb.attn, D.hq, D.hkv);
 }
 
 }  // namespace sdv

@@ -132,20 +132,6 @@ void launch_resid_norm(const Dims& D, int T, const float* part, int S, float* x,
         resid_norm_dispatch<float>(T, part, S, x, (const float*)gamma, (float*)h, D.d, D.eps, s);
 }
 
-// four values as bf16 (8 bytes); the activation planes hi = bf16(v),
-// lo = bf16(v - hi) of four consecutive columns
-__device__ __forceinline__ uint2 pack_bf16x4(const float (&v)[4]) {
-    return uint2{(uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16),
-                 (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16)};
-}
-__device__ __forceinline__ void st_act4(bf16_t* p, size_t plane, size_t i, const float (&v)[4]) {
-    float lo[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) lo[e] = v[e] - bf16_to_f32(f32_to_bf16(v[e]));
-    *(uint2*)(p + i) = pack_bf16x4(v);
-    *(uint2*)(p + plane + i) = pack_bf16x4(lo);
-}
-
 // ---------------------------------------------------------------------------
 // bf16 configuration: split-K reduction fused with the residual add and the
 // elementwise half of the next RMSNorm.  x[t] += sum_s part[s][t] (split

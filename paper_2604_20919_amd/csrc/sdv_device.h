@@ -47,6 +47,20 @@ template <> __device__ __forceinline__ void st_act<bf16_t>(bf16_t* p, size_t pla
     p[plane + i] = f32_to_bf16(v - bf16_to_f32(hi));
 }
 
+// four values as bf16 (8 bytes); the activation planes hi = bf16(v),
+// lo = bf16(v - hi) of four consecutive columns
+__device__ __forceinline__ uint2 pack_bf16x4(const float (&v)[4]) {
+    return uint2{(uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16),
+                 (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16)};
+}
+__device__ __forceinline__ void st_act4(bf16_t* p, size_t plane, size_t i, const float (&v)[4]) {
+    float lo[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) lo[e] = v[e] - bf16_to_f32(f32_to_bf16(v[e]));
+    *(uint2*)(p + i) = pack_bf16x4(v);
+    *(uint2*)(p + plane + i) = pack_bf16x4(lo);
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
