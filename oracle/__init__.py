@@ -11,12 +11,18 @@ keys/values produced by ``workload``.
 
 Parity status of each function (see the test suite for the pins):
   philox4x64_10    -- pinned to numpy's independent Philox implementation
-  sample           -- pinned by brute-force enumeration, q = p, greedy longest
-                      prefix, and the geometric mean of eq. (1)
+  sample           -- pinned by exact enumeration of the output law on tiny
+                      vocabularies (every draft sequence, accept/reject
+                      outcome and resampled token over several rounds, using
+                      the oracle's own ratios and race weights: the law of
+                      the first n tokens equals the target's to 1e-6), by
+                      Monte-Carlo chi^2 tests of the race itself, q = p,
+                      greedy longest prefix, and the geometric mean of eq. (1)
   forward          -- pinned by textbook special cases (RMSNorm, RoPE,
                       attention, SwiGLU structure), verify/prefill and
                       autoregressive consistency, and a torch.nn.functional
-                      re-implementation on a tiny model
+                      re-implementation on tiny models, with and without the
+                      bf16 rounding of the new slots' keys and values
 """
 from __future__ import annotations
 
@@ -88,7 +94,7 @@ def lib():
         L.or_forward.argtypes = [ctypes.POINTER(_Model), i32, vp, vp, vp, vp, vp, vp,
                                  _LAYER_FN, _KV_FN, vp, vp, vp, vp]
         L.or_sample.argtypes = [i32, i32, vp, vp, ctypes.c_int64, vp, vp, vp, vp, u64, u64,
-                                vp, vp, vp, vp, vp]
+                                vp, vp, vp, vp, vp, vp]
         _lib = L
     return _lib
 
@@ -293,10 +299,11 @@ def expand_sparse_q(idx, val, rest, V: int) -> np.ndarray:
 
 
 def sample(mode, users, draft_len, logits, drafts, q, accept_u=None, seed: int = 0,
-           round_: int = 0):
+           round_: int = 0, want_race_w: bool = False):
     """Verify decisions for a batch: returns dict with n_acc, token, and the
     diagnostics ratio (p/q per draft, fp32), u (uniform per draft) and
-    race_gap (relative gap of the two best race keys per user)."""
+    race_gap (relative gap of the two best race keys per user); with
+    want_race_w also race_w [B][V], the weights of the stop slot's race."""
     mode = MODES[mode] if isinstance(mode, str) else int(mode)
     users = np.ascontiguousarray(users, dtype=np.int32)
     L = np.ascontiguousarray(draft_len, dtype=np.int32)
@@ -317,6 +324,10 @@ def sample(mode, users, draft_len, logits, drafts, q, accept_u=None, seed: int =
     uu = np.empty(max(nd, 1), np.float32)
     gap = np.empty(B, np.float64)
     qp = q if q.size else np.zeros((1, V), np.float32)
+    rw = np.empty((B, V), np.float32) if want_race_w else None
     lib().or_sample(mode, B, _p(users), _p(L), V, _p(logits), _p(drafts), _p(qp), _p(au),
-                    int(seed), int(round_), _p(n_acc), _p(tok), _p(ratio), _p(uu), _p(gap))
-    return {"n_acc": n_acc, "token": tok, "ratio": ratio[:nd], "u": uu[:nd], "race_gap": gap}
+                    int(seed), int(round_), _p(n_acc), _p(tok), _p(ratio), _p(uu), _p(gap), _p(rw))
+    out = {"n_acc": n_acc, "token": tok, "ratio": ratio[:nd], "u": uu[:nd], "race_gap": gap}
+    if want_race_w:
+        out["race_w"] = rw
+    return out

@@ -404,13 +404,15 @@ static int race(const float* w, long V, uint64_t seed, uint64_t round, uint64_t 
  *               rejection race over max(0, p - q) (fallback p if that is all
  *               zero); if all L accepted race over p at slot L.
  *   force:      accept all, token = argmax at slot L (teacher forcing).
- * Outputs n_acc[b], token[b]; optional diagnostics ratio/u per draft and
- * race_gap per user (INFINITY when no race ran).
+ * Outputs n_acc[b], token[b]; optional diagnostics ratio/u per draft,
+ * race_gap per user (INFINITY when no race ran) and race_w [n_users][V], the
+ * weights the stop slot's race ran over (zeros when no race ran), so that a
+ * test can compute the law of the emitted token exactly.
  */
 int or_sample(int32_t mode, int32_t n_users, const int32_t* user_ids, const int32_t* L,
               int64_t V, const float* logits, const int32_t* drafts, const float* q,
               const float* accept_u, uint64_t seed, uint64_t round, int32_t* n_acc,
-              int32_t* token, float* ratio, float* u_used, double* race_gap) {
+              int32_t* token, float* ratio, float* u_used, double* race_gap, float* race_w) {
     long toff = 0, doff = 0;
     float* w = (float*)malloc(sizeof(float) * (size_t)V);
     for (int b = 0; b < n_users; ++b) {
@@ -464,6 +466,10 @@ int or_sample(int32_t mode, int32_t n_users, const int32_t* user_ids, const int3
                     for (long k = 0; k < V; ++k) w[k] = prob32(z[k], mx, sum);
             }
             tok = race(w, V, seed, round, user, (uint64_t)a, &gap);
+        }
+        if (race_w) {
+            float* rw = race_w + (size_t)b * V;
+            for (long k = 0; k < V; ++k) rw[k] = mode == OR_STOCHASTIC ? w[k] : 0.0f;
         }
         n_acc[b] = a;
         token[b] = tok;

@@ -36,7 +36,16 @@ def _rope_torch(x, pos, base):
     return torch.cat([c.real, c.imag], dim=-1)
 
 
-def torch_verify(m, ws, kv, prefix_len, n_slots, tokens):
+def _bf16(x):
+    """round through float32 to bfloat16 (nearest-even), back to float64"""
+    return x.to(torch.float32).to(torch.bfloat16).to(torch.float64)
+
+
+def torch_verify(m, ws, kv, prefix_len, n_slots, tokens, kv_bf16=False, round_at="cache"):
+    """Verify logits from torch.nn.functional routines in float64.  With
+    kv_bf16 the new slots' keys and values are rounded to bfloat16 where a
+    bf16 cache stores them: keys after QK-norm and RoPE (round_at="cache"),
+    or, for the sensitivity check, before them (round_at="projection")."""
     d, hq, hkv, hd, eps = m.d_model, m.n_q_heads, m.n_kv_heads, m.head_dim, m.rms_eps
     T = int(np.sum(n_slots))
     x = _t(ws.global_(wl.EMBED), m)[torch.tensor(tokens, dtype=torch.long)]
@@ -48,10 +57,16 @@ def torch_verify(m, ws, kv, prefix_len, n_slots, tokens):
         q = F.linear(h, w[wl.W_Q]).view(T, hq, hd)
         k = F.linear(h, w[wl.W_K]).view(T, hkv, hd)
         v = F.linear(h, w[wl.W_V]).view(T, hkv, hd)
+        if kv_bf16 and round_at == "projection":
+            k = _bf16(k)
         if m.qk_norm:
             q = F.rms_norm(q, (hd,), w[wl.N_Q], eps)
             k = F.rms_norm(k, (hd,), w[wl.N_K], eps)
         q, k = _rope_torch(q, pos, m.rope_base), _rope_torch(k, pos, m.rope_base)
+        if kv_bf16:
+            if round_at == "cache":
+                k = _bf16(k)
+            v = _bf16(v)
         out = torch.empty(T, hq, hd, dtype=torch.float64)
         for b in range(len(n_slots)):
             P, n = int(prefix_len[b]), int(n_slots[b])
@@ -169,6 +184,27 @@ def test_structured_weights_closed_form():
     h = E / np.sqrt((E * E).mean(1, keepdims=True) + m.rms_eps) * g
     ref = h @ ws.global_(wl.LM_HEAD).astype(np.float64).T
     assert _rel_err(got, ref) < 1e-6
+
+
+@pytest.mark.parametrize("model", ["tiny-bf16", "tiny-qknorm"])
+def test_bf16_kv_rounding_matches_torch(model):
+    """The oracle's bf16 cache reading: the new slots' keys (after QK-norm
+    and RoPE) and values are rounded to bf16 before any slot reads them.
+    A torch float64 re-implementation that rounds at exactly those points
+    agrees to fp32 storage; rounding the keys before QK-norm/RoPE instead
+    (a plausible misplacement) is far outside that bound."""
+    m = wl.MODELS[model]
+    ws = oracle.WeightSource(m, seed=27, gamma="uniform")
+    prefix, slots = [9, 0, 21], [3, 4, 2]
+    kv = oracle.KVSource(m, 27, [0, 1, 2], prefix)
+    tokens = _tokens(m, sum(slots), 6)
+    got = oracle.forward(m, ws, kv, prefix, slots, tokens, kv_bf16=True)
+    ref = torch_verify(m, ws, kv, prefix, slots, tokens, kv_bf16=True)
+    assert _rel_err(got, ref) < 1e-6
+    unrounded = torch_verify(m, ws, kv, prefix, slots, tokens, kv_bf16=False)
+    misplaced = torch_verify(m, ws, kv, prefix, slots, tokens, kv_bf16=True, round_at="projection")
+    assert _rel_err(got, unrounded) > 1e-4
+    assert _rel_err(got, misplaced) > 1e-4
 
 
 def test_bf16_kv_cache_rounding_changes_little():

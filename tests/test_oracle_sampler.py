@@ -8,6 +8,7 @@ speculative-sampling work the paper cites in Sec. I, whose defining property
 is that emitted tokens follow the target distribution.  Each test below
 checks one of these facts on toy tables where the exact answer is known.
 """
+import itertools
 import math
 
 import numpy as np
@@ -312,3 +313,131 @@ def test_sparse_draft_rows_keep_the_target_distribution():
     first = [e[0] for e in _emitted(res, drafts, L)]
     ok, pv = _chi2_ok(np.bincount(first, minlength=V), p[0])
     assert ok, pv
+
+
+# ----------------------------------------------------------------------------
+# exact output law by enumeration
+# ----------------------------------------------------------------------------
+
+class _ContextTables:
+    """Target p(.|ctx) and draft q(.|ctx) for every context (a tuple of
+    tokens), drawn from a seed keyed by the context, with zeros: p forbids a
+    token that q may propose, and q never proposes a token p may need (only
+    the residual can supply it).  The rows differ from context to context, so
+    a sampler reading the wrong slot's row gets a different law."""
+
+    def __init__(self, V, seed):
+        self.V, self.seed = V, seed
+        self._p, self._q = {}, {}
+
+    def _rng(self, ctx, which):
+        return np.random.default_rng([self.seed, which, len(ctx), *ctx])
+
+    def p(self, ctx):
+        if ctx not in self._p:
+            r = self._rng(ctx, 1).dirichlet(np.full(self.V, 0.7))
+            r[(len(ctx) + sum(ctx)) % self.V] = 0.0
+            # round-trip through the float32 logits the oracle receives, so
+            # the law below is the one the logits define
+            z = _logits(r / r.sum())
+            e = np.exp(z.astype(np.float64) - z.max())
+            self._p[ctx] = (z, e / e.sum())
+        return self._p[ctx]
+
+    def q(self, ctx):
+        if ctx not in self._q:
+            r = self._rng(ctx, 2).dirichlet(np.full(self.V, 0.7))
+            r[(len(ctx) + 2 * sum(ctx) + 1) % self.V] = 0.0
+            if len(ctx) % 2 == 0:
+                r[(sum(ctx) + 3) % self.V] = 0.0
+            self._q[ctx] = (r / r.sum()).astype(np.float32)
+        return self._q[ctx]
+
+
+def _round_law(tab, ctx, L, seed):
+    """Exact law of one verification round from context ctx: every draft
+    sequence weighted by its draft probability, every stop slot a weighted by
+    the oracle's own accept ratios (P(accept) = min(1, r) for a uniform u),
+    and the emitted token weighted by the oracle's own race weights at the
+    stop slot (an exponential race picks k with probability w_k / sum w).
+    Returns {emitted tuple: probability}."""
+    V = tab.V
+    seqs = list(itertools.product(range(V), repeat=L))
+    B = len(seqs)
+    logits = np.empty((B * (L + 1), V), np.float32)
+    q = np.empty((B * L, V), np.float32)
+    for b, d in enumerate(seqs):
+        for j in range(L + 1):
+            logits[b * (L + 1) + j] = tab.p(ctx + d[:j])[0]
+        for j in range(L):
+            q[b * L + j] = tab.q(ctx + d[:j])
+    drafts = np.array(seqs, np.int32).reshape(-1)
+    users, lens = np.arange(B), np.full(B, L)
+    law = {}
+    for a in range(L + 1):
+        # uniforms that force the stop at slot a: 0 accepts any r > 0, +inf
+        # rejects any finite r (branches they cannot force have probability 0)
+        u = np.zeros((B, L), np.float32)
+        if a < L:
+            u[:, a] = np.inf
+        res = oracle.sample("stochastic", users, lens, logits, drafts, q, accept_u=u.reshape(-1),
+                            seed=seed, want_race_w=True)
+        r = res["ratio"].reshape(B, L).astype(np.float64)
+        for b, d in enumerate(seqs):
+            pd = float(np.prod([q[b * L + j, d[j]] for j in range(L)], dtype=np.float64))
+            if pd == 0.0:
+                continue  # a draft q never proposes (its ratio may be 0/0)
+            acc = np.minimum(1.0, r[b])
+            pa = float(np.prod(acc[:a])) * (1.0 - acc[a] if a < L else 1.0)
+            if pa == 0.0:
+                continue
+            assert res["n_acc"][b] == a
+            w = res["race_w"][b].astype(np.float64)
+            assert w.sum() > 0
+            for k in np.nonzero(w)[0]:
+                e = tuple(d[:a]) + (int(k),)
+                law[e] = law.get(e, 0.0) + pd * pa * w[k] / w.sum()
+    return law
+
+
+def _first_n_law(tab, ctx, n, L, seed, memo):
+    """Exact law of the first n emitted tokens from ctx over as many rounds
+    as it takes (each round continues from the tokens it emitted)."""
+    if n <= 0:
+        return {(): 1.0}
+    key = (ctx, n)
+    if key in memo:
+        return memo[key]
+    out = {}
+    for e, pe in _round_law(tab, ctx, L, seed).items():
+        if len(e) >= n:
+            out[e[:n]] = out.get(e[:n], 0.0) + pe
+        else:
+            for rest, pr in _first_n_law(tab, ctx + e, n - len(e), L, seed, memo).items():
+                out[e + rest] = out.get(e + rest, 0.0) + pe * pr
+    memo[key] = out
+    return out
+
+
+@pytest.mark.parametrize("V,L,n", [(4, 1, 3), (4, 2, 4), (3, 3, 4), (5, 2, 3)])
+def test_output_law_by_enumeration(V, L, n):
+    """The tokens emitted by repeated verification rounds follow the target
+    model exactly: the law of the first n tokens, summed over every draft
+    sequence, accept/reject outcome and resampled token, equals the product
+    of the target rows along the sequence (the defining property of the
+    speculative-sampling rule of the works cited in Sec. I)."""
+    tab = _ContextTables(V, seed=100 * V + 10 * L + n)
+    law = _first_n_law(tab, (), n, L, seed=3, memo={})
+    worst = 0.0
+    total = 0.0
+    for y in itertools.product(range(V), repeat=n):
+        want = 1.0
+        for t in range(n):
+            want *= tab.p(y[:t])[1][y[t]]
+        got = law.get(y, 0.0)
+        total += got
+        worst = max(worst, abs(got - want))
+        if want == 0.0:
+            assert got == 0.0, f"{y} emitted although the target forbids it"
+    assert abs(total - 1.0) < 1e-6
+    assert worst < 1e-6, f"max |law - target| = {worst}"
