@@ -8,6 +8,11 @@ steps, so every step verifies the same batch.  Reported value: accepted
 tokens per second, sum over users of (a_m + 1) per step / seconds per step
 (the numerator of DiP-SD's throughput, eq. 2 and eq. 22).
 
+The headline workload is the 32-user ragged batch of the Qwen3-32B shape
+(prefixes U{256..4096}, l_m U{1..12}); the 16-user batch (stochastic and
+greedy) and the four pipelined 16-user batches (HIP graphs, two streams)
+are timed in the same run and reported under "workloads".
+
 Prints one JSON line (rank 0, one GPU).  Inputs are seeded synthetic stand-ins:
 random-init Qwen3-shaped weights, synthetic cached KV, synthetic draft
 distributions; no trained weights or prompts are used.
@@ -35,10 +40,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="qwen3-32b-b16")
+    ap.add_argument("--workload", default="qwen3-32b-ragged32")
+    ap.add_argument("--extra", default="qwen3-32b-b16,qwen3-32b-pipe4x16",
+                    help="comma-separated workloads timed after the headline one ('none': skip)")
     ap.add_argument("--mode", default="stochastic", choices=["stochastic", "greedy"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-layers", type=int, default=8,
+    ap.add_argument("--cpu-layers", type=int, default=4,
                     help="decoder layers the CPU-baseline sample runs (extrapolated to all)")
     ap.add_argument("--breakdown", action="store_true", help="time every kernel class")
     ap.add_argument("--no-greedy", action="store_true",
@@ -59,6 +66,111 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+class Run:
+    """One workload on the GPU: weights, verifier context, cached KV and
+    device inputs, ready to time."""
+
+    def __init__(self, name, args, torch, graph=-1, q_topk=0, mode="stochastic"):
+        import workload as wl
+        from workload.device import DeviceWeights, batch_to_device, kv_rows
+        from paper_2604_20919_amd.verifier import Verifier
+        self.torch = torch
+        self.name = name
+        self.mode = mode
+        w = self.w = wl.workload(name)
+        m = self.m = w.model
+        self.graph = (1 if w.n_batches > 1 else 0) if graph < 0 else graph
+        t0 = time.time()
+        self.dw = DeviceWeights(m, w.seed)
+        log(f"{name}: weights {self.dw.nbytes() / 1e9:.1f} GB generated on GPU in {time.time() - t0:.1f}s")
+        names = {"wq": wl.W_Q, "wk": wl.W_K, "wv": wl.W_V, "wo": wl.W_O, "wg": wl.W_G, "wu": wl.W_U,
+                 "wd": wl.W_D, "norm1": wl.N_1, "norm2": wl.N_2, "qnorm": wl.N_Q, "knorm": wl.N_K}
+        dw = self.dw
+        ptrs = {"embed": dw.ptr(wl.EMBED), "lm_head": dw.ptr(wl.LM_HEAD), "norm_f": dw.ptr(wl.NORM_F),
+                "layers": [{f: dw.ptr(k, l) for f, k in names.items()} for l in range(m.n_layers)]}
+        nb = self.nb = w.n_batches
+        batches = self.batches = [w.batch(n) for n in range(nb)]
+        max_ctx = int((w.prefix_len + w.draft_len).max()) + 1
+        pages = sum((int(p) + int(l) + 1 + 15) // 16 for p, l in zip(w.prefix_len, w.draft_len)) + 16
+        v = self.v = Verifier(m, ptrs, n_pages=pages, max_users=w.n_users, max_draft=int(w.draft_len.max()),
+                              max_batch_users=max(len(b.users) for b in batches),
+                              max_batch_tokens=max(b.T for b in batches), max_ctx=max_ctx,
+                              max_pending=min(nb, 8))
+        log(f"{name}: KV pool {v.kv_bytes / 1e9:.1f} GB, workspace {v.ws_bytes / 1e9:.2f} GB")
+        t0 = time.time()
+        dt = torch.int16 if m.dtype == "bf16" else torch.float32
+        pmax = int(w.prefix_len.max())
+        buf = (torch.empty((pmax, m.n_kv_heads, m.head_dim), dtype=dt, device="cuda"),
+               torch.empty((pmax, m.n_kv_heads, m.head_dim), dtype=dt, device="cuda"))
+        for b in batches:
+            for i, u in enumerate(b.users):
+                P = int(b.prefix_len[i])
+                v.reset_user(int(u), P, int(b.root[i]))
+                for l in range(m.n_layers):
+                    k, vv = kv_rows(m, w.seed, l, int(u), P, out=buf)
+                    v.write_kv(int(u), l, 0, k, vv)
+        torch.cuda.synchronize()
+        del buf
+        self.kv_tokens = int(w.prefix_len.sum())
+        log(f"{name}: cached KV of {self.kv_tokens} tokens written in {time.time() - t0:.1f}s")
+        self.sparse = None
+        self.q_topk = q_topk
+        if q_topk > 0:
+            self.sparse = []
+            for b in batches:
+                sr = wl.sparsify(b, q_topk, w.seed)   # redraws b.drafts from the sparse rows
+                self.sparse.append(tuple(torch.from_numpy(a).cuda() for a in (sr.idx, sr.val, sr.rest)))
+        self.dev_in = [batch_to_device(b) for b in batches]
+        if mode == "greedy":
+            plant_greedy_drafts(v, w, batches, self.dev_in, torch)
+        self.streams = [torch.cuda.Stream() for _ in range(min(nb, 2))]
+        self.verified_step = sum(b.T for b in batches)
+
+    def step(self, one_stream=False, mode=None):
+        # one_stream: every batch on the first stream, so that the event pairs
+        # of the profiling passes time kernels that share the GPU with nothing
+        mode = mode or self.mode
+        w, v = self.w, self.v
+        for n in range(self.nb):
+            d, q, au = self.dev_in[n]
+            st = self.streams[0] if one_stream else self.streams[n % len(self.streams)]
+            if self.sparse is not None and mode == "stochastic":
+                v.verify_sparse(n, w.assign, w.draft_len, d, *self.sparse[n], mode, seed=w.seed,
+                                round_=0, accept_u=au, stream=st)
+                continue
+            v.verify(n, w.assign, w.draft_len, d, q, mode, seed=w.seed, round_=0,
+                     accept_u=au if mode == "stochastic" else None, stream=st, graph=bool(self.graph))
+        acc = 0
+        for n in range(self.nb):
+            n_acc, _ = v.accept(n, w.n_users)
+            acc += int((n_acc[self.batches[n].users] + 1).sum())
+        return acc
+
+    def time(self, steps, warmup, mode=None):
+        """Timed region: `steps` whole steps after `warmup` untimed ones,
+        bracketed by device synchronisation; returns ms per step, accepted
+        tokens per step and the per-step times."""
+        torch = self.torch
+        for _ in range(warmup):
+            self.step(mode=mode)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        accepted = 0
+        marks = [t0]
+        for _ in range(steps):
+            accepted += self.step(mode=mode)   # ends in sd_accept, which waits for the batch
+            marks.append(time.perf_counter())
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        return 1e3 * elapsed / steps, accepted / steps, np.diff(np.array(marks)) * 1e3
+
+    def close(self):
+        self.v.close()
+        del self.v, self.dw, self.dev_in, self.sparse
+        self.torch.cuda.synchronize()
+        self.torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -66,10 +178,7 @@ def main():
                           "n_gpus": args.gpus}))
         sys.exit(2)
     import torch
-    import workload as wl
-    from workload.device import DeviceWeights, batch_to_device, kv_rows
     from paper_2604_20919_amd import sdverify as sv
-    from paper_2604_20919_amd.verifier import Verifier
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     sv.lib()  # fails loudly if the HIP library is not built
@@ -83,130 +192,51 @@ def main():
         log("copy calibration: 3 x 1 GiB device-to-device copies done")
         del src, dst
 
-    w = wl.workload(args.workload)
-    m = w.model
-    if args.graph < 0:
-        args.graph = 1 if w.n_batches > 1 else 0
-    t0 = time.time()
-    dw = DeviceWeights(m, w.seed)
-    log(f"weights {dw.nbytes() / 1e9:.1f} GB generated on GPU in {time.time() - t0:.1f}s")
-
-    names = {"wq": wl.W_Q, "wk": wl.W_K, "wv": wl.W_V, "wo": wl.W_O, "wg": wl.W_G, "wu": wl.W_U,
-             "wd": wl.W_D, "norm1": wl.N_1, "norm2": wl.N_2, "qnorm": wl.N_Q, "knorm": wl.N_K}
-    ptrs = {"embed": dw.ptr(wl.EMBED), "lm_head": dw.ptr(wl.LM_HEAD), "norm_f": dw.ptr(wl.NORM_F),
-            "layers": [{f: dw.ptr(k, l) for f, k in names.items()} for l in range(m.n_layers)]}
-    nb = w.n_batches
-    batches = [w.batch(n) for n in range(nb)]
-    max_ctx = int((w.prefix_len + w.draft_len).max()) + 1
-    pages = sum((int(p) + int(l) + 1 + 15) // 16 for p, l in zip(w.prefix_len, w.draft_len)) + 16
-    v = Verifier(m, ptrs, n_pages=pages, max_users=w.n_users, max_draft=int(w.draft_len.max()),
-                 max_batch_users=max(len(b.users) for b in batches),
-                 max_batch_tokens=max(b.T for b in batches), max_ctx=max_ctx,
-                 max_pending=min(nb, 8))
-    log(f"KV pool {v.kv_bytes / 1e9:.1f} GB, workspace {v.ws_bytes / 1e9:.2f} GB")
-
-    t0 = time.time()
-    dt = torch.int16 if m.dtype == "bf16" else torch.float32
-    pmax = int(w.prefix_len.max())
-    buf = (torch.empty((pmax, m.n_kv_heads, m.head_dim), dtype=dt, device="cuda"),
-           torch.empty((pmax, m.n_kv_heads, m.head_dim), dtype=dt, device="cuda"))
-    for b in batches:
-        for i, u in enumerate(b.users):
-            P = int(b.prefix_len[i])
-            v.reset_user(int(u), P, int(b.root[i]))
-            for l in range(m.n_layers):
-                k, vv = kv_rows(m, w.seed, l, int(u), P, out=buf)
-                v.write_kv(int(u), l, 0, k, vv)
-    torch.cuda.synchronize()
-    del buf
-    kv_tokens = int(w.prefix_len.sum())
-    log(f"cached KV of {kv_tokens} tokens written in {time.time() - t0:.1f}s")
-
-    sparse = None
-    if args.q_topk > 0:
-        sparse = []
-        for b in batches:
-            sr = wl.sparsify(b, args.q_topk, w.seed)   # redraws b.drafts from the sparse rows
-            sparse.append(tuple(torch.from_numpy(a).cuda() for a in (sr.idx, sr.val, sr.rest)))
-    dev_in = [batch_to_device(b) for b in batches]
-    if args.mode == "greedy":
-        plant_greedy_drafts(v, w, batches, dev_in, torch)
-    streams = [torch.cuda.Stream() for _ in range(min(nb, 2))]
-
-    def step(one_stream=False):
-        # one_stream: every batch on the first stream, so that the event pairs
-        # of the profiling passes time kernels that share the GPU with nothing
-        for n in range(nb):
-            d, q, au = dev_in[n]
-            st = streams[0] if one_stream else streams[n % len(streams)]
-            if sparse is not None and args.mode == "stochastic":
-                v.verify_sparse(n, w.assign, w.draft_len, d, *sparse[n], args.mode, seed=w.seed,
-                                round_=0, accept_u=au, stream=st)
-                continue
-            v.verify(n, w.assign, w.draft_len, d, q, args.mode, seed=w.seed, round_=0,
-                     accept_u=au, stream=st, graph=bool(args.graph))
-        acc = 0
-        for n in range(nb):
-            n_acc, _ = v.accept(n, w.n_users)
-            acc += int((n_acc[batches[n].users] + 1).sum())
-        return acc
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    accepted = 0
-    marks = [t0]
-    for _ in range(args.steps):
-        accepted += step()   # ends in sd_accept, which waits for the batch
-        marks.append(time.perf_counter())
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    per_step = np.diff(np.array(marks)) * 1e3
-    ms_step = 1e3 * elapsed / args.steps
-    acc_step = accepted / args.steps
-    verified_step = sum(b.T for b in batches)
+    run = Run(args.workload, args, torch, graph=args.graph, q_topk=args.q_topk, mode=args.mode)
+    w, m, v, nb, batches = run.w, run.m, run.v, run.nb, run.batches
+    ms_step, acc_step, per_step = run.time(args.steps, args.warmup)
+    verified_step = run.verified_step
     value = acc_step / (ms_step / 1e3)
-    log(f"{ms_step:.3f} ms/step, {acc_step:.1f} accepted / {verified_step} verified tokens per step")
+    log(f"{args.workload}: {ms_step:.3f} ms/step, {acc_step:.1f} accepted / {verified_step} verified tokens per step")
+    step = run.step
 
     # ---- roofline of the dominant kernel (gate/up GEMM + SwiGLU), timed live ----
-    # slots per launch: the batches' mean (each batch launches once per layer)
-    T = sum(b.T for b in batches) / nb
-    per_layer_w = 2 * m.d_ffn * m.d_model * m.wbytes
-    # weights once, plus the activation input and SwiGLU output at 4 B per
-    # element: two bf16 planes (hi, lo) in the bf16 path, fp32 otherwise
-    act_bytes = 4
-    gu_bytes = int(per_layer_w + T * m.d_model * act_bytes + T * m.d_ffn * act_bytes)
+    # Algorithmic bytes per launch: the layer's gate and up weights, read once
+    # (2 x d_ffn x d_model bf16).  Time per launch: the average of HIP-event
+    # pairs recorded around every gate/up launch on the stream it runs on.
+    T = sum(b.T for b in batches) / nb   # slots per launch (the batches' mean)
+    gu_bytes = 2 * m.d_ffn * m.d_model * m.wbytes
+    gu_flops = 2.0 * T * 2 * m.d_ffn * m.d_model   # model FLOPs per launch
     prof_steps = max(3, args.steps // 2)
     sv.sd_profile_begin(v.ctx, sv.SD_K_GATEUP, prof_steps * nb * m.n_layers + 8)
     for _ in range(prof_steps):
         step(one_stream=True)
     gu_ms, gu_n = sv.sd_profile_end(v.ctx)
-    # cost of an event pair with nothing between them, on the same stream
+    # cost of an event pair with nothing between them, on the same stream (reported only)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(64)]
     for a, b in ev:
-        a.record(streams[0])
-        b.record(streams[0])
+        a.record(run.streams[0])
+        b.record(run.streams[0])
     torch.cuda.synchronize()
     pair_ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
-    gu_avg_s = max(gu_ms / max(gu_n, 1) - pair_ms, 1e-6) / 1e3
+    gu_avg_s = gu_ms / max(gu_n, 1) / 1e3
     achieved = gu_bytes / gu_avg_s / 1e9
     traffic = measured_traffic(args.workload)
-    roofline = {"bound": "hbm", "kernel": "k_gemm16/k_gemm32 (gate/up + SwiGLU epilogue)",
+    mfma_tf = gu_flops / gu_avg_s / 1e12
+    roofline = {"bound": "hbm", "kernel": "gate/up GEMM with the SwiGLU epilogue (k_gemm16/k_gemm32)",
                 "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "traffic_over_algorithmic": round(traffic / gu_bytes, 4) if traffic else None,
-                "bytes_per_launch": gu_bytes, "avg_launch_us": round(gu_avg_s * 1e6, 2),
-                "launches": gu_n, "event_pair_us_subtracted": round(pair_ms * 1e3, 2),
-                "mfma_tflops": round(2.0 * T * 2 * m.d_ffn * m.d_model / gu_avg_s / 1e12, 1),
-                "mfma_frac_bf16": round(2.0 * T * 2 * m.d_ffn * m.d_model / gu_avg_s / 1e12 / BF16_PEAK_TFLOPS, 4)}
+                "bytes_per_launch": gu_bytes, "slots_per_launch": T, "avg_launch_us": round(gu_avg_s * 1e6, 2),
+                "launches": gu_n, "empty_event_pair_us": round(pair_ms * 1e3, 2),
+                "mfma_tflops": round(mfma_tf, 1), "mfma_frac_bf16": round(mfma_tf / BF16_PEAK_TFLOPS, 4)}
 
     # achievable peaks of this GPU (library calibration kernels): a read-only
     # stream and a copy of 1 GiB (4x the last-level cache), and a bf16 MFMA
     # loop with no memory traffic
     cal_buf = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
     cal_sink = torch.empty(4, dtype=torch.float32, device="cuda")
-    cs0 = streams[0].cuda_stream
+    cs0 = run.streams[0].cuda_stream
     achievable = {"hbm_read_gbs": round(sv.sd_calib_hbm(cal_buf.data_ptr(), cal_buf.numel(), 1, 10, cs0), 1),
                   "hbm_copy_gbs": round(sv.sd_calib_hbm(cal_buf.data_ptr(), cal_buf.numel(), 0, 10, cs0), 1),
                   "mfma_bf16_tflops": round(sv.sd_calib_mfma(cal_sink.data_ptr(), 2048, cs0), 1),
@@ -215,29 +245,30 @@ def main():
     del cal_buf, cal_sink
     hbm_ach = achievable["hbm_read_gbs"]
     roofline["frac_of_achievable"] = round(achieved / hbm_ach, 4)
-    roofline["mfma_frac_of_achievable"] = round(roofline["mfma_tflops"] / achievable["mfma_bf16_tflops"], 4)
+    roofline["mfma_frac_of_achievable"] = round(mfma_tf / achievable["mfma_bf16_tflops"], 4)
     # the matrix cores run each product on both activation planes: twice the model's FLOPs
-    roofline["mfma_issued_tflops"] = round(2 * roofline["mfma_tflops"], 1)
-    roofline["mfma_issued_frac_of_achievable"] = round(2 * roofline["mfma_tflops"] / achievable["mfma_bf16_tflops"], 4)
+    roofline["mfma_issued_tflops"] = round(2 * mfma_tf, 1)
+    roofline["mfma_issued_frac_bf16"] = round(2 * mfma_tf / BF16_PEAK_TFLOPS, 4)
+    roofline["mfma_issued_frac_of_achievable"] = round(2 * mfma_tf / achievable["mfma_bf16_tflops"], 4)
 
     def class_ms(k, steps=3):
-        """Per-step device time of one kernel class (event pair per scope,
-        the empty pair's cost subtracted)."""
+        """Per-step device time of one kernel class (sum of the event pairs
+        around its launches)."""
         sv.sd_profile_begin(v.ctx, k, steps * nb * (4 * m.n_layers + 8))
         for _ in range(steps):
             step(one_stream=True)
         ms, n = sv.sd_profile_end(v.ctx)
-        return max(ms - n * pair_ms, 1e-6) / steps
+        return max(ms, 1e-6) / steps
 
     # attention (all layers, KV streamed once per user) and sampler rates
     kv_read_step = sum(int(p + l + 1) for p, l in zip(w.prefix_len, w.draft_len)) * m.kv_bytes_per_token()
     attn_ms = class_ms(sv.SD_K_ATTN)
     nd_all = int(sum(int(b.draft_len.sum()) for b in batches))
-    if sparse is not None:
+    if run.sparse is not None:
         # logits once; every sparse row's K entries (the accept lookups) and remainders
-        samp_bytes = sum(b.T for b in batches) * m.vocab * 4 + nd_all * (args.q_topk * 8 + 4)
+        samp_bytes = verified_step * m.vocab * 4 + nd_all * (args.q_topk * 8 + 4)
     else:
-        samp_bytes = sum(b.T for b in batches) * m.vocab * 4 + int(w.n_users) * m.vocab * 4
+        samp_bytes = verified_step * m.vocab * 4 + int(w.n_users) * m.vocab * 4
     samp_ms = class_ms(sv.SD_K_SAMPLER)
     kernels = {
         "attention": {"achieved": round(kv_read_step / (attn_ms / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
@@ -250,7 +281,7 @@ def main():
                     "frac_of_achievable": round(samp_bytes / (samp_ms / 1e3) / 1e9 / hbm_ach, 4),
                     "bytes_per_step": samp_bytes, "ms_per_step": round(samp_ms, 4),
                     "note": ("accept/reject + resample kernels; bytes = T x V fp32 logits + "
-                             + ("the sparse rows" if sparse is not None else "one q row per user"))},
+                             + ("the sparse rows" if run.sparse is not None else "one q row per user"))},
     }
 
     breakdown = None
@@ -259,19 +290,14 @@ def main():
         for name, k in (("qkv", sv.SD_K_QKV), ("attention", sv.SD_K_ATTN), ("o_proj", sv.SD_K_O),
                         ("gate_up", sv.SD_K_GATEUP), ("down", sv.SD_K_DOWN), ("lm_head", sv.SD_K_LMHEAD),
                         ("sampler", sv.SD_K_SAMPLER), ("small", sv.SD_K_SMALL)):
-            sv.sd_profile_begin(v.ctx, k, 3 * nb * (4 * m.n_layers + 8))
-            for _ in range(3):
-                step(one_stream=True)
-            ms, n = sv.sd_profile_end(v.ctx)
-            breakdown[name] = round(ms / 3, 4)
+            breakdown[name] = round(class_ms(k), 4)
         log(f"per-step ms by kernel class: {breakdown}")
 
     # algorithmic bytes of one step: weights once per batch, each user's KV
     # once, logits and q rows once
     wbytes = (m.n_layers * m.layer_params() + 2 * m.vocab * m.d_model) * m.wbytes
     wbytes -= m.vocab * m.d_model * m.wbytes  # embedding: only T rows are read
-    kv_read = sum(int(p + l + 1) for p, l in zip(w.prefix_len, w.draft_len)) * m.kv_bytes_per_token()
-    step_bytes = nb * wbytes + kv_read
+    step_bytes = nb * wbytes + kv_read_step
     result = {
         "metric": "accepted tokens/s, Qwen3-32B-shaped batch verify; MFMA util + HBM GB/s",
         "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
@@ -282,12 +308,12 @@ def main():
         "data": "synthetic (random-init weights N(0,0.02), synthetic KV N(0,1), synthetic draft q)",
         "config": {"workload": args.workload, "model": m.name, "mode": args.mode,
                    "users": int(w.n_users), "batches": nb, "verified_tokens_per_step": verified_step,
-                   "prefix_tokens": kv_tokens, "hip_graph": bool(args.graph) and sparse is None,
-                   "q_payload": (f"sparse top-{args.q_topk} + remainder" if sparse is not None
+                   "prefix_tokens": run.kv_tokens, "hip_graph": bool(run.graph) and run.sparse is None,
+                   "q_payload": (f"sparse top-{args.q_topk} + remainder" if run.sparse is not None
                                  else "dense fp32 rows"),
-                   "q_payload_bytes_per_step": (nd_all * (args.q_topk * 8 + 4) if sparse is not None
+                   "q_payload_bytes_per_step": (nd_all * (args.q_topk * 8 + 4) if run.sparse is not None
                                                 else nd_all * m.vocab * 4),
-                   "streams": len(streams)},
+                   "streams": len(run.streams)},
         "verified_tokens_per_s": round(verified_step / (ms_step / 1e3), 1),
         "accepted_per_step": acc_step,
         "step_hbm_floor_ms": round(step_bytes / (HBM_PEAK_GBS * 1e9) * 1e3, 3),
@@ -299,12 +325,33 @@ def main():
     }
     if breakdown is not None:
         result["breakdown_ms"] = breakdown
-    if args.mode == "stochastic" and not args.no_greedy:
-        result["greedy"] = greedy_run(v, w, batches, dev_in, step_args=(streams, nb), steps=args.steps,
-                                      warmup=args.warmup, torch=torch, graph=bool(args.graph))
+    if args.mode == "stochastic" and not args.no_greedy and "greedy" in w.modes:
+        result["greedy"] = greedy_run(run, args.steps, args.warmup)
+    cpu_batch = batches[0]
+    run.close()
+    del run
+
+    extras = [x for x in args.extra.split(",") if x and x != "none" and x != args.workload]
+    if extras:
+        result["workloads"] = {}
+    for name in extras:
+        r = Run(name, args, torch)
+        ms_x, acc_x, per_x = r.time(args.steps, args.warmup)
+        rec = {"value": round(acc_x / (ms_x / 1e3), 2), "unit": "tokens/s", "ms_per_step": round(ms_x, 4),
+               "ms_per_step_p10_p50_p90": [round(float(np.percentile(per_x, q)), 4) for q in (10, 50, 90)],
+               "accepted_per_step": acc_x, "verified_tokens_per_step": r.verified_step,
+               "verified_tokens_per_s": round(r.verified_step / (ms_x / 1e3), 1),
+               "users": int(r.w.n_users), "batches": r.nb, "prefix_tokens": r.kv_tokens,
+               "hip_graph": bool(r.graph), "streams": len(r.streams), "mode": "stochastic"}
+        log(f"{name}: {ms_x:.3f} ms/step, {acc_x:.1f} accepted / {r.verified_step} verified tokens per step")
+        if not args.no_greedy and "greedy" in r.w.modes:
+            rec["greedy"] = greedy_run(r, args.steps, args.warmup)
+        result["workloads"][name] = rec
+        r.close()
+        del r
+
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(w, batches[0], args.cpu_layers, acc_step / verified_step)
-    v.close()
+        result["cpu_baseline"] = cpu_baseline(w, cpu_batch, args.cpu_layers, acc_step / verified_step)
     print(json.dumps(result), flush=True)
 
 
@@ -328,35 +375,15 @@ def measured_traffic(workload):
     return int(m.group(1))
 
 
-def greedy_run(v, w, batches, dev_in, step_args, steps, warmup, torch, graph):
+def greedy_run(run, steps, warmup):
     """The same workload in greedy mode (accept iff the draft is the
     target's argmax), with drafts planted to follow the target's own argmax
     for k_m ~ U{0..l_m} steps; timed like the stochastic run."""
-    streams, nb = step_args
-    plant_greedy_drafts(v, w, batches, dev_in, torch)
-
-    def step():
-        for n in range(nb):
-            d, q, au = dev_in[n]
-            v.verify(n, w.assign, w.draft_len, d, q, "greedy", seed=w.seed, round_=0,
-                     stream=streams[n % len(streams)], graph=graph)
-        acc = 0
-        for n in range(nb):
-            n_acc, _ = v.accept(n, w.n_users)
-            acc += int((n_acc[batches[n].users] + 1).sum())
-        return acc
-
-    for _ in range(warmup):
-        step()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    accepted = 0
-    for _ in range(steps):
-        accepted += step()
-    torch.cuda.synchronize()
-    ms_step = 1e3 * (time.perf_counter() - t0) / steps
-    return {"value": round(accepted / steps / (ms_step / 1e3), 2), "unit": "tokens/s",
-            "ms_per_step": round(ms_step, 4), "accepted_per_step": accepted / steps,
+    plant_greedy_drafts(run.v, run.w, run.batches, run.dev_in, run.torch)
+    ms_step, acc_step, _ = run.time(steps, warmup, mode="greedy")
+    log(f"{run.name} greedy: {ms_step:.3f} ms/step, {acc_step:.1f} accepted per step")
+    return {"value": round(acc_step / (ms_step / 1e3), 2), "unit": "tokens/s",
+            "ms_per_step": round(ms_step, 4), "accepted_per_step": acc_step,
             "drafts": "first k_m drafts follow the target's argmax, k_m ~ U{0..l_m}"}
 
 
@@ -386,16 +413,30 @@ def plant_greedy_drafts(v, w, batches, dev_in, torch):
         b.drafts = drafts
 
 
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, b, n_layers_sample, acc_per_verified):
     """The oracle on the host cores: every user of the batch through
     n_layers_sample decoder layers, plus lm_head and the sampler, timed with
-    weight generation excluded; the per-layer time is extrapolated to all
-    layers (users are independent and every layer costs the same)."""
+    weight generation excluded (and reported); the per-layer time is
+    extrapolated to all layers (users are independent and every layer costs
+    the same)."""
     import oracle
     m = w.model
-    threads = int(os.environ.get("OMP_NUM_THREADS") or os.cpu_count() or 1)
+    threads = oracle.omp_threads()
+    t0 = time.perf_counter()
     ws = oracle.WeightSource(m, w.seed)
     layers = {l: ws.layer(l) for l in range(n_layers_sample)}
+    t_gen = time.perf_counter() - t0
 
     class Cached(oracle.WeightSource):
         def __init__(self):
@@ -425,12 +466,15 @@ def cpu_baseline(w, b, n_layers_sample, acc_per_verified):
     slots = int(n.sum())
     cpu_tok_s = slots * acc_per_verified / per_batch
     return {"value": round(cpu_tok_s, 4), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "cpu_model": _cpu_model(), "omp_threads": threads, "host_cpus": os.cpu_count(),
+            "weight_generation_s": round(t_gen, 2), "per_batch_s_extrapolated": round(per_batch, 2),
             "sample": (f"all {len(users)} users of the batch ({slots} query slots, prefixes "
                        f"{int(P.min())}-{int(P.max())}): {n_layers_sample} of {m.n_layers} decoder layers "
                        f"timed ({t_layer:.2f} s/layer), lm_head {t_head:.2f} s and sampler {t_samp:.2f} s "
-                       f"timed ({t_fwd + t_head + t_samp:.1f} s of CPU work), extrapolated to "
-                       f"{per_batch:.1f} s per batch; accepted = verified x {acc_per_verified:.3f} "
-                       f"(the GPU run's ratio); weight generation excluded")}
+                       f"timed ({t_fwd + t_head + t_samp:.1f} s of CPU work on {threads} OpenMP threads), "
+                       f"extrapolated to {per_batch:.1f} s per batch; accepted = verified x "
+                       f"{acc_per_verified:.3f} (the GPU run's ratio); weight generation "
+                       f"({t_gen:.1f} s for {n_layers_sample} layers) excluded")}
 
 
 if __name__ == "__main__":

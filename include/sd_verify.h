@@ -164,12 +164,17 @@ sd_status sd_user_state(sd_ctx* ctx, int32_t user, int32_t* prefix_len, int32_t*
 /* Copy keys/values of positions pos0..pos0+n-1 of `user`, layer `layer`, into
  * the paged cache.  k, v: device [n][n_kv_heads][head_dim] in dtype (k after
  * QK-norm and RoPE, as the forward stores it).  Requires pos0 + n <= the
- * user's prefix_len.  Enqueued on `stream`. */
+ * user's prefix_len.  Enqueued on `stream` without waiting: the page ids
+ * travel in the kernel arguments (one launch per 256 pages), so back-to-back
+ * writes need no host synchronisation and the call can be captured into a
+ * graph.  The page mapping is the one at the time of the call; the data must
+ * stay valid until the stream reaches the copy. */
 sd_status sd_kv_write(sd_ctx* ctx, int32_t user, int32_t layer, int32_t pos0, int32_t n,
                       const void* k, const void* v, sd_stream stream);
 
 /* Inverse of sd_kv_write (for tests): k, v device [n][n_kv_heads][head_dim];
- * positions may reach prefix_len + l_m + 1 of the user's pending batch. */
+ * positions may reach prefix_len + l_m + 1 of the user's pending batch.
+ * Enqueued on `stream` without waiting, like sd_kv_write. */
 sd_status sd_kv_read(sd_ctx* ctx, int32_t user, int32_t layer, int32_t pos0, int32_t n,
                      void* k, void* v, sd_stream stream);
 

@@ -95,6 +95,7 @@ def lib():
                                  _LAYER_FN, _KV_FN, vp, vp, vp, vp]
         L.or_sample.argtypes = [i32, i32, vp, vp, ctypes.c_int64, vp, vp, vp, vp, u64, u64,
                                 vp, vp, vp, vp, vp, vp]
+        L.or_omp_threads.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -109,6 +110,11 @@ def _p(a: Optional[np.ndarray]):
 # ----------------------------------------------------------------------------
 # primitives (exposed for the pins)
 # ----------------------------------------------------------------------------
+
+def omp_threads() -> int:
+    """Threads the oracle's OpenMP loops use."""
+    return int(lib().or_omp_threads())
+
 
 def philox4x64_10(ctr, key) -> np.ndarray:
     c = np.asarray(ctr, dtype=np.uint64).copy()

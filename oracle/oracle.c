@@ -36,9 +36,13 @@
  * written here from the paper's definition.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+
+/* threads the OpenMP loops of this file run on */
+int or_omp_threads(void) { return omp_get_max_threads(); }
 
 /* ------------------------------------------------------------------ */
 /* Philox-4x64-10                                                      */

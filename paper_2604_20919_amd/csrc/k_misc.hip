@@ -507,16 +507,19 @@ void launch_qkv_finish(const Dims& D, const BatchView& bv, const SlotBufs& sb, c
 }
 
 // ---------------------------------------------------------------------------
-// KV copy between a caller buffer [n][hkv][hd] and one user's pages
+// KV copy between a caller buffer [n][hkv][hd] and one user's pages.  The
+// pages of one launch travel in its kernel arguments (at most kKVCopyPages
+// of them, starting at the user's page index page0), so a copy needs no
+// device staging buffer and no host wait.
 // ---------------------------------------------------------------------------
 template <typename TA>
-__global__ void k_kv_copy(KVPool kv, const int32_t* pages, int layer, int pos0, int n, TA* k,
+__global__ void k_kv_copy(KVPool kv, KVCopyPages pages, int layer, int pos0, int n, TA* k,
                           TA* v, int to_pool) {
     const int i = blockIdx.x, g = blockIdx.y;
     if (i >= n) return;
     const int hd = kv.hd, hkv = kv.hkv;
     const int pos = pos0 + i;
-    const int page = pages[pos / kPageTokens], off = pos % kPageTokens;
+    const int page = pages.id[pos / kPageTokens - pages.page0], off = pos % kPageTokens;
     TA* base = (TA*)kv.base;
     TA* kp = base + kv.k_off(layer, page, g) + (size_t)off * hd;
     TA* vp = base + kv.v_off(layer, page, g);
@@ -533,14 +536,14 @@ __global__ void k_kv_copy(KVPool kv, const int32_t* pages, int layer, int pos0, 
     }
 }
 
-void launch_kv_copy(const Dims& D, const KVPool& kv, const int32_t* pages_dev, int layer,
+void launch_kv_copy(const Dims& D, const KVPool& kv, const KVCopyPages& pages, int layer,
                     int pos0, int n, const void* k, const void* v, int to_pool, hipStream_t s) {
     if (n <= 0) return;
     if (D.bf16)
-        hipLaunchKernelGGL(k_kv_copy<bf16_t>, dim3(n, D.hkv), dim3(128), 0, s, kv, pages_dev,
+        hipLaunchKernelGGL(k_kv_copy<bf16_t>, dim3(n, D.hkv), dim3(128), 0, s, kv, pages,
                            layer, pos0, n, (bf16_t*)k, (bf16_t*)v, to_pool);
     else
-        hipLaunchKernelGGL(k_kv_copy<float>, dim3(n, D.hkv), dim3(128), 0, s, kv, pages_dev, layer,
+        hipLaunchKernelGGL(k_kv_copy<float>, dim3(n, D.hkv), dim3(128), 0, s, kv, pages, layer,
                            pos0, n, (float*)k, (float*)v, to_pool);
 }
 

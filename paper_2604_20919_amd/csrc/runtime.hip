@@ -42,7 +42,7 @@ struct Layout {
     size_t gpart_floats;
     int nsq;
     // global region after the slots
-    size_t kvw_pages, total;
+    size_t total;
     int max_pages, max_items, rows_max, Tmax, Bmax;
 };
 
@@ -147,8 +147,7 @@ Layout plan(const sd_config& c) {
     L.spartB = take((size_t)L.Bmax * kVocabChunks * 4 * 4);
     L.result = take((size_t)(2 * L.Bmax + 4) * 4);
     L.slot_bytes = s;
-    L.kvw_pages = L.slot_bytes * (size_t)c.max_pending;
-    L.total = align_up(L.kvw_pages + (size_t)L.max_pages * 4);
+    L.total = align_up(L.slot_bytes * (size_t)c.max_pending);
     return L;
 }
 
@@ -212,7 +211,6 @@ struct sd_ctx {
     std::vector<User> users;
     std::vector<int> free_pages;  // stack: back is allocated first
     Slot slots[kMaxPending];
-    int32_t* kvw_host = nullptr;  // pinned page list for kv copies
     int device = 0;
     int attn_cap = 512;  // attention work items that run in one wave of workgroups
     // diagnostic timing of one kernel class
@@ -634,8 +632,6 @@ sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_poo
         b.result = (int32_t*)(s.base + L.result);
         b.bmax = L.Bmax;
     }
-    ok = ok && hipHostMalloc((void**)&c->kvw_host, (size_t)L.max_pages * 4, hipHostMallocDefault) ==
-                   hipSuccess;
     if (ok) {
         // The attention kernel reads whole 32-token blocks and multiplies the
         // value rows past a user's context by an exact 0; zeroing the pool
@@ -684,7 +680,6 @@ sd_status sd_verify_destroy(sd_ctx* c) {
         if (s.stage_host) (void)hipHostFree(s.stage_host);
         if (s.result_host) (void)hipHostFree(s.result_host);
     }
-    if (c->kvw_host) (void)hipHostFree(c->kvw_host);
     for (hipEvent_t e : c->prof_ev) (void)hipEventDestroy(e);
     delete c;
     return SD_OK;
@@ -740,14 +735,21 @@ static sd_status kv_copy(sd_ctx* c, int32_t user, int32_t layer, int32_t pos0, i
     if (n == 0) return SD_OK;
     if (to_pool && u.pending_slot >= 0) return SD_ESTATE;
     hipStream_t st = (hipStream_t)stream;
-    const int np = (int)u.pages.size();
-    std::memcpy(c->kvw_host, u.pages.data(), (size_t)np * 4);
-    int32_t* dev_pages = (int32_t*)(c->ws + c->lay.kvw_pages);
-    SD_HIP(hipMemcpyAsync(dev_pages, c->kvw_host, (size_t)np * 4, hipMemcpyHostToDevice, st));
-    launch_kv_copy(c->D, c->kv, dev_pages, layer, pos0, n, k, v, to_pool, st);
-    SD_HIP(hipGetLastError());
-    // the page list buffers are reused by the next call
-    SD_HIP(hipStreamSynchronize(st));
+    // one launch per kKVCopyPages pages; the page ids ride in the kernel
+    // arguments, so nothing is staged and the call does not wait
+    const size_t row = (size_t)c->D.hkv * c->D.hd * (c->D.bf16 ? 2 : 4);
+    const int end = pos0 + n;
+    for (int p0 = pos0; p0 < end;) {
+        KVCopyPages pg;
+        pg.page0 = p0 / kPageTokens;
+        const int pmax = std::min((int)u.pages.size(), pg.page0 + kKVCopyPages);
+        for (int j = pg.page0; j < pmax; ++j) pg.id[j - pg.page0] = u.pages[j];
+        const int p1 = std::min(end, pmax * kPageTokens);
+        launch_kv_copy(c->D, c->kv, pg, layer, p0, p1 - p0, (const char*)k + (size_t)(p0 - pos0) * row,
+                       (const char*)v + (size_t)(p0 - pos0) * row, to_pool, st);
+        SD_HIP(hipGetLastError());
+        p0 = p1;
+    }
     return SD_OK;
 }
 

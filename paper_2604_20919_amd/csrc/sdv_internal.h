@@ -158,7 +158,15 @@ void launch_sampler(const Dims& D, const BatchView& bv, const SlotBufs& sb, cons
 void launch_probs(const Dims& D, const BatchView& bv, const SlotBufs& sb, const float* logits,
                   float* probs, hipStream_t s);
 
-void launch_kv_copy(const Dims& D, const KVPool& kv, const int32_t* pages_dev, int layer,
+// Page ids of one KV copy launch: pages page0 .. page0 + kKVCopyPages - 1
+// of a user (a by-value kernel argument of 1 KB).
+constexpr int kKVCopyPages = 256;
+struct KVCopyPages {
+    int32_t page0;
+    int32_t id[kKVCopyPages];
+};
+
+void launch_kv_copy(const Dims& D, const KVPool& kv, const KVCopyPages& pages, int layer,
                     int pos0, int n, const void* k, const void* v, int to_pool, hipStream_t s);
 
 }  // namespace sdv

@@ -1,15 +1,23 @@
 """Parity at the benchmark sizes.
 
 The Qwen3-32B-shaped workloads (16-user batch, 32-user ragged batch, four
-pipelined 16-user batches) run through the C ABI exactly as the benchmark
-runs them; the oracle recomputes sampled users one by one (users are
-independent, so a user's logits and decisions do not depend on the rest of
-its batch).  All 32B workloads are drawn with one seed (their shapes and
-distributions are the benchmark's; the draws differ from the benchmark's
-own seeds) so that the host generates the 64 layers once for the oracle.  The Qwen3-1.7B-shaped batch is
-compared in full.  Properties that hold at any size (q = p accepts every
-draft; planted greedy prefixes; run-to-run bit identity) are checked on the
-whole 32B batch.
+pipelined 16-user batches, plus two batches at 40 and 88 slots) run through
+the C ABI exactly as the benchmark runs them, and the oracle recomputes
+users one by one (users are independent, so a user's logits and decisions
+do not depend on the rest of its batch):
+  * the 16-user batch: every user, in stochastic and in greedy mode;
+  * ragged batches: for every GEMM slot tile (16 slots below 97, 32 above)
+    the user holding its first slot, plus the users with the shortest and
+    the longest context (one attention chunk against several) and the most
+    drafts;
+  * the pipelined batches: the user with most slots in the first batch and
+    the one with the longest prefix in the last.
+All 32B workloads are drawn with one seed (their shapes and distributions
+are the benchmark's; the draws differ from the benchmark's own seeds) so
+that the host generates the 64 layers once for the oracle.  The
+Qwen3-1.7B-shaped batch is compared in full.  Properties that hold at any
+size (q = p accepts every draft; planted greedy prefixes; run-to-run bit
+identity) are checked on the whole 32B batch.
 """
 import dataclasses
 
@@ -19,7 +27,7 @@ import torch
 
 import oracle
 import workload as wl
-from gpu_harness import compare_decisions, load_synthetic_kv, logit_rel_err, make_verifier
+from gpu_harness import assert_decisions, compare_decisions, load_synthetic_kv, logit_rel_err, make_verifier
 from workload.device import DeviceWeights, batch_to_device
 
 pytestmark = pytest.mark.gpu
@@ -35,12 +43,13 @@ CUSTOM32 = {
     "qwen3-32b-t40": ([100 + 37 * i for i in range(8)], [4] * 8),
     "qwen3-32b-t88": ([64 + 23 * i for i in range(16)], [4, 5] * 8),
 }
+MODES32 = {"qwen3-32b-b16": ("stochastic", "greedy")}
 TOL = 2e-2
 
 
 @dataclasses.dataclass
 class Sampled:
-    """GPU results of one sampled user plus what the oracle needs."""
+    """GPU results of one user plus what the oracle needs."""
     workload: str
     user: int
     prefix: int
@@ -50,26 +59,25 @@ class Sampled:
     q: np.ndarray
     accept_u: object
     logits: np.ndarray      # GPU logits [L+1][V]
-    n_acc: int
-    token: int
+    decisions: dict         # mode -> (n_acc, token)
 
 
 def _pick(w: wl.Workload, n: int, b: wl.Batch):
-    """Indices (within batch n) of the users the oracle recomputes: both ends
-    of a uniform batch; the user with most slots and the one with the
-    longest prefix of a ragged batch; of the pipelined batches, the user
-    with most slots in the first and the one with the longest prefix in the
-    last."""
+    """Indices (within batch n) of the users the oracle recomputes."""
     if w.n_batches > 1:
         if n == 0:
             return [int(np.argmax(b.draft_len))]
         return [int(np.argmax(b.prefix_len))] if n == w.n_batches - 1 else []
     if np.all(b.draft_len == b.draft_len[0]) and np.all(b.prefix_len == b.prefix_len[0]):
-        return [0, len(b.users) - 1]
-    return sorted({int(np.argmax(b.draft_len)), int(np.argmax(b.prefix_len))})
+        return list(range(len(b.users)))
+    tile = 16 if b.T < 97 else 32
+    so = np.concatenate([[0], np.cumsum(b.n_slots)])
+    first = [int(np.searchsorted(so, t0, side="right") - 1) for t0 in range(0, b.T, tile)]
+    ctx = b.prefix_len + b.n_slots
+    return sorted(set(first) | {int(np.argmin(ctx)), int(np.argmax(ctx)), int(np.argmax(b.draft_len))})
 
 
-def _run_workload(name, dw, mode="stochastic"):
+def _run_workload(name, dw):
     if name in CUSTOM32:
         w = wl.custom_workload("qwen3-32b", *CUSTOM32[name], seed=SEED32)
     else:
@@ -83,29 +91,44 @@ def _run_workload(name, dw, mode="stochastic"):
         for i, u in enumerate(b.users):
             v.reset_user(int(u), int(b.prefix_len[i]), int(b.root[i]))
     torch.cuda.synchronize()
-    # all batches in flight on alternating streams, as the benchmark runs them
-    for n in range(w.n_batches):
-        d, q, au = dev[n]
-        v.verify(n, w.assign, w.draft_len, d, q, mode, seed=w.seed, round_=0, accept_u=au,
-                 stream=streams[n % len(streams)])
-    torch.cuda.synchronize()
-    out = []
-    for n, b in enumerate(batches):
-        lg = v.logits(n, b.T).cpu().numpy()
-        n_acc, tok = v.accept(n, w.n_users)
-        so = np.concatenate([[0], np.cumsum(b.n_slots)])
-        do = np.concatenate([[0], np.cumsum(b.draft_len)])
-        for i in _pick(w, n, b):
-            u, L = int(b.users[i]), int(b.draft_len[i])
-            out.append(Sampled(
-                name, u, int(b.prefix_len[i]), L,
-                b.slot_tokens()[so[i]:so[i + 1]], b.drafts[do[i]:do[i + 1]], b.q[do[i]:do[i + 1]],
-                None if b.accept_u is None else b.accept_u[do[i]:do[i + 1]],
-                lg[so[i]:so[i + 1]].copy(), int(n_acc[u]), int(tok[u])))
+    out = {}
+    for mode in MODES32.get(name, ("stochastic",)):
+        # all batches in flight on alternating streams, as the benchmark runs them
+        for n in range(w.n_batches):
+            d, q, au = dev[n]
+            v.verify(n, w.assign, w.draft_len, d, q, mode, seed=w.seed, round_=0, accept_u=au,
+                     stream=streams[n % len(streams)])
+        torch.cuda.synchronize()
+        for n, b in enumerate(batches):
+            lg = v.logits(n, b.T).cpu().numpy()
+            n_acc, tok = v.accept(n, w.n_users)
+            so = np.concatenate([[0], np.cumsum(b.n_slots)])
+            do = np.concatenate([[0], np.cumsum(b.draft_len)])
+            for i in _pick(w, n, b):
+                u, L = int(b.users[i]), int(b.draft_len[i])
+                if u not in out:
+                    out[u] = Sampled(
+                        name, u, int(b.prefix_len[i]), L,
+                        b.slot_tokens()[so[i]:so[i + 1]], b.drafts[do[i]:do[i + 1]], b.q[do[i]:do[i + 1]],
+                        None if b.accept_u is None else b.accept_u[do[i]:do[i + 1]],
+                        lg[so[i]:so[i + 1]].copy(), {})
+                else:  # logits do not depend on the mode
+                    assert np.array_equal(out[u].logits, lg[so[i]:so[i + 1]])
+                out[u].decisions[mode] = (int(n_acc[u]), int(tok[u]))
     v.close()
     del v, dev
     torch.cuda.empty_cache()
-    return w, out
+    return w, list(out.values())
+
+
+class _Progress(oracle.WeightSource):
+    """The seeded weights, with a progress line every eight layers (the
+    host forward over every compared user takes minutes)."""
+
+    def layer(self, l):
+        if l % 8 == 0:
+            print(f"oracle layer {l}/{self.m.n_layers}", flush=True)
+        return super().layer(l)
 
 
 @pytest.fixture(scope="module")
@@ -123,39 +146,39 @@ def results32():
     # one oracle pass over every sampled user (each with its own prefix)
     users = [s.user for s in samples]
     prefix = [s.prefix for s in samples]
+    print(f"oracle forward over {len(samples)} users, {sum(s.L + 1 for s in samples)} slots", flush=True)
     kv = oracle.KVSource(m, SEED32, users, prefix)
-    ref = oracle.forward(m, oracle.WeightSource(m, SEED32), kv, prefix, [s.L + 1 for s in samples],
+    ref = oracle.forward(m, _Progress(m, SEED32), kv, prefix, [s.L + 1 for s in samples],
                          np.concatenate([s.tokens for s in samples]))
     print("oracle forward done", flush=True)
     return samples, ref, seeds
 
 
-def _compare(samples, ref_logits, seed, label):
-    off = np.concatenate([[0], np.cumsum([s.L + 1 for s in samples])])
-    worst = 0.0
-    for k, s in enumerate(samples):
-        rl = ref_logits[off[k]:off[k + 1]]
-        err = logit_rel_err(s.logits, rl)
-        worst = max(worst, float(err.max()))
-        assert err.max() < TOL, f"{label} user {s.user}: logit error {err.max()}"
-        res = oracle.sample("stochastic", [s.user], [s.L], rl, s.drafts, s.q, s.accept_u, seed, 0)
-        extra = np.expm1(2.0 * np.array([float(np.max(np.abs(s.logits - rl)))]))
-        bad, border = compare_decisions([s.n_acc], [s.token], res, [s.L], extra=extra)
-        print(f"{label} user {s.user} (prefix {s.prefix}, l {s.L}): rel err {err.max():.2e}, "
-              f"n_acc {s.n_acc}/{res['n_acc'][0]}, token {s.token}/{res['token'][0]}, "
-              f"mismatch {bad}, borderline {border}")
-        assert bad == 0
-    return worst
-
-
 @pytest.mark.parametrize("name", WORKLOADS32 + tuple(CUSTOM32))
-def test_qwen3_32b_sampled_users_match_oracle(results32, name):
+def test_qwen3_32b_users_match_oracle(results32, name):
+    """Logits of every compared user within the bf16 bar; decisions of every
+    mode run bit-exact with the oracle's except counted borderline cases
+    (at most 1% of the decisions)."""
     samples, ref, seeds = results32
     off = np.concatenate([[0], np.cumsum([s.L + 1 for s in samples])])
     mine = [k for k, s in enumerate(samples) if s.workload == name]
     assert mine
-    rows = np.concatenate([np.arange(off[k], off[k + 1]) for k in mine])
-    _compare([samples[k] for k in mine], ref[rows], seeds[name], name)
+    gl = np.concatenate([samples[k].logits for k in mine])
+    rl = np.concatenate([ref[off[k]:off[k + 1]] for k in mine])
+    err = logit_rel_err(gl, rl)
+    print(f"{name}: {len(mine)} users, logit rel err max {err.max():.3e} mean {err.mean():.3e}")
+    assert err.max() < TOL, f"{name}: logit error {err.max()}"
+    users = [samples[k].user for k in mine]
+    Ls = [samples[k].L for k in mine]
+    drafts = np.concatenate([samples[k].drafts for k in mine])
+    q = np.concatenate([samples[k].q for k in mine])
+    au = None if samples[mine[0]].accept_u is None else np.concatenate([samples[k].accept_u for k in mine])
+    for mode in MODES32.get(name, ("stochastic",)):
+        res = oracle.sample(mode, users, Ls, rl, drafts, q, au, seeds[name], 0)
+        ga = [samples[k].decisions[mode][0] for k in mine]
+        gt = [samples[k].decisions[mode][1] for k in mine]
+        chk = compare_decisions(ga, gt, res, Ls, mode, drafts, gl, rl)
+        assert_decisions(chk, f"{name}/{mode}", end_to_end=True)
 
 
 def test_qwen3_1p7b_full_batch_matches_oracle():
@@ -181,15 +204,8 @@ def test_qwen3_1p7b_full_batch_matches_oracle():
     print(f"qwen3-1.7b-b8: logit rel err max {err.max():.3e} mean {err.mean():.3e}")
     assert err.max() < TOL
     res = oracle.sample("stochastic", b.users, b.draft_len, ref, b.drafts, b.q, b.accept_u, w.seed, 0)
-    per_user = []
-    o = 0
-    for n in b.n_slots:
-        per_user.append(float(np.max(np.abs(lg[o:o + n] - ref[o:o + n]))))
-        o += int(n)
-    bad, border = compare_decisions(n_acc[b.users], tok[b.users], res, b.draft_len,
-                                    extra=np.expm1(2.0 * np.array(per_user)))
-    print(f"qwen3-1.7b-b8: decision mismatches {bad}, borderline {border}")
-    assert bad == 0
+    chk = compare_decisions(n_acc[b.users], tok[b.users], res, b.draft_len, "stochastic", b.drafts, lg, ref)
+    assert_decisions(chk, "qwen3-1.7b-b8", end_to_end=True)
 
 
 @pytest.fixture(scope="module")

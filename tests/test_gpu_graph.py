@@ -13,7 +13,7 @@ import pytest
 import torch
 
 import workload as wl
-from gpu_harness import compare_decisions, load_synthetic_kv, logit_rel_err, make_verifier, run_oracle
+from gpu_harness import assert_decisions, compare_decisions, load_synthetic_kv, logit_rel_err, make_verifier, run_oracle
 from workload.device import DeviceWeights, batch_to_device
 
 pytestmark = pytest.mark.gpu
@@ -61,9 +61,8 @@ def test_graph_replays_match_eager(mode):
     rl, oref = run_oracle(w, b, mode, seed=5)
     err = float(logit_rel_err(ref[2], rl).max())
     assert err < 2e-2, err
-    extra = np.expm1(2.0 * np.abs(ref[2] - rl).max())
-    bad, _ = compare_decisions(ref[0], ref[1], oref, b.draft_len, extra=np.full(len(b.users), extra))
-    assert bad == 0
+    assert_decisions(compare_decisions(ref[0], ref[1], oref, b.draft_len, mode, b.drafts, ref[2], rl),
+                     f"graph pass/{mode}", end_to_end=True)
     v.close()
 
 

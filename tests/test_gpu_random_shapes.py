@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 import workload as wl
-from gpu_harness import compare_decisions, load_synthetic_kv, logit_rel_err, make_verifier, run_gpu, run_oracle
+from gpu_harness import assert_decisions, compare_decisions, load_synthetic_kv, logit_rel_err, make_verifier, run_gpu, run_oracle
 from workload.device import DeviceWeights
 
 pytestmark = pytest.mark.gpu
@@ -42,13 +42,8 @@ def test_random_ragged_shapes_match_oracle(seed):
     label = f"seed {seed}: users {b.users.tolist()} prefix {b.prefix_len.tolist()} L {b.draft_len.tolist()} {mode}"
     print(f"{label}: logit rel err {err.max():.2e}")
     assert err.max() < 2e-2, label
-    per_user, o = [], 0
-    for n in b.n_slots:
-        per_user.append(float(np.max(np.abs(gpu.logits[o:o + n] - rl[o:o + n]))))
-        o += int(n)
-    extra = np.expm1(2.0 * np.asarray(per_user))
-    bad, border = compare_decisions(gpu.n_acc, gpu.token, ref, b.draft_len, extra=extra)
-    assert bad == 0, label
+    chk = compare_decisions(gpu.n_acc, gpu.token, ref, b.draft_len, mode, b.drafts, gpu.logits, rl)
+    assert_decisions(chk, label, end_to_end=True)
     if mode == "force":
         assert np.array_equal(gpu.n_acc, b.draft_len)
     v.close()

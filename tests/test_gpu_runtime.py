@@ -170,3 +170,50 @@ def test_misaligned_gain_pointers_are_rejected():
     # the aligned pointers still initialise
     Verifier(w.model, layer_ptrs(dw), n_pages=16, max_users=w.n_users, max_draft=4,
              max_batch_users=w.n_users, max_batch_tokens=16, max_ctx=64, max_pending=1).close()
+
+
+def test_kv_writes_back_to_back_without_host_sync():
+    """sd_kv_write and sd_kv_read enqueue without waiting: several writes of
+    one user on one stream, issued back to back with no host synchronisation
+    (pieces that start and end inside pages, a piece spanning more pages than
+    one launch carries, overwrites of earlier pieces), then reads of the same
+    ranges on the same stream; after one final synchronisation every entry
+    holds the last value written to it."""
+    w = wl.custom_workload("tiny-bf16", [4700, 40], [1, 1], seed=73)
+    m = w.model
+    dw = DeviceWeights(m, w.seed)
+    P = int(w.prefix_len[0])
+    v = _verifier(w, dw, n_pages=(P + 15) // 16 + 16, max_ctx=P + 8)
+    v.reset_user(0, P, 1)
+    v.reset_user(1, 40, 1)
+    st = torch.cuda.Stream()
+    g = torch.Generator(device="cpu").manual_seed(5)
+    full_k = torch.randint(-2**15, 2**15, (P, m.n_kv_heads, m.head_dim), dtype=torch.int16, generator=g)
+    full_v = torch.randint(-2**15, 2**15, (P, m.n_kv_heads, m.head_dim), dtype=torch.int16, generator=g)
+    want_k, want_v = full_k.clone(), full_v.clone()
+    # (pos0, n): whole range (more than 256 pages: two launches), ragged pieces,
+    # an overwrite crossing the launch boundary at 4096 tokens
+    pieces = [(0, P), (3, 29), (17, 1), (4090, 13), (4700 - 5, 5), (100, 300)]
+    src = []
+    for i, (p0, n) in enumerate(pieces):
+        k = full_k[p0:p0 + n] if i == 0 else torch.randint(
+            -2**15, 2**15, (n, m.n_kv_heads, m.head_dim), dtype=torch.int16, generator=g)
+        vv = full_v[p0:p0 + n] if i == 0 else torch.randint(
+            -2**15, 2**15, (n, m.n_kv_heads, m.head_dim), dtype=torch.int16, generator=g)
+        want_k[p0:p0 + n] = k
+        want_v[p0:p0 + n] = vv
+        src.append((p0, k.cuda(), vv.cuda()))
+    outs = [(p0, n, torch.empty((n, m.n_kv_heads, m.head_dim), dtype=torch.int16, device="cuda"),
+             torch.empty((n, m.n_kv_heads, m.head_dim), dtype=torch.int16, device="cuda"))
+            for p0, n in [(0, P), (4080, 40), (0, 20)]]
+    torch.cuda.synchronize()
+    # nothing but library calls between here and the final synchronisation
+    for p0, kd, vd in src:
+        v.write_kv(0, 1, p0, kd, vd, stream=st)
+    for p0, n, kd, vd in outs:
+        v.read_kv(0, 1, p0, kd, vd, stream=st)
+    torch.cuda.synchronize()
+    for p0, n, kd, vd in outs:
+        assert torch.equal(kd.cpu(), want_k[p0:p0 + n]), (p0, n)
+        assert torch.equal(vd.cpu(), want_v[p0:p0 + n]), (p0, n)
+    v.close()

@@ -12,7 +12,7 @@ import torch
 
 import oracle
 import workload as wl
-from gpu_harness import compare_decisions
+from gpu_harness import assert_decisions, compare_decisions
 from paper_2604_20919_amd.verifier import Verifier
 
 pytestmark = pytest.mark.gpu
@@ -91,9 +91,10 @@ def test_sampler_matches_oracle(V, mode, with_u):
                  accept_u=dev(au))
         n_acc, tok = v.accept(0, M)
         ref = oracle.sample(mode, users, Ls, logits, drafts, q, au, seed, rep)
-        bad, border = compare_decisions(n_acc[users], tok[users], ref, Ls)
-        total_bad += bad
-        total_border += border
+        chk = compare_decisions(n_acc[users], tok[users], ref, Ls, mode)
+        assert_decisions(chk, f"V={V} {mode} u={with_u} rep {rep}", end_to_end=False)
+        total_bad += chk.bad
+        total_border += chk.border
         if mode == "force":
             assert np.array_equal(n_acc[users], np.asarray(Ls))
     print(f"V={V} mode={mode} accept_u={with_u}: mismatches={total_bad} borderline={total_border}")
