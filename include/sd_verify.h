@@ -44,7 +44,8 @@ enum {
     SD_ESTATE = -4,   /* call out of order (batch pending / not pending) */
     SD_EDEVICE = -5,  /* the GPU found bad input data (token id out of range) */
     SD_ENOTIMPL = -6, /* configuration not supported by this build */
-    SD_ENODEV = -7    /* no usable gfx950 device */
+    SD_ENODEV = -7,   /* no usable gfx950 device */
+    SD_ELIMIT = -8    /* input beyond the fixed limits of sd_sample_logits_noalloc */
 };
 
 enum { SD_F32 = 0, SD_BF16 = 1 };
@@ -323,6 +324,46 @@ sd_status sd_sample_logits(sd_ctx* ctx, int32_t batch, int32_t n_users, const in
  * [sum(l_m+1)][vocab]) into dst (device), ordered after the batch on
  * `stream`.  SD_ESTATE if the batch is not pending. */
 sd_status sd_debug_logits(sd_ctx* ctx, int32_t batch, float* dst, sd_stream stream);
+
+/*
+ * For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc: the
+ * accept/resample step of sd_sample_logits with no context, no workspace
+ * and no allocation of any kind.  Its scratch (batch tables, per-slot
+ * statistics, vocab-chunk partials) is a fixed array in the library's
+ * device memory, SD_NOALLOC_SCRATCH_BYTES on every GPU the library runs on,
+ * held until the process ends; the caller passes only inputs and outputs.
+ *   n_users:      B, 1..SD_NOALLOC_MAX_USERS users, in the order the rows
+ *                 below follow (any order; no user state is involved)
+ *   user_ids:     host [B], ids >= 0 that key the Philox draws (as the
+ *                 global user ids of sd_sample_logits do)
+ *   draft_len:    host [B], l_m >= 1; T = sum(l_m + 1) <= SD_NOALLOC_MAX_SLOTS
+ *   vocab:        V, 1..SD_NOALLOC_MAX_VOCAB
+ *   draft_tokens: device [sum l_m] int32, users in order
+ *   q:            device [sum l_m][V] fp32 (stochastic mode; else may be NULL)
+ *   logits:       device [T][V] fp32, rows user by user, slot 0 first
+ *   mode, seed, round, accept_u: as for sd_verify_batch
+ *   result:       device int32 [2*B + 1], written on `stream`: n_acc[B],
+ *                 then token[B], then a flag word (nonzero: a draft token
+ *                 was outside [0, V); n_acc and token are then undefined)
+ * Decisions and tokens are those of sd_sample_logits on the same inputs
+ * (the same kernels).  Asynchronous on `stream`; nothing waits.  Every call
+ * on a GPU uses that GPU's one scratch array, so calls that overlap on one
+ * GPU (two streams, two host threads) race and must be ordered by the
+ * caller.  The array keeps the last call's contents; everything a call
+ * reads from it is written earlier in the same call (the error flag is
+ * cleared by its first kernel).
+ * Errors (nothing enqueued): SD_EINVAL (bad argument), SD_ELIMIT (more
+ * users, slots or vocabulary than the fixed scratch holds), SD_EHIP.
+ */
+#define SD_NOALLOC_MAX_USERS 64
+#define SD_NOALLOC_MAX_SLOTS 1024
+#define SD_NOALLOC_MAX_VOCAB (1 << 20)
+#define SD_NOALLOC_SCRATCH_BYTES 1179648
+sd_status sd_sample_logits_noalloc(int32_t n_users, const int32_t* user_ids, const int32_t* draft_len,
+                                   int32_t vocab, const int32_t* draft_tokens, const float* q,
+                                   const float* logits, int32_t mode, uint64_t seed, uint64_t round,
+                                   const float* accept_u, int32_t* result, sd_stream stream);
 
 /* Kernel classes for sd_profile_begin. */
 enum {

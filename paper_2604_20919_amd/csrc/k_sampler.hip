@@ -312,6 +312,50 @@ void launch_probs(const Dims& D, const BatchView& bv, const SlotBufs& sb, const 
     hipLaunchKernelGGL(k_probs, dim3(blocks, bv.T), dim3(256), 0, s, bv, logits, sb.sstat, probs, D.V);
 }
 
+// Batch tables of the context-free sampler call, built on the device from
+// the kernel argument (nothing is copied from the host): user ids and draft
+// lengths as given, slot and draft offsets, the (user, slot) of every slot;
+// the error flags are cleared and every draft token is range-checked.  One
+// workgroup of 1024 threads.
+__global__ __launch_bounds__(1024) void k_noalloc_stage(NoallocMeta m, NoallocTables t,
+                                                        const int32_t* drafts) {
+    const int tid = threadIdx.x;
+    if (tid < m.B) {
+        t.user_id[tid] = m.user_id[tid];
+        t.L[tid] = m.L[tid];
+    }
+    if (tid == 0) {
+        int so = 0, dof = 0;
+        for (int b = 0; b < m.B; ++b) {
+            t.slot_off[b] = so;
+            t.draft_off[b] = dof;
+            so += m.L[b] + 1;
+            dof += m.L[b];
+        }
+        t.slot_off[m.B] = so;
+        t.draft_off[m.B] = dof;
+        *t.flags = 0;
+    }
+    __syncthreads();
+    const int T = t.slot_off[m.B], nd = t.draft_off[m.B];
+    for (int i = tid; i < T; i += blockDim.x) {
+        int b = 0;
+        while (t.slot_off[b + 1] <= i) ++b;
+        t.slot_b[i] = b;
+        t.slot_j[i] = i - t.slot_off[b];
+    }
+    __syncthreads();  // flags cleared above before any thread sets a bit
+    for (int i = tid; i < nd; i += blockDim.x) {
+        const int d = drafts[i];
+        if (d < 0 || d >= m.V) atomicOr(t.flags, 1);
+    }
+}
+
+void launch_noalloc_stage(const NoallocMeta& m, const NoallocTables& t, const int32_t* drafts,
+                          hipStream_t s) {
+    hipLaunchKernelGGL(k_noalloc_stage, dim3(1), dim3(1024), 0, s, m, t, drafts);
+}
+
 void launch_sampler(const Dims& D, const BatchView& bv, const SlotBufs& sb, const float* logits,
                     hipStream_t s) {
     SampP p;

@@ -11,6 +11,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -523,6 +524,50 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
 
 }  // namespace
 
+// ---------------------------------------------------------------------------
+// Scratch of sd_sample_logits_noalloc: one fixed array per GPU (each device
+// the library runs on holds its own copy until the process ends).  Layout:
+// the batch tables, then the sampler's per-slot statistics and vocab-chunk
+// partials, each section 256-byte aligned.  Host code never uses the name
+// `scratch` as an address: it takes the device address from
+// hipGetSymbolAddress, once per device, and passes that to the kernels.
+// ---------------------------------------------------------------------------
+namespace {
+constexpr size_t na_align(size_t x) { return (x + 255) & ~(size_t)255; }
+constexpr size_t kNaTables = na_align((size_t)(4 * kNoallocUsers + 2 + 2 * kNoallocSlots + 1) * 4);
+constexpr size_t kNaSstat = na_align((size_t)kNoallocSlots * 4 * 4);
+constexpr size_t kNaSpart = na_align((size_t)kNoallocSlots * kVocabChunks * 4 * 4);
+constexpr size_t kNaSpartB = na_align((size_t)kNoallocUsers * kVocabChunks * 4 * 4);
+constexpr size_t kNaBytes = kNaTables + kNaSstat + kNaSpart + kNaSpartB;
+static_assert(kNaBytes <= SD_NOALLOC_SCRATCH_BYTES, "scratch layout exceeds the declared size");
+static_assert(kNoallocUsers == SD_NOALLOC_MAX_USERS && kNoallocSlots == SD_NOALLOC_MAX_SLOTS,
+              "limits of the header and the kernels differ");
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[SD_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kNaMaxDevices = 64;
+std::mutex g_na_mutex;
+unsigned char* g_na_ptr[kNaMaxDevices] = {};
+
+// Device address of this GPU's scratch array (looked up on the first call
+// on the device, with that device current).
+sd_status na_scratch(unsigned char** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return SD_EHIP;
+    if (dev >= kNaMaxDevices) return SD_ENODEV;
+    std::lock_guard<std::mutex> lock(g_na_mutex);
+    if (!g_na_ptr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return SD_EHIP;
+        g_na_ptr[dev] = (unsigned char*)ptr;
+    }
+    *out = g_na_ptr[dev];
+    return SD_OK;
+}
+}  // namespace
+
 extern "C" {
 
 const char* sd_status_str(sd_status s) {
@@ -535,6 +580,7 @@ const char* sd_status_str(sd_status s) {
         case SD_EDEVICE: return "device reported bad input data";
         case SD_ENOTIMPL: return "configuration not supported";
         case SD_ENODEV: return "no gfx950 device";
+        case SD_ELIMIT: return "input exceeds the fixed limits of this call";
     }
     return "unknown status";
 }
@@ -1056,6 +1102,72 @@ sd_status sd_profile_end(sd_ctx* c, double* total_ms, int32_t* launches) {
     c->prof_class = 0;
     c->prof_used = 0;
     return SD_OK;
+}
+
+sd_status sd_sample_logits_noalloc(int32_t n_users, const int32_t* user_ids, const int32_t* draft_len,
+                                   int32_t vocab, const int32_t* draft_tokens, const float* q,
+                                   const float* logits, int32_t mode, uint64_t seed, uint64_t round,
+                                   const float* accept_u, int32_t* result, sd_stream stream) {
+    if (mode != SD_GREEDY && mode != SD_STOCHASTIC && mode != SD_FORCE) return SD_EINVAL;
+    if (n_users < 1 || !user_ids || !draft_len || !draft_tokens || !logits || !result || vocab < 1)
+        return SD_EINVAL;
+    if (mode == SD_STOCHASTIC && !q) return SD_EINVAL;
+    if (n_users > SD_NOALLOC_MAX_USERS || vocab > SD_NOALLOC_MAX_VOCAB) return SD_ELIMIT;
+    NoallocMeta meta;
+    meta.B = n_users;
+    meta.V = vocab;
+    int T = 0, nd = 0;
+    for (int b = 0; b < n_users; ++b) {
+        if (user_ids[b] < 0 || draft_len[b] < 1) return SD_EINVAL;
+        if (draft_len[b] >= SD_NOALLOC_MAX_SLOTS) return SD_ELIMIT;
+        meta.user_id[b] = user_ids[b];
+        meta.L[b] = draft_len[b];
+        T += draft_len[b] + 1;
+        nd += draft_len[b];
+        if (T > SD_NOALLOC_MAX_SLOTS) return SD_ELIMIT;
+    }
+    unsigned char* sp = nullptr;
+    sd_status r = na_scratch(&sp);
+    if (r != SD_OK) return r;
+    int32_t* tab = (int32_t*)sp;
+    NoallocTables t;
+    t.user_id = tab;
+    t.L = t.user_id + kNoallocUsers;
+    t.slot_off = t.L + kNoallocUsers;
+    t.draft_off = t.slot_off + kNoallocUsers + 1;
+    t.slot_b = t.draft_off + kNoallocUsers + 1;
+    t.slot_j = t.slot_b + kNoallocSlots;
+    t.flags = t.slot_j + kNoallocSlots;
+    BatchView bv{};
+    bv.B = n_users;
+    bv.T = T;
+    bv.nd = nd;
+    bv.mode = mode;
+    bv.seed = seed;
+    bv.round = round;
+    bv.user_id = t.user_id;
+    bv.L = t.L;
+    bv.slot_off = t.slot_off;
+    bv.draft_off = t.draft_off;
+    bv.slot_b = t.slot_b;
+    bv.slot_j = t.slot_j;
+    bv.drafts = draft_tokens;
+    bv.q = q;
+    bv.accept_u = accept_u;
+    bv.qk = 0;
+    bv.flags = t.flags;
+    SlotBufs sb{};
+    sb.sstat = (float*)(sp + kNaTables);
+    sb.spart = (float*)(sp + kNaTables + kNaSstat);
+    sb.spartB = (float*)(sp + kNaTables + kNaSstat + kNaSpart);
+    sb.result = result;  // the caller's output: n_acc [B], token [B], flags
+    sb.bmax = n_users;
+    Dims D{};
+    D.V = vocab;
+    hipStream_t st = (hipStream_t)stream;
+    launch_noalloc_stage(meta, t, draft_tokens, st);
+    launch_sampler(D, bv, sb, logits, st);
+    return hip_status(hipGetLastError());
 }
 
 }  // extern "C"

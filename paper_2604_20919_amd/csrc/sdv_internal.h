@@ -166,6 +166,20 @@ struct KVCopyPages {
     int32_t id[kKVCopyPages];
 };
 
+// Context-free sampler call: per-batch tables in a fixed scratch array.
+constexpr int kNoallocUsers = 64;
+constexpr int kNoallocSlots = 1024;
+struct NoallocMeta {  // kernel argument (520 bytes)
+    int32_t B, V;
+    int32_t user_id[kNoallocUsers];
+    int32_t L[kNoallocUsers];
+};
+struct NoallocTables {  // device pointers into the scratch array
+    int32_t *user_id, *L, *slot_off, *draft_off, *slot_b, *slot_j, *flags;
+};
+void launch_noalloc_stage(const NoallocMeta& m, const NoallocTables& t, const int32_t* drafts,
+                          hipStream_t s);
+
 void launch_kv_copy(const Dims& D, const KVPool& kv, const KVCopyPages& pages, int layer,
                     int pos0, int n, const void* k, const void* v, int to_pool, hipStream_t s);
 

@@ -16,15 +16,17 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libsdverify.so")
 
-SD_OK, SD_EINVAL, SD_ENOMEM, SD_EHIP, SD_ESTATE, SD_EDEVICE, SD_ENOTIMPL, SD_ENODEV = (
-    0, -1, -2, -3, -4, -5, -6, -7)
+SD_OK, SD_EINVAL, SD_ENOMEM, SD_EHIP, SD_ESTATE, SD_EDEVICE, SD_ENOTIMPL, SD_ENODEV, SD_ELIMIT = (
+    0, -1, -2, -3, -4, -5, -6, -7, -8)
+SD_NOALLOC_MAX_USERS, SD_NOALLOC_MAX_SLOTS, SD_NOALLOC_MAX_VOCAB = 64, 1024, 1 << 20
 SD_F32, SD_BF16 = 0, 1
 SD_GREEDY, SD_STOCHASTIC, SD_FORCE = 0, 1, 2
 MODES = {"greedy": SD_GREEDY, "stochastic": SD_STOCHASTIC, "force": SD_FORCE}
 
 EXPORTS = ("sd_verify_query_sizes", "sd_verify_init", "sd_verify_destroy", "sd_user_reset",
            "sd_user_release", "sd_user_state", "sd_kv_write", "sd_kv_read", "sd_verify_batch",
-           "sd_verify_batch_graph", "sd_verify_batch_sparse", "sd_draft_batch", "sd_accept", "sd_sample_logits", "sd_debug_logits", "sd_profile_begin", "sd_profile_end",
+           "sd_verify_batch_graph", "sd_verify_batch_sparse", "sd_draft_batch", "sd_accept", "sd_sample_logits",
+           "sd_sample_logits_noalloc", "sd_debug_logits", "sd_profile_begin", "sd_profile_end",
            "sd_calib_hbm", "sd_calib_mfma", "sd_status_str")
 SD_K_QKV, SD_K_ATTN, SD_K_O, SD_K_GATEUP, SD_K_DOWN, SD_K_LMHEAD, SD_K_SAMPLER, SD_K_SMALL = range(1, 9)
 
@@ -81,6 +83,7 @@ def lib() -> ctypes.CDLL:
                                              vp, vp]
         L.sd_accept.argtypes = [vp, i32, vp, vp, i32]
         L.sd_sample_logits.argtypes = [vp, i32, i32, vp, vp, vp, vp, vp, i32, u64, u64, vp, vp]
+        L.sd_sample_logits_noalloc.argtypes = [i32, vp, vp, i32, vp, vp, vp, i32, u64, u64, vp, vp, vp]
         L.sd_debug_logits.argtypes = [vp, i32, vp, vp]
         L.sd_profile_begin.argtypes = [vp, i32, i32]
         L.sd_profile_end.argtypes = [vp, P(ctypes.c_double), P(i32)]
@@ -220,6 +223,20 @@ def sd_sample_logits(ctx: int, batch: int, assign, draft_len, draft_tokens, q, l
     _check("sd_sample_logits", lib().sd_sample_logits(
         ctx, batch, a.size, a.ctypes.data, L.ctypes.data, _dev(draft_tokens), _dev(q), _dev(logits),
         mode, int(seed), int(round_), _dev(accept_u), _stream(stream)))
+
+
+def sd_sample_logits_noalloc(user_ids, draft_len, vocab: int, draft_tokens, q, logits, mode,
+                             result, seed: int = 0, round_: int = 0, accept_u=None,
+                             stream=None) -> None:
+    """Context-free accept/resample on caller logits; result: device int32
+    [2*B + 1] (n_acc, token, flag word), written asynchronously."""
+    u, L = _host_i32(user_ids), _host_i32(draft_len)
+    if u.size != L.size:
+        raise ValueError("user_ids and draft_len differ in length")
+    mode = MODES[mode] if isinstance(mode, str) else int(mode)
+    _check("sd_sample_logits_noalloc", lib().sd_sample_logits_noalloc(
+        u.size, u.ctypes.data, L.ctypes.data, int(vocab), _dev(draft_tokens), _dev(q), _dev(logits),
+        mode, int(seed), int(round_), _dev(accept_u), _dev(result), _stream(stream)))
 
 
 def sd_accept(ctx: int, batch: int, n_users: int, commit: bool = False):

@@ -93,3 +93,21 @@ def test_null_arguments_are_rejected_without_a_device():
     assert lib.sd_accept(None, 0, None, None, 0) == sv.SD_EINVAL
     assert lib.sd_verify_batch(None, 0, 1, None, None, None, None, 0, 0, 0, None, None) == sv.SD_EINVAL
     assert lib.sd_verify_destroy(None) == sv.SD_EINVAL
+
+
+def test_noalloc_limits_are_checked_before_any_device_call():
+    """sd_sample_logits_noalloc refuses arguments on the host, before it
+    looks up its scratch array or enqueues anything."""
+    lib = sv.lib()
+    u = (ctypes.c_int32 * 65)(*range(65))
+    L = (ctypes.c_int32 * 65)(*([1] * 65))
+    p = ctypes.c_void_p(16)  # never dereferenced: every call below is refused first
+    assert lib.sd_sample_logits_noalloc(65, u, L, 16, p, p, p, 0, 0, 0, None, p, None) == sv.SD_ELIMIT
+    L2 = (ctypes.c_int32 * 2)(512, 511)  # 1025 slots
+    assert lib.sd_sample_logits_noalloc(2, u, L2, 16, p, p, p, 0, 0, 0, None, p, None) == sv.SD_ELIMIT
+    assert lib.sd_sample_logits_noalloc(1, u, L, sv.SD_NOALLOC_MAX_VOCAB + 1, p, p, p, 0, 0, 0, None, p,
+                                        None) == sv.SD_ELIMIT
+    assert lib.sd_sample_logits_noalloc(0, u, L, 16, p, p, p, 0, 0, 0, None, p, None) == sv.SD_EINVAL
+    assert lib.sd_sample_logits_noalloc(1, u, L, 16, p, None, p, 1, 0, 0, None, p, None) == sv.SD_EINVAL
+    assert lib.sd_sample_logits_noalloc(1, u, L, 16, p, p, p, 3, 0, 0, None, p, None) == sv.SD_EINVAL
+    assert sv.status_str(sv.SD_ELIMIT) != "unknown status"
