@@ -45,7 +45,7 @@ def parse():
                     help="comma-separated workloads timed after the headline one ('none': skip)")
     ap.add_argument("--mode", default="stochastic", choices=["stochastic", "greedy"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-layers", type=int, default=4,
+    ap.add_argument("--cpu-layers", type=int, default=3,
                     help="decoder layers the CPU-baseline sample runs (extrapolated to all)")
     ap.add_argument("--breakdown", action="store_true", help="time every kernel class")
     ap.add_argument("--no-greedy", action="store_true",

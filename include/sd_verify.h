@@ -119,7 +119,10 @@ typedef struct sd_ctx sd_ctx;
  *   batches of up to max_batch_tokens slots.
  * weight_pack_bytes: the library's copy of the projection matrices and the
  *   lm_head in its streaming layout (SD_BF16; 0 for SD_F32).
- * Returns SD_EINVAL if cfg is inconsistent. Host-only; needs no device. */
+ * Returns SD_EINVAL if cfg is inconsistent, SD_ENOTIMPL for shapes the
+ * kernels do not cover (SD_BF16: head_dim 128, widths in whole tiles, at most
+ * 416 slots per batch, one layer's pages below 4 GB). Host-only; needs no
+ * device. */
 sd_status sd_verify_query_sizes(const sd_config* cfg, uint64_t* kv_pool_bytes,
                                 uint64_t* workspace_bytes, uint64_t* weight_pack_bytes);
 

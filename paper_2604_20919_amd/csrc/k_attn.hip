@@ -8,8 +8,14 @@
 // bf16 path (MFMA).  A workgroup takes one work item (b, g, context chunk);
 // the host sizes chunks so that a batch has about 512 items of equal length.
 // The chunk is streamed in 32-token blocks (two KV pages, 16 KB of K and V)
-// with direct global-to-LDS loads into a ring of LDS buffers, so several
-// blocks per workgroup are in flight without staging registers.  Each lane
+// with direct global-to-LDS loads (one buffer resource over the layer's
+// pages, 32-bit offsets) into a ring of LDS buffers, so the next block is in
+// flight while one is multiplied, without staging registers.  The block's
+// fragments are read from LDS by ds_read instructions issued in inline
+// assembly: for reads the compiler sees, it cannot tell a ring buffer from
+// the one being loaded and waits for every direct-to-LDS load in flight,
+// which leaves nothing in flight during the products (C4 attention 6.1 ->
+// 5.5 ms per step); their completion is waited for explicitly.  Each lane
 // gathers the piece that belongs to its LDS slot, which leaves the block in
 // MFMA fragment order: every operand read is one contiguous 1 KB wave read.
 // Wave w owns query-row tiles w, w+4, ... (16 rows each) and, per block:
@@ -92,11 +98,209 @@ __device__ __forceinline__ float row_sum4(float v) {
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// Eight 16-byte LDS reads of consecutive 1 KB fragments starting at LDS
+// byte address `a` (this lane's slot), issued without a wait.
+__device__ __forceinline__ void lds_read8(bf16x8 (&f)[8], uint32_t a) {
+    asm volatile(
+        "ds_read_b128 %0, %8\n\t"
+        "ds_read_b128 %1, %8 offset:1024\n\t"
+        "ds_read_b128 %2, %8 offset:2048\n\t"
+        "ds_read_b128 %3, %8 offset:3072\n\t"
+        "ds_read_b128 %4, %8 offset:4096\n\t"
+        "ds_read_b128 %5, %8 offset:5120\n\t"
+        "ds_read_b128 %6, %8 offset:6144\n\t"
+        "ds_read_b128 %7, %8 offset:7168"
+        : "=&v"(f[0]), "=&v"(f[1]), "=&v"(f[2]), "=&v"(f[3]), "=&v"(f[4]), "=&v"(f[5]), "=&v"(f[6]),
+          "=&v"(f[7])
+        : "v"(a)
+        : "memory");
+}
+
+// Per-item constants of the ring and the per-pass state of a wave's row tiles.
+struct AttnItem {
+    int c0, c1, nblk, prefix, wave, lane, lg, g;
+    const cint32_t* pt;
+    int kpg0, koff0, kpg1, koff1, vpg0, voff0, vpg1, voff1;  // this thread's gather sources
+};
+struct AttnState {
+    bf16x8 qf[RT_MAX][4], ql[RT_MAX][4];  // query hi / lo planes
+    int lim[RT_MAX];
+    float m[RT_MAX], l[RT_MAX];
+    f32x4 o[RT_MAX][8];
+    bool act[RT_MAX];
+};
+
+// The chunk's blocks through the LDS ring (buffers r0..r3) for one pass of
+// row tiles.
 template <int NBUF>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_attn_bf16(AttnP p) {
+__device__ __forceinline__ void attn_ring(const AttnP& p, const AttnItem& ac, AttnState& st, uint4* r0,
+                                          uint4* r1, uint4* r2, uint4* r3) {
     constexpr int PD = NBUF - 1;  // blocks in flight
     static_assert(NBUF >= 2 && NBUF <= 4, "the ring's tail waits cover up to three blocks in flight");
-    __shared__ __attribute__((aligned(16))) uint4 kvs[NBUF][1024];
+    const int c0 = ac.c0, c1 = ac.c1, nblk = ac.nblk, prefix = ac.prefix, wave = ac.wave;
+    const int lane = ac.lane, lg = ac.lg, g = ac.g;
+    const int kpg0 = ac.kpg0, koff0 = ac.koff0, kpg1 = ac.kpg1, koff1 = ac.koff1;
+    const int vpg0 = ac.vpg0, voff0 = ac.voff0, vpg1 = ac.vpg1, voff1 = ac.voff1;
+    const cint32_t* pt = ac.pt;
+    auto& qf = st.qf;
+    auto& ql = st.ql;
+    auto& lim = st.lim;
+    auto& m = st.m;
+    auto& l = st.l;
+    auto& o = st.o;
+    auto& act = st.act;
+    // One buffer resource over this layer's pages (the host keeps a layer's
+    // pages below 4 GB); per lane a 32-bit offset: page * page bytes + the
+    // KV head's block + the piece.
+    const uint32_t page_bytes = (uint32_t)(p.kv.page_elems() * 2);
+    const uint32_t gk = (uint32_t)(p.kv.k_off(0, 0, g) * 2);  // K block of head g
+    const uint32_t gv = (uint32_t)(p.kv.v_off(0, 0, g) * 2);  // V block of head g
+    const __amdgpu_buffer_rsrc_t kres = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)((const char*)p.kv.base + p.kv.k_off(p.layer, 0, 0) * 2), (short)0,
+        (int)(uint32_t)((uint64_t)p.kv.n_pages * page_bytes), 0x00020000);
+    typedef __attribute__((address_space(3))) void lds_void;
+    // Requests block blk into LDS buffer buf: four 16-byte direct loads per
+    // thread.  Tokens past the chunk end are read from the chunk's last page
+    // (the page index is clamped); their scores are masked, and V there is
+    // finite (pool zeroed at init, later only model values), so p = 0
+    // contributes exactly 0.
+    auto issue = [&](int blk, uint4* buf) __attribute__((always_inline)) {
+        const int t0 = c0 + blk * 32;
+        const uint32_t pb0 = (uint32_t)pt[min(t0, c1 - 1) >> 4] * page_bytes;
+        const uint32_t pb1 = (uint32_t)pt[min(t0 + 16, c1 - 1) >> 4] * page_bytes;
+        uint4* dst = buf + wave * 64;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(kres, (lds_void*)dst, 16, (int)((kpg0 ? pb1 : pb0) + gk + koff0), 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(kres, (lds_void*)(dst + 256), 16, (int)((kpg1 ? pb1 : pb0) + gk + koff1), 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(kres, (lds_void*)(dst + 512), 16, (int)((vpg0 ? pb1 : pb0) + gv + voff0), 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(kres, (lds_void*)(dst + 768), 16, (int)((vpg1 ? pb1 : pb0) + gv + voff1), 0, 0, 0);
+    };
+
+        // One 32-token block for this wave's row tiles.  Scores stay in the
+    // raw (unscaled) domain until the exponent, which folds the scale in:
+    // p = 2^(s*c - m*c) with c = log2(e)/sqrt(hd).  Blocks that every
+    // row sees completely skip the causal/chunk mask; the running output
+    // is rescaled only when some row's maximum grew; the row sum stays
+    // per lane until the end of the chunk.
+    auto compute = [&](const uint4* buf, int blk) __attribute__((always_inline)) {
+        const int t0 = c0 + blk * 32;
+        const bool full = t0 + 32 <= c1 && t0 + 31 <= prefix;
+        // The block's 16 fragments (8 K, 8 V^T; shared by the wave's row
+        // tiles) are read by ds_read instructions the compiler does not see:
+        // it cannot tell these reads apart from the direct-to-LDS loads into
+        // the other ring buffers and would make them wait for every load in
+        // flight.  The reads' completion is waited for explicitly below (the
+        // waits take the fragments as operands, so nothing that uses a
+        // fragment can be scheduled before its wait).
+        bf16x8 kfr[8], vfr[8];
+        const uint32_t la = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint4*)buf + lane * 16u;
+        lds_read8(kfr, la);
+        lds_read8(vfr, la + 512u * 16u);
+        asm volatile("s_waitcnt lgkmcnt(8)"
+                     : "+v"(kfr[0]), "+v"(kfr[1]), "+v"(kfr[2]), "+v"(kfr[3]), "+v"(kfr[4]),
+                       "+v"(kfr[5]), "+v"(kfr[6]), "+v"(kfr[7]));
+#pragma unroll
+        for (int i = 0; i < RT_MAX; ++i) {
+            if (!act[i]) continue;
+            // S^T = K (Q_hi + Q_lo)^T
+            f32x4 sa = f32x4{0.f, 0.f, 0.f, 0.f}, sb = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ds = 0; ds < 4; ++ds) {
+                const bf16x8 ka = kfr[ds];
+                const bf16x8 kk = kfr[4 + ds];
+                sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[i][ds], sa, 0, 0, 0);
+                sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, ql[i][ds], sa, 0, 0, 0);
+                sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qf[i][ds], sb, 0, 0, 0);
+                sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, ql[i][ds], sb, 0, 0, 0);
+            }
+            // lane holds the scores of its query row at tokens t0 + 8*lg + e
+            float sc[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                sc[e] = sa[e];
+                sc[4 + e] = sb[e];
+            }
+            if (!full) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int tok = t0 + 8 * lg + e;
+                    sc[e] = (tok < c1 && tok <= lim[i]) ? sc[e] : -INFINITY;
+                }
+            }
+            float bm = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
+                             fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
+            bm = row_max4(bm);
+            const float mn = fmaxf(m[i], bm);
+            const bool live = mn != -INFINITY;  // something visible for this row
+            const float ms = live ? mn * p.scale_log2 : 0.f;
+            const float alpha = live ? __builtin_amdgcn_exp2f((m[i] - mn) * p.scale_log2) : 1.f;
+            // P as hi + lo bf16 pair (about 16 significant bits)
+            float rs = 0.f;
+            bf16x8 pb, pl;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float pe = __builtin_amdgcn_exp2f(fmaf(sc[e], p.scale_log2, -ms));
+                rs += pe;
+                pb[e] = (__bf16)pe;
+                pl[e] = (__bf16)(pe - (float)pb[e]);
+            }
+            l[i] = fmaf(l[i], alpha, rs);
+            m[i] = mn;
+            if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
+#pragma unroll
+                for (int dt = 0; dt < 8; ++dt) o[i][dt] *= alpha;
+            }
+            if (i == 0)
+                asm volatile("s_waitcnt lgkmcnt(0)"
+                             : "+v"(vfr[0]), "+v"(vfr[1]), "+v"(vfr[2]), "+v"(vfr[3]), "+v"(vfr[4]),
+                               "+v"(vfr[5]), "+v"(vfr[6]), "+v"(vfr[7]));
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt) {
+                const bf16x8 vf = vfr[dt];
+                o[i][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb, o[i][dt], 0, 0, 0);
+                o[i][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl, o[i][dt], 0, 0, 0);
+            }
+        }
+    };
+
+    // Ring pipeline over NBUF LDS buffers.  Iteration k waits for its own
+    // loads of block k (the loads of the blocks issued after it may stay
+    // in flight: 4*(PD-1), or 4*(last-k) in the tail) and its LDS reads,
+    // then a barrier makes every wave's loads of block k visible and
+    // retires every wave's reads of block k-1, whose buffer then
+    // receives block k+PD while there is one.  Loads retire in issue
+    // order, so the counts are exact; the prologue clamps its block
+    // indices (a chunk shorter than PD blocks re-reads its last one,
+    // which only makes the waits stricter).
+    const int last = nblk - 1;
+#pragma unroll
+    for (int u = 0; u < PD; ++u) issue(min(u, last), u == 0 ? r0 : u == 1 ? r1 : r2);
+    for (int k0 = 0; k0 < nblk; k0 += NBUF) {
+#pragma unroll
+        for (int u = 0; u < NBUF; ++u) {
+            const int k = k0 + u;
+            if (k >= nblk) break;
+            if (k + PD <= last) {
+                wait_vm<4 * (PD - 1), true>();
+                barrier_nofence();
+                const int nb = (u + PD) % NBUF;
+                issue(k + PD, nb == 0 ? r0 : nb == 1 ? r1 : nb == 2 ? r2 : r3);
+            } else {
+                // tail: blocks k..last are the only ones in flight
+                if (last - k >= 2) wait_vm<8, true>();
+                else if (last - k == 1) wait_vm<4, true>();
+                else wait_vm<0, true>();
+                barrier_nofence();
+            }
+            compute(u == 0 ? r0 : u == 1 ? r1 : u == 2 ? r2 : r3, k);
+        }
+    }
+    // drain the tail loads before the buffers are reused or released
+    wait_vm<0>();
+
+}
+
+template <int NBUF>
+__device__ __forceinline__ void attn_bf16_body(const AttnP& p, uint4* r0, uint4* r1, uint4* r2, uint4* r3) {
     // The batch metadata is read-only while the kernel runs: reading it
     // through the constant address space gives scalar loads, which keep the
     // vector memory counter (waited on below) free of anything but KV.
@@ -111,7 +315,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const int prefix = ((const cint32_t*)p.bv.prefix)[b];
     const int tbase = ((const cint32_t*)p.bv.slot_off)[b];
     const cint32_t* pt = (const cint32_t*)p.bv.page_table + (size_t)b * p.bv.max_pages;
-    const char* kvb = (const char*)p.kv.base;
     const int nblk = (c1 - c0 + 31) >> 5;
 
     // this thread's four gather sources (page of the block, byte offset)
@@ -120,35 +323,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     k_slot_src(256 + threadIdx.x, kpg1, koff1);
     v_slot_src(threadIdx.x, vpg0, voff0);
     v_slot_src(256 + threadIdx.x, vpg1, voff1);
-    const size_t kstride = p.kv.v_off(0, 0, 0) - p.kv.k_off(0, 0, 0);  // K block -> V block
-    // Requests block blk into LDS buffer buf: four 16-byte direct loads per
-    // thread.  Tokens past the chunk end are read from the chunk's last page
-    // (the page index is clamped); their scores are masked, and V there is
-    // finite (pool zeroed at init, later only model values), so p = 0
-    // contributes exactly 0.
-    auto issue = [&](int blk, int buf) {
-        const int t0 = c0 + blk * 32;
-        const int page0 = pt[min(t0, c1 - 1) >> 4];
-        const int page1 = pt[min(t0 + 16, c1 - 1) >> 4];
-        const char* k0 = kvb + p.kv.k_off(p.layer, page0, g) * 2;
-        const char* k1 = kvb + p.kv.k_off(p.layer, page1, g) * 2;
-        uint4* dst = &kvs[buf][wave * 64];
-        __builtin_amdgcn_global_load_lds((const void*)((kpg0 ? k1 : k0) + koff0), (void*)dst, 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((const void*)((kpg1 ? k1 : k0) + koff1), (void*)(dst + 256), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((const void*)((vpg0 ? k1 : k0) + kstride * 2 + voff0),
-                                         (void*)(dst + 512), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((const void*)((vpg1 ? k1 : k0) + kstride * 2 + voff1),
-                                         (void*)(dst + 768), 16, 0, 0);
-    };
-
+    AttnItem ac;
+    ac.c0 = c0;
+    ac.c1 = c1;
+    ac.nblk = nblk;
+    ac.prefix = prefix;
+    ac.wave = wave;
+    ac.lane = lane;
+    ac.lg = lg;
+    ac.g = g;
+    ac.pt = pt;
+    ac.kpg0 = kpg0; ac.koff0 = koff0; ac.kpg1 = kpg1; ac.koff1 = koff1;
+    ac.vpg0 = vpg0; ac.voff0 = voff0; ac.vpg1 = vpg1; ac.voff1 = voff1;
     const int ntiles = (R + 15) >> 4;
     for (int rp = 0; rp < ntiles; rp += 4 * RT_MAX) {
         // this wave's row tiles in this pass: rp + wave + 4*i
-        bf16x8 qf[RT_MAX][4], ql[RT_MAX][4];  // query hi / lo planes
-        int lim[RT_MAX];
-        float m[RT_MAX], l[RT_MAX];
-        f32x4 o[RT_MAX][8];
-        bool act[RT_MAX];
+        AttnState st;
+        auto& qf = st.qf;  // query hi / lo planes
+        auto& ql = st.ql;
+        auto& lim = st.lim;
+        auto& m = st.m;
+        auto& l = st.l;
+        auto& o = st.o;
+        auto& act = st.act;
 #pragma unroll
         for (int i = 0; i < RT_MAX; ++i) {
             const int tile = rp + wave + 4 * i;
@@ -172,110 +369,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         // the query loads must not be counted by the block waits below
         wait_vm<0>();
 
-        // One 32-token block for this wave's row tiles.  Scores stay in the
-        // raw (unscaled) domain until the exponent, which folds the scale in:
-        // p = 2^(s*c - m*c) with c = log2(e)/sqrt(hd).  Blocks that every
-        // row sees completely skip the causal/chunk mask; the running output
-        // is rescaled only when some row's maximum grew; the row sum stays
-        // per lane until the end of the chunk.
-        auto compute = [&](int buf, int blk) {
-            const int t0 = c0 + blk * 32;
-            const bool full = t0 + 32 <= c1 && t0 + 31 <= prefix;
-            const uint4* kb = kvs[buf];
-            const uint4* vb = kvs[buf] + 512;
-#pragma unroll
-            for (int i = 0; i < RT_MAX; ++i) {
-                if (!act[i]) continue;
-                // S^T = K (Q_hi + Q_lo)^T
-                f32x4 sa = f32x4{0.f, 0.f, 0.f, 0.f}, sb = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int ds = 0; ds < 4; ++ds) {
-                    const bf16x8 ka = __builtin_bit_cast(bf16x8, kb[ds * 64 + lane]);
-                    const bf16x8 kk = __builtin_bit_cast(bf16x8, kb[(4 + ds) * 64 + lane]);
-                    sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[i][ds], sa, 0, 0, 0);
-                    sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, ql[i][ds], sa, 0, 0, 0);
-                    sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, qf[i][ds], sb, 0, 0, 0);
-                    sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kk, ql[i][ds], sb, 0, 0, 0);
-                }
-                // lane holds the scores of its query row at tokens t0 + 8*lg + e
-                float sc[8];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    sc[e] = sa[e];
-                    sc[4 + e] = sb[e];
-                }
-                if (!full) {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const int tok = t0 + 8 * lg + e;
-                        sc[e] = (tok < c1 && tok <= lim[i]) ? sc[e] : -INFINITY;
-                    }
-                }
-                float bm = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])),
-                                 fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
-                bm = row_max4(bm);
-                const float mn = fmaxf(m[i], bm);
-                const bool live = mn != -INFINITY;  // something visible for this row
-                const float ms = live ? mn * p.scale_log2 : 0.f;
-                const float alpha = live ? __builtin_amdgcn_exp2f((m[i] - mn) * p.scale_log2) : 1.f;
-                // P as hi + lo bf16 pair (about 16 significant bits)
-                float rs = 0.f;
-                bf16x8 pb, pl;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const float pe = __builtin_amdgcn_exp2f(fmaf(sc[e], p.scale_log2, -ms));
-                    rs += pe;
-                    pb[e] = (__bf16)pe;
-                    pl[e] = (__bf16)(pe - (float)pb[e]);
-                }
-                l[i] = fmaf(l[i], alpha, rs);
-                m[i] = mn;
-                if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
-#pragma unroll
-                    for (int dt = 0; dt < 8; ++dt) o[i][dt] *= alpha;
-                }
-#pragma unroll
-                for (int dt = 0; dt < 8; ++dt) {
-                    const bf16x8 vf = __builtin_bit_cast(bf16x8, vb[dt * 64 + lane]);
-                    o[i][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb, o[i][dt], 0, 0, 0);
-                    o[i][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl, o[i][dt], 0, 0, 0);
-                }
-            }
-        };
-
-        // Ring pipeline over NBUF LDS buffers.  Iteration k waits for its own
-        // loads of block k (the loads of the blocks issued after it may stay
-        // in flight: 4*(PD-1), or 4*(last-k) in the tail) and its LDS reads,
-        // then a barrier makes every wave's loads of block k visible and
-        // retires every wave's reads of block k-1, whose buffer then
-        // receives block k+PD while there is one.  Loads retire in issue
-        // order, so the counts are exact; the prologue clamps its block
-        // indices (a chunk shorter than PD blocks re-reads its last one,
-        // which only makes the waits stricter).
-        const int last = nblk - 1;
-#pragma unroll
-        for (int u = 0; u < PD; ++u) issue(min(u, last), u);
-        for (int k0 = 0; k0 < nblk; k0 += NBUF) {
-#pragma unroll
-            for (int u = 0; u < NBUF; ++u) {
-                const int k = k0 + u;
-                if (k >= nblk) break;
-                if (k + PD <= last) {
-                    wait_vm<4 * (PD - 1), true>();
-                    barrier_nofence();
-                    issue(k + PD, (u + PD) % NBUF);
-                } else {
-                    // tail: blocks k..last are the only ones in flight
-                    if (last - k >= 2) wait_vm<8, true>();
-                    else if (last - k == 1) wait_vm<4, true>();
-                    else wait_vm<0, true>();
-                    barrier_nofence();
-                }
-                compute(u, k);
-            }
-        }
-        // drain the tail loads before the buffers are reused or released
-        wait_vm<0>();
+        attn_ring<NBUF>(p, ac, st, r0, r1, r2, r3);
 
         // partial of this item: lane holds O^T[d = dt*16 + 4*lg + r][row lr]
 #pragma unroll
@@ -295,6 +389,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         }
         __syncthreads();  // the LDS buffers are reused by the next row pass
     }
+}
+
+template <int NBUF>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_attn_bf16(AttnP p) {
+    __shared__ __attribute__((aligned(16))) uint4 kv0[1024];
+    __shared__ __attribute__((aligned(16))) uint4 kv1[1024];
+    __shared__ __attribute__((aligned(16))) uint4 kv2[NBUF > 2 ? 1024 : 1];
+    __shared__ __attribute__((aligned(16))) uint4 kv3[NBUF > 3 ? 1024 : 1];
+    attn_bf16_body<NBUF>(p, kv0, kv1, kv2, kv3);
 }
 
 // Merge the partials of the chunks of (b, g) for one query row in chunk

@@ -87,6 +87,10 @@ sd_status validate_config(const sd_config* c) {
         if (D.nqkv() % 128 || D.d % 128 || (2 * D.F) % 128 || D.V % 128) return SD_ENOTIMPL;
         if (D.hq * D.hd % 16 || D.hkv * D.hd % 16) return SD_ENOTIMPL;
         if (c->max_batch_tokens > 416) return SD_ENOTIMPL;
+        // the attention kernel addresses one layer's pages with 32-bit
+        // offsets: below 4 GB per layer (65535 pages of the 32B shape)
+        const uint64_t page_bytes = 2ull * D.hkv * kPageTokens * D.hd * 2;
+        if ((uint64_t)c->n_pages * page_bytes >= (1ull << 32)) return SD_ENOTIMPL;
     } else {
         if (c->head_dim > 128) return SD_ENOTIMPL;
     }

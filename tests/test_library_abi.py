@@ -111,3 +111,12 @@ def test_noalloc_limits_are_checked_before_any_device_call():
     assert lib.sd_sample_logits_noalloc(1, u, L, 16, p, None, p, 1, 0, 0, None, p, None) == sv.SD_EINVAL
     assert lib.sd_sample_logits_noalloc(1, u, L, 16, p, p, p, 3, 0, 0, None, p, None) == sv.SD_EINVAL
     assert sv.status_str(sv.SD_ELIMIT) != "unknown status"
+
+
+def test_query_sizes_rejects_a_layer_of_pages_beyond_4gb():
+    """The attention kernel addresses one layer's pages with 32-bit offsets:
+    65535 pages of the 32B shape (64 KB each) pass, 65536 do not."""
+    sv.sd_verify_query_sizes(_cfg(n_pages=65535))
+    with pytest.raises(sv.SdError) as e:
+        sv.sd_verify_query_sizes(_cfg(n_pages=65536))
+    assert e.value.status == sv.SD_ENOTIMPL
