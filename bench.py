@@ -250,6 +250,13 @@ def main():
     roofline["mfma_issued_tflops"] = round(2 * mfma_tf, 1)
     roofline["mfma_issued_frac_bf16"] = round(2 * mfma_tf / BF16_PEAK_TFLOPS, 4)
     roofline["mfma_issued_frac_of_achievable"] = round(2 * mfma_tf / achievable["mfma_bf16_tflops"], 4)
+    # MFMA work the counters saw (both planes and the last slot tile's padding),
+    # over the live launch time, and the counted busy fraction of all SIMDs
+    mm = measured_mfma(args.workload)
+    if mm is not None:
+        roofline["mfma_counted_tflops"] = round(mm[0] / gu_avg_s / 1e12, 1)
+        roofline["mfma_counted_frac_bf16"] = round(mm[0] / gu_avg_s / 1e12 / BF16_PEAK_TFLOPS, 4)
+        roofline["mfma_busy_frac_counted"] = mm[1]
 
     def class_ms(k, steps=3):
         """Per-step device time of one kernel class (sum of the event pairs
@@ -353,6 +360,25 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, cpu_batch, args.cpu_layers, acc_step / verified_step)
     print(json.dumps(result), flush=True)
+
+
+def measured_mfma(workload):
+    """MFMA work and busy fraction per gate/up launch from the committed SQ
+    counter summary (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512, SQ_VALU_MFMA_BUSY_CYCLES),
+    or None when it covers another workload or the GEMM source has changed."""
+    import hashlib
+    import re
+    path = os.path.join(ROOT, "profiles", f"mfma_lds_counters_{workload}.md")
+    src = os.path.join(ROOT, "paper_2604_20919_amd", "csrc", "k_gemm.hip")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    f = re.search(r"gateup_mfma_flop_per_launch: (\d+)", text)
+    b = re.search(r"gateup_mfma_busy_frac: ([0-9.]+)", text)
+    h = re.search(r"k_gemm.hip sha256: ([0-9a-f]{64})", text)
+    if not (f and b and h) or hashlib.sha256(open(src, "rb").read()).hexdigest() != h.group(1):
+        return None
+    return int(f.group(1)), float(b.group(1))
 
 
 def measured_traffic(workload):
