@@ -35,6 +35,20 @@ class RoundLog:
 
 
 @dataclass
+class VerifyRecord:
+    """One verification of GpuVerify, kept when it records: the batch and
+    round, its users, the drafts and draft distributions it was given, and
+    what sd_accept returned for each user."""
+    batch: int
+    round: int
+    users: List[int]
+    drafts: object        # int32 [sum l_m]
+    q: object             # fp32 [sum l_m][V]
+    n_acc: List[int]
+    token: List[int]
+
+
+@dataclass
 class PipelineResult:
     rounds: int
     total_ms: float
@@ -127,7 +141,7 @@ class GpuVerify:
     scale, drafts sampled from q (stochastic accept/resample)."""
 
     def __init__(self, verifier, assign: Sequence[int], l: Sequence[int], vocab: int,
-                 q_sigma: float, seed: int = 0, commit: bool = True):
+                 q_sigma: float, seed: int = 0, commit: bool = True, record: bool = False):
         import torch
         self.torch = torch
         self.v = verifier
@@ -141,6 +155,7 @@ class GpuVerify:
         self.commit = commit
         self.accepted: List[int] = []
         self.drafted: List[int] = []
+        self.records: Optional[List[VerifyRecord]] = [] if record else None
 
     def __call__(self, n: int, r: int) -> int:
         torch = self.torch
@@ -150,7 +165,10 @@ class GpuVerify:
         q = torch.softmax(logits, dim=1)
         d = torch.multinomial(q, 1, generator=self.g).to(torch.int32).reshape(-1)
         self.v.verify(n, self.assign, self.l, d, q, "stochastic", seed=self.seed, round_=r)
-        n_acc, _ = self.v.accept(n, len(self.assign), commit=self.commit)
+        n_acc, tok = self.v.accept(n, len(self.assign), commit=self.commit)
+        if self.records is not None:
+            self.records.append(VerifyRecord(n, r, users, d.cpu().numpy(), q.cpu().numpy(),
+                                             [int(n_acc[m]) for m in users], [int(tok[m]) for m in users]))
         for m in users:
             self.accepted.append(int(n_acc[m]))
             self.drafted.append(self.l[m])
