@@ -271,11 +271,13 @@ def main():
     kv_read_step = sum(int(p + l + 1) for p, l in zip(w.prefix_len, w.draft_len)) * m.kv_bytes_per_token()
     attn_ms = class_ms(sv.SD_K_ATTN)
     nd_all = int(sum(int(b.draft_len.sum()) for b in batches))
+    # phase A comes from the lm_head epilogue's statistics (no logits read);
+    # phase B reads the stop slot's logits row and q row of every user
     if run.sparse is not None:
-        # logits once; every sparse row's K entries (the accept lookups) and remainders
-        samp_bytes = verified_step * m.vocab * 4 + nd_all * (args.q_topk * 8 + 4)
+        # the stop rows; every sparse row's K entries (the accept lookups) and remainders
+        samp_bytes = int(w.n_users) * m.vocab * 4 + nd_all * (args.q_topk * 8 + 4)
     else:
-        samp_bytes = verified_step * m.vocab * 4 + int(w.n_users) * m.vocab * 4
+        samp_bytes = 2 * int(w.n_users) * m.vocab * 4
     samp_ms = class_ms(sv.SD_K_SAMPLER)
     kernels = {
         "attention": {"achieved": round(kv_read_step / (attn_ms / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
@@ -287,7 +289,8 @@ def main():
                     "unit": "GB/s", "frac": round(samp_bytes / (samp_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
                     "frac_of_achievable": round(samp_bytes / (samp_ms / 1e3) / 1e9 / hbm_ach, 4),
                     "bytes_per_step": samp_bytes, "ms_per_step": round(samp_ms, 4),
-                    "note": ("accept/reject + resample kernels; bytes = T x V fp32 logits + "
+                    "note": ("phase-A merge of the lm_head statistics + accept/reject + resample "
+                             "kernels; bytes = one fp32 logits row per user + "
                              + ("the sparse rows" if run.sparse is not None else "one q row per user"))},
     }
 
@@ -416,25 +419,27 @@ def greedy_run(run, steps, warmup):
 def plant_greedy_drafts(v, w, batches, dev_in, torch):
     """Greedy workload: user m's first k_m drafts follow the target's own
     argmax continuation (k_m uniform in 0..l_m, seeded), then one random
-    token; found with l_max teacher-forced passes on the GPU."""
+    token; found with l_max greedy passes on the GPU: at pass j a user whose
+    first j drafts already follow the argmax stops at slot j, where the
+    returned token is the argmax (or later, when its draft j is the argmax
+    already)."""
     import workload as wl
     for n, b in enumerate(batches):
         d, q, au = dev_in[n]
         k = wl._ints(len(b.users), w.seed, wl.S_LEN << 8, 0, int(b.draft_len.max()))
         k = np.minimum(k, b.draft_len)
+        doff = np.concatenate([[0], np.cumsum(b.draft_len)]).astype(np.int64)
         drafts = b.drafts.copy()
         for j in range(int(b.draft_len.max())):
             d.copy_(torch.from_numpy(drafts))
-            v.verify(n, w.assign, w.draft_len, d, q, "force")
-            lg = v.logits(n, b.T)
-            v.accept(n, w.n_users)
-            am = lg.argmax(dim=1).cpu().numpy()
-            so, do = 0, 0
-            for i, L in enumerate(b.draft_len):
-                if j < L and j < k[i]:
-                    drafts[do + j] = am[so + j]
-                so += int(L) + 1
-                do += int(L)
+            v.verify(n, w.assign, w.draft_len, d, q, "greedy")
+            n_acc, tok = v.accept(n, w.n_users)
+            for i, u in enumerate(b.users):
+                if j < b.draft_len[i] and j < k[i]:
+                    a = int(n_acc[u])
+                    assert a >= j, "a planted argmax draft was rejected"
+                    if a == j:
+                        drafts[doff[i] + j] = tok[u]
         d.copy_(torch.from_numpy(drafts))
         b.drafts = drafts
 

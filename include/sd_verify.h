@@ -83,7 +83,30 @@ typedef struct sd_config {
     int32_t max_pending;  /* batches that may be in flight at once (1..8) */
     float rope_base;      /* RoPE base (1e6 for Qwen3 shapes) */
     float rms_eps;        /* RMSNorm epsilon */
+    int32_t logits_out;   /* SD_LOGITS_AS_NEEDED (0), SD_LOGITS_ALL or SD_LOGITS_UNFUSED */
 } sd_config;
+
+/* Where the accept step of Sec. II-A step 2 gets each slot's softmax
+ * statistics (row max, sum of exp(z - max), argmax, logit of the next
+ * draft) and which passes store the fp32 logits [sum(l_m+1)][vocab].
+ * bf16 configuration:
+ *   SD_LOGITS_AS_NEEDED  the lm_head product emits the statistics from its
+ *                        epilogue; logits are stored only when a later step
+ *                        reads them: SD_STOCHASTIC (the resampling race at
+ *                        the stop slot, which is known only after every
+ *                        slot's statistics) and decode steps with probs.
+ *                        SD_GREEDY / SD_FORCE passes store none, and
+ *                        sd_debug_logits returns SD_ESTATE for them;
+ *   SD_LOGITS_ALL        statistics from the epilogue, logits stored by
+ *                        every pass;
+ *   SD_LOGITS_UNFUSED    logits stored by every pass and the statistics
+ *                        computed from them by separate kernels (the
+ *                        sd_sample_logits path).  Decisions and tokens equal
+ *                        the fused modes' except where u lies within a few
+ *                        fp32 ulps of p(d)/q(d) or two race keys do: the
+ *                        exp-sum is added up in another grouping.
+ * The fp32 configuration always stores logits and ignores this field. */
+enum { SD_LOGITS_AS_NEEDED = 0, SD_LOGITS_ALL = 1, SD_LOGITS_UNFUSED = 2 };
 
 /* Device pointers of one decoder layer, each row-major [out][in] so that
  * y = W x; element type sd_config.dtype.  The gain vectors (norm1, norm2,
@@ -325,7 +348,8 @@ sd_status sd_sample_logits(sd_ctx* ctx, int32_t batch, int32_t n_users, const in
 
 /* Diagnostic: copy the logits of pending batch `batch` (device fp32
  * [sum(l_m+1)][vocab]) into dst (device), ordered after the batch on
- * `stream`.  SD_ESTATE if the batch is not pending. */
+ * `stream`.  SD_ESTATE if the batch is not pending or its pass stored no
+ * logits (sd_config.logits_out). */
 sd_status sd_debug_logits(sd_ctx* ctx, int32_t batch, float* dst, sd_stream stream);
 
 /*

@@ -68,7 +68,46 @@ struct GemmP {
     const float* nss;
     int nnb;
     float eps;
+    // EPI_LMSTAT: per (slot, workgroup) statistics [T][tiles], the logit of
+    // each slot's next draft, that draft per slot (-1: none)
+    VStat* lstat;
+    float* zd;
+    const int32_t* dnext;
 };
+
+// lm_head epilogue, the part common to both MFMA forms: the per-wave
+// statistics of every slot (staged in LDS as [wave][slot]) are merged over
+// the workgroup's waves in wave order, i.e. in increasing vocab rows, and
+// leave as one 16-byte record per (workgroup, slot)
+template <int NTH, int NW, int NSLOT>
+__device__ __forceinline__ void lmstat_merge_waves(const GemmP& p, const VStat* stg, int wgi) {
+    for (int i = threadIdx.x; i < NSLOT && i < p.T; i += NTH) {
+        VStat st = stg[i];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) st = vstat_merge(st, stg[w * NSLOT + i]);
+        p.lstat[(size_t)i * p.tiles + wgi] = st;
+    }
+}
+
+// statistics of the n logits one lane holds for one slot (rows in
+// increasing order); the draft's logit goes to zd when its row is here
+template <int N>
+__device__ __forceinline__ VStat lane_stat(const float (&z)[N], const int (&row)[N], int d, float* zd) {
+    VStat st = vstat_empty();
+#pragma unroll
+    for (int e = 0; e < N; ++e) {
+        if (z[e] > st.v) { st.v = z[e]; st.i = row[e]; }
+        if (row[e] == d) *zd = z[e];
+    }
+    st.m = st.v;
+    if (st.m != -INFINITY) {
+        float sum = 0.f;
+#pragma unroll
+        for (int e = 0; e < N; ++e) sum += expf(z[e] - st.m);
+        st.s = sum;
+    }
+    return st;
+}
 
 // block sums of one slot row, all loads issued before the sum (at most
 // kNormKMax / kNormBlock blocks)
@@ -364,6 +403,42 @@ void k_gemm16(GemmP p) {
         }
     }
 
+    if constexpr (EPI == EPI_LMSTAT) {
+        // lane holds D[n = 4*lg + r][t = lr]: a slot's 16 rows of a group sit
+        // in lanes lr, lr + 16, lr + 32, lr + 48
+        static_assert(!SPLIT, "the lm_head statistics need whole k sums");
+        constexpr int NSLOT = MT * 16;
+        static_assert(NW * NSLOT * (int)sizeof(VStat) <= (int)sizeof(xs), "statistics staging exceeds LDS");
+        VStat* stg = reinterpret_cast<VStat*>(&xs[0][0]);
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+            const int t = m * 16 + lr;
+            VStat st = vstat_empty();
+            if (has_unit && m < mt_act && t < p.T) {
+                const float sc = rsl[t];
+                float z[NSUB * 4];
+                int row[NSUB * 4];
+#pragma unroll
+                for (int s = 0; s < NSUB; ++s) {
+                    const int r0 = (unit * NSUB + s) * 16 + 4 * lg;
+                    f32x4 v = acc[s][m] * sc;
+                    if (p.out) *(f32x4*)((float*)p.out + (size_t)t * p.ldo + r0) = v;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        z[s * 4 + e] = v[e];
+                        row[s * 4 + e] = r0 + e;
+                    }
+                }
+                st = lane_stat(z, row, p.dnext[t], p.zd + t);
+            }
+            st = vstat_merge(st, vstat_shfl_xor(st, 16));
+            st = vstat_merge(st, vstat_shfl_xor(st, 32));
+            if (lg == 0) stg[wv * NSLOT + t] = st;
+        }
+        __syncthreads();
+        lmstat_merge_waves<NTH, NW, NSLOT>(p, stg, wgi);
+        return;
+    }
     // lane holds D[n = 4*lg + r][t = lr] of each (sub-tile, slot tile)
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
@@ -602,6 +677,45 @@ void k_gemm32(GemmP p) {
                 for (int m = 0; m < PA; ++m) acc[s][m][e] += acc[s][m + PA + 1][e];
             }
     }
+    if constexpr (EPI == EPI_LMSTAT) {
+        // lane l holds slot 32m + l % 32 and rows 8q + 4(l/32) + 0..3 of its
+        // 32-row group: a slot's rows sit in lanes l and l ^ 32
+        static_assert(!SPLIT, "the lm_head statistics need whole k sums");
+        constexpr int MTO = PK ? PA + 1 : MT;
+        constexpr int NSLOT = MTO * 32;
+        static_assert(NW * NSLOT * (int)sizeof(VStat) <= (int)sizeof(xs), "statistics staging exceeds LDS");
+        VStat* stg = reinterpret_cast<VStat*>(&xs[0][0]);
+#pragma unroll
+        for (int m = 0; m < MTO; ++m) {
+            const int t = m * 32 + lc;
+            VStat st = vstat_empty();
+            if (has_unit && t < p.T && !(PK && m == PA && lc >= 16)) {
+                const float sc = rsl[t];
+                float z[NS * 16];
+                int row[NS * 16];
+#pragma unroll
+                for (int s = 0; s < NS; ++s)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int r0 = (unit * NS + s) * 32 + 8 * q + 4 * lh;
+                        const f32x4 v = f32x4{acc[s][m][4 * q], acc[s][m][4 * q + 1], acc[s][m][4 * q + 2],
+                                              acc[s][m][4 * q + 3]} * sc;
+                        if (p.out) *(f32x4*)((float*)p.out + (size_t)t * p.ldo + r0) = v;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            z[s * 16 + 4 * q + e] = v[e];
+                            row[s * 16 + 4 * q + e] = r0 + e;
+                        }
+                    }
+                st = lane_stat(z, row, p.dnext[t], p.zd + t);
+            }
+            st = vstat_merge(st, vstat_shfl_xor(st, 32));
+            if (lh == 0) stg[wv * NSLOT + m * 32 + lc] = st;
+        }
+        __syncthreads();
+        lmstat_merge_waves<NTH, NW, NSLOT>(p, stg, wgi);
+        return;
+    }
     if constexpr (SPLIT) {
         // one 32-slot tile at a time through the (now idle) staging buffer
         constexpr int WR = NW * NS * 32;  // weight rows of the workgroup
@@ -810,13 +924,16 @@ static GemmShape shape_for(int T, int vcols, bool raw, int K) {
         return GemmShape{16, mt, 2, 64, 4, 2, 0};
     }
     const int mt = (T + 31) / 32;
-    if (mt <= 4) return wide ? GemmShape{32, mt, 1, 64, 8, 2, 0} : GemmShape{32, mt, 1, 64, 4, 2, 0};
-    if (mt <= 7) return wide ? GemmShape{32, mt, 1, 64, 8, 1, 0} : GemmShape{32, mt, 1, 64, 4, 1, 0};
+    // eight-wave workgroups also for the lm_head, whose row count is not a
+    // multiple of 256 (the workgroups then take 7 or 8 row units each)
+    const bool w8 = wide || (!raw && vcols % 32 == 0);
+    if (mt <= 4) return w8 ? GemmShape{32, mt, 1, 64, 8, 2, 0} : GemmShape{32, mt, 1, 64, 4, 2, 0};
+    if (mt <= 7) return w8 ? GemmShape{32, mt, 1, 64, 8, 1, 0} : GemmShape{32, mt, 1, 64, 4, 1, 0};
     // 225..256 slots: eight waves with 32-k chunks (double-buffered staging
     // of 2 x 256 rows then fits one workgroup of 256 weight rows per CU);
     // same-box probe at T = 240: gate/up 292 vs 392 us, QKV 63 vs 99, O 51
     // vs 93, down 143 vs 210 us against four waves with 64-k chunks
-    if (mt <= 8) return wide ? GemmShape{32, 8, 1, 32, 8, 1, 0} : GemmShape{32, 8, 1, 64, 4, 1, 0};
+    if (mt <= 8) return w8 ? GemmShape{32, 8, 1, 32, 8, 1, 0} : GemmShape{32, 8, 1, 64, 4, 1, 0};
     if (mt <= 10) return {32, 10, 1, 32, 4, 1, 0};
     if (mt <= 13) return {32, 13, 1, 16, 4, 1, 0};
     return {0, 0, 0, 0, 0, 0, 0};
@@ -834,6 +951,7 @@ static GemmFn pick_epi(int epi) {
         switch (epi) {
             case EPI_RESID: return k_gemm16<MT, 2, KC, EPI_RESID, false, NW, 2, PD>;
             case EPI_SWIGLU: return k_gemm16<MT, 2, KC, EPI_SWIGLU, false, NW, 2, PD>;
+            case EPI_LMSTAT: return k_gemm16<MT, 2, KC, EPI_LMSTAT, false, NW, 2, PD>;
             default: return k_gemm16<MT, 2, KC, EPI_STORE, false, NW, 2, PD>;
         }
     } else {
@@ -841,6 +959,7 @@ static GemmFn pick_epi(int epi) {
         switch (epi) {
             case EPI_RESID: return k_gemm32<MT, 1, KC, EPI_RESID, false, NW, 2, PD, PK>;
             case EPI_SWIGLU: return k_gemm32<MT, 1, KC, EPI_SWIGLU, false, NW, 2, PD, PK>;
+            case EPI_LMSTAT: return k_gemm32<MT, 1, KC, EPI_LMSTAT, false, NW, 2, PD, PK>;
             default: return k_gemm32<MT, 1, KC, EPI_STORE, false, NW, 2, PD, PK>;
         }
     }
@@ -972,7 +1091,7 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
     // not a multiple of NW units (its surplus waves load and store nothing)
     const int units = p.vcols / unit_rows;
     p.tiles = (units + sh.NW - 1) / sh.NW;
-    int S = choose_splits(p.tiles, p.kchunks, sh.FILL ? 8 : sh.NW);
+    int S = g.epi == EPI_LMSTAT ? 1 : choose_splits(p.tiles, p.kchunks, sh.FILL ? 8 : sh.NW);
     while (S > 1 && (size_t)S * g.T * p.vcols > sb.gpart_floats) {
         int t = S - 1;
         while (t > 1 && p.kchunks % t) --t;
@@ -988,6 +1107,10 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
     p.nss = g.norm_ss;
     p.nnb = g.norm_nb;
     p.eps = D.eps;
+    p.lstat = reinterpret_cast<VStat*>(g.lstat);
+    p.zd = g.zd;
+    p.dnext = g.dnext;
+    if (g.groups_out) *g.groups_out = p.tiles;
     if (g.raw) {
         // S partial planes [S][T][N] for a fused consumer to reduce
         hipLaunchKernelGGL(pick<true>(sh, EPI_STORE), dim3(p.tiles * S), dim3(64 * sh.NW), 0, s, p);

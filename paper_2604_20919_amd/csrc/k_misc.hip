@@ -11,7 +11,7 @@ namespace sdv {
 // range checks, and cos/sin of the RoPE angle pos * base^(-2a/hd) per slot,
 // computed in double so that large positions keep full fp32 accuracy.
 // ---------------------------------------------------------------------------
-__global__ void k_prepare(BatchView bv, int32_t* tok, float* cs, int half, int V,
+__global__ void k_prepare(BatchView bv, int32_t* tok, int32_t* dnext, float* cs, int half, int V,
                           double log_base, int hd) {
     const int t = blockIdx.x;
     if (t >= bv.T) return;
@@ -23,6 +23,14 @@ __global__ void k_prepare(BatchView bv, int32_t* tok, float* cs, int half, int V
             v = 0;
         }
         tok[t] = v;
+        // the draft whose acceptance slot t decides (-1 after the last
+        // draft; an out-of-range draft, flagged by slot t + 1, reads as 0)
+        int dn = -1;
+        if (j < bv.L[b]) {
+            dn = bv.drafts[bv.draft_off[b] + j];
+            if (dn < 0 || dn >= V) dn = 0;
+        }
+        dnext[t] = dn;
     }
     const double pos = (double)(bv.prefix[b] + j);
     for (int a = threadIdx.x; a < half; a += blockDim.x) {
@@ -35,7 +43,7 @@ __global__ void k_prepare(BatchView bv, int32_t* tok, float* cs, int half, int V
 }
 
 void launch_prepare(const Dims& D, const BatchView& bv, const SlotBufs& sb, hipStream_t s) {
-    hipLaunchKernelGGL(k_prepare, dim3(bv.T), dim3(64), 0, s, bv, sb.tok, sb.cs, D.hd / 2, D.V,
+    hipLaunchKernelGGL(k_prepare, dim3(bv.T), dim3(64), 0, s, bv, sb.tok, sb.dnext, sb.cs, D.hd / 2, D.V,
                        log((double)D.rope_base), D.hd);
 }
 

@@ -3,8 +3,11 @@
 // token).  Two kernels, both split over vocab chunks so that every row is
 // read by many workgroups at once:
 //   phase A, per query slot: row max, sum of exp(z - max) and argmax (lowest
-//     index on ties) per vocab chunk; a second kernel merges the chunk
-//     partials of a slot in chunk order and takes the slot's accept decision:
+//     index on ties) per vocab chunk -- or, in the verify pass of the bf16
+//     configuration, per lm_head workgroup, written by the lm_head
+//     epilogue together with the logit of the slot's next draft, so the
+//     logits need not be read back; a second kernel merges the partials of
+//     a slot in a fixed order and takes the slot's accept decision:
 //     greedy: draft == argmax; stochastic: u < p(d)/q(d) as an fp32
 //     division, u from the caller or from Philox;
 //   phase B, per user: a = number of leading accepts; greedy/force emit the
@@ -30,14 +33,12 @@ struct SampP {
     float* spartB;        // [B][kVocabChunks][4]
     int32_t* result;      // n_acc [Bmax], token [Bmax], flags
     int bmax;
+    // statistics of the lm_head epilogue: groups partials per slot
+    // ([groups][T]) and the logit of each slot's next draft
+    const VStat* lstat;
+    const float* zd;
+    int groups;
 };
-
-__device__ __forceinline__ void merge_ms(float& m, float& s, float m2, float s2) {
-    if (m2 == -INFINITY) return;
-    if (m == -INFINITY) { m = m2; s = s2; return; }
-    if (m2 > m) { s = s * expf(m - m2) + s2; m = m2; }
-    else s += s2 * expf(m2 - m);
-}
 
 // A1: per (slot, vocab chunk): max, sum of exp(z - max), argmax (lowest index)
 __global__ __launch_bounds__(256) void k_samp_a1(SampP p) {
@@ -98,30 +99,59 @@ __global__ __launch_bounds__(256) void k_samp_a1(SampP p) {
     }
 }
 
-// A2: one thread per slot: merge the chunk partials in chunk order and take
-// the slot's accept decision for the draft that follows it
+// A2: merge a slot's partials and take its accept decision for the draft
+// that follows it.  Unfused: one wave per slot, lane i holding vocab chunk
+// i's partial.  FUSED: one workgroup per slot over the lm_head workgroups'
+// records ([T][groups]); thread i merges records i, i + 256, ... in that
+// order, then the lanes and the four waves are merged.  Ties of the argmax
+// go to the lowest index either way.
+template <bool FUSED>
 __global__ __launch_bounds__(256) void k_samp_a2(SampP p, int chunks) {
-    const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+    __shared__ VStat wst[4];
     const int lane = threadIdx.x & 63;
     const BatchView& bv = p.bv;
-    if (t >= bv.T) return;
-    // lane i holds chunk i's partial; a fixed butterfly merges them (ties of
-    // the argmax to the lowest index, so the result is the chunk-order one)
-    float M = -INFINITY, S = 0.f, BV = -INFINITY;
+    int t;
+    float M = -INFINITY, S = 0.f;
     int BI = 0x7fffffff;
-    if (lane < chunks) {
-        const float4 e = *(const float4*)(p.spartA + ((size_t)t * kVocabChunks + lane) * 4);
-        M = e.x; S = e.y; BV = e.z; BI = __float_as_int(e.w);
-    }
+    if (FUSED) {
+        t = blockIdx.x;
+        const VStat* rec = p.lstat + (size_t)t * p.groups;
+        VStat a = vstat_empty();
+        for (int g0 = 0; g0 < p.groups; g0 += 4 * 256) {
+            VStat r[4];
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const float m2 = __shfl_xor(M, o, 64), s2 = __shfl_xor(S, o, 64);
-        const float v2 = __shfl_xor(BV, o, 64);
-        const int i2 = __shfl_xor(BI, o, 64);
-        // both partners combine the pair in the same (lower lane first) order
-        if (lane & o) { float mt = M, st = S; M = m2; S = s2; merge_ms(M, S, mt, st); }
-        else merge_ms(M, S, m2, s2);
-        if (v2 > BV || (v2 == BV && i2 < BI)) { BV = v2; BI = i2; }
+            for (int u = 0; u < 4; ++u) {
+                const int g = g0 + (int)threadIdx.x + u * 256;
+                r[u] = g < p.groups ? rec[g] : vstat_empty();
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) a = vstat_merge(a, r[u]);
+        }
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) a = vstat_merge(a, vstat_shfl_xor(a, o));
+        if (lane == 0) wst[threadIdx.x >> 6] = a;
+        __syncthreads();
+        if (threadIdx.x >= 64) return;
+        a = wst[0];
+#pragma unroll
+        for (int w = 1; w < 4; ++w) a = vstat_merge(a, wst[w]);
+        M = a.m; S = a.s; BI = a.i;
+    } else {
+        t = blockIdx.x * 4 + (threadIdx.x >> 6);
+        if (t >= bv.T) return;
+        float BV = -INFINITY;
+        if (lane < chunks) {
+            const float4 e = *(const float4*)(p.spartA + ((size_t)t * kVocabChunks + lane) * 4);
+            M = e.x; S = e.y; BV = e.z; BI = __float_as_int(e.w);
+        }
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const float m2 = __shfl_xor(M, o, 64), s2 = __shfl_xor(S, o, 64);
+            const float v2 = __shfl_xor(BV, o, 64);
+            const int i2 = __shfl_xor(BI, o, 64);
+            merge_ms(M, S, m2, s2);
+            if (v2 > BV || (v2 == BV && i2 < BI)) { BV = v2; BI = i2; }
+        }
     }
     if (BI == 0x7fffffff) BI = 0;  // a row of -inf logits only
     const int b = bv.slot_b[t], j = bv.slot_j[t];
@@ -145,7 +175,8 @@ __global__ __launch_bounds__(256) void k_samp_a2(SampP p, int chunks) {
         if (bv.mode == 0) acc = (d == BI) ? 1.f : 0.f;
         else if (bv.mode == 2) acc = 1.f;
         else {
-            const float pd = expf(p.logits[(size_t)t * p.V + d] - M) / S;
+            const float zdv = FUSED ? p.zd[t] : p.logits[(size_t)t * p.V + d];
+            const float pd = expf(zdv - M) / S;
             const float qd = bv.qk > 0 ? qsp : bv.q[(size_t)di * p.V + d];
             const float r = pd / qd;
             float u;
@@ -357,7 +388,7 @@ void launch_noalloc_stage(const NoallocMeta& m, const NoallocTables& t, const in
 }
 
 void launch_sampler(const Dims& D, const BatchView& bv, const SlotBufs& sb, const float* logits,
-                    hipStream_t s) {
+                    hipStream_t s, int groups) {
     SampP p;
     p.bv = bv;
     p.logits = logits;
@@ -368,9 +399,16 @@ void launch_sampler(const Dims& D, const BatchView& bv, const SlotBufs& sb, cons
     p.spartB = sb.spartB;
     p.result = sb.result;
     p.bmax = sb.bmax;
+    p.lstat = reinterpret_cast<const VStat*>(sb.lstat);
+    p.zd = sb.zd;
+    p.groups = groups;
     const int chunks = (D.V + p.cw - 1) / p.cw;
-    hipLaunchKernelGGL(k_samp_a1, dim3(bv.T, chunks), dim3(256), 0, s, p);
-    hipLaunchKernelGGL(k_samp_a2, dim3((bv.T + 3) / 4), dim3(256), 0, s, p, chunks);
+    if (groups > 0) {
+        hipLaunchKernelGGL(k_samp_a2<true>, dim3(bv.T), dim3(256), 0, s, p, chunks);
+    } else {
+        hipLaunchKernelGGL(k_samp_a1, dim3(bv.T, chunks), dim3(256), 0, s, p);
+        hipLaunchKernelGGL(k_samp_a2<false>, dim3((bv.T + 3) / 4), dim3(256), 0, s, p, chunks);
+    }
     if (bv.mode == 1) {
         if (bv.qk > 0)
             hipLaunchKernelGGL(k_samp_b1<true>, dim3(bv.B, chunks), dim3(256), 0, s, p);

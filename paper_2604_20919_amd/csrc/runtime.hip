@@ -39,7 +39,7 @@ struct Layout {
         st_ioff, st_flags, st_prow, st_bytes;
     // slot buffers (byte offsets within the slot)
     size_t stage, tok, cs, x, ssq, h, ffn, qbuf, attn, apart, aml, gpart, logits, sstat, spart,
-        spartB, result, slot_bytes;
+        spartB, lstat, zd, dnext, result, slot_bytes;
     size_t gpart_floats;
     int nsq;
     // global region after the slots
@@ -78,6 +78,7 @@ sd_status validate_config(const sd_config* c) {
     if (c->max_pending < 1 || c->max_pending > kMaxPending) return SD_EINVAL;
     if (!(c->rope_base > 1.0f) || !(c->rms_eps >= 0.0f)) return SD_EINVAL;
     if (c->qk_norm != 0 && c->qk_norm != 1) return SD_EINVAL;
+    if (c->logits_out < SD_LOGITS_AS_NEEDED || c->logits_out > SD_LOGITS_UNFUSED) return SD_EINVAL;
     if (c->dtype == SD_BF16) {
         // MFMA kernels: 128-wide heads, k dimensions in whole LDS chunks and
         // output widths in whole 128-column tiles
@@ -150,6 +151,9 @@ Layout plan(const sd_config& c) {
     L.sstat = take((size_t)L.Tmax * 4 * 4);
     L.spart = take((size_t)L.Tmax * kVocabChunks * 4 * 4);
     L.spartB = take((size_t)L.Bmax * kVocabChunks * 4 * 4);
+    L.lstat = take(D.bf16 ? (size_t)lm_stat_groups_max(D.V) * L.Tmax * 4 * 4 : 16);
+    L.zd = take((size_t)L.Tmax * 4);
+    L.dnext = take((size_t)L.Tmax * 4);
     L.result = take((size_t)(2 * L.Bmax + 4) * 4);
     L.slot_bytes = s;
     L.total = align_up(L.slot_bytes * (size_t)c.max_pending);
@@ -185,6 +189,7 @@ struct User {
 struct Slot {
     bool pending = false;
     bool sample_only = false;
+    bool logits_ok = false;  // the pending pass stored every slot's logits
     int batch = -1;
     int B = 0, T = 0, nd = 0;
     std::vector<int> users;  // global ids in batch order
@@ -405,7 +410,11 @@ struct ProfScope {
     }
 };
 
-sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t st) {
+// write_logits: store the fp32 logits of every slot; *groups receives the
+// number of phase-A statistic records per slot the lm_head writes (0: the
+// sampler computes phase A from the logits)
+sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t st, bool write_logits,
+                          int* groups) {
     const Dims& D = c->D;
     const SlotBufs& sb = s.bufs;
     const int T = bv.T;
@@ -519,9 +528,20 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
     lm.N = D.V;
     lm.K = D.d;
     lm.T = T;
-    lm.epi = EPI_STORE;
-    lm.out = sb.logits;
     lm.ldo = D.V;
+    *groups = 0;
+    if (D.bf16 && c->cfg.logits_out != SD_LOGITS_UNFUSED) {
+        // phase-A statistics from the epilogue; logits only when asked for
+        lm.epi = EPI_LMSTAT;
+        lm.out = write_logits ? sb.logits : nullptr;
+        lm.lstat = sb.lstat;
+        lm.zd = sb.zd;
+        lm.dnext = sb.dnext;
+        lm.groups_out = groups;
+    } else {
+        lm.epi = EPI_STORE;
+        lm.out = sb.logits;
+    }
     launch_gemm(D, lm, sb, st);
     return hip_status(hipGetLastError());
 }
@@ -679,6 +699,9 @@ sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_poo
         b.sstat = (float*)(s.base + L.sstat);
         b.spart = (float*)(s.base + L.spart);
         b.spartB = (float*)(s.base + L.spartB);
+        b.lstat = (float*)(s.base + L.lstat);
+        b.zd = (float*)(s.base + L.zd);
+        b.dnext = (int32_t*)(s.base + L.dnext);
         b.result = (int32_t*)(s.base + L.result);
         b.bmax = L.Bmax;
     }
@@ -813,6 +836,16 @@ sd_status sd_kv_read(sd_ctx* c, int32_t user, int32_t layer, int32_t pos0, int32
     return kv_copy(c, user, layer, pos0, n, k, v, stream, 0);
 }
 
+// Whether a verify pass stores the fp32 logits of every slot: always with
+// SD_LOGITS_ALL / SD_LOGITS_UNFUSED or the fp32 configuration; otherwise
+// only when something reads them after phase A -- the stochastic race of
+// phase B (the stop slot is known only once every slot's statistics are
+// complete) or the probabilities of a decode step.
+static bool pass_writes_logits(const sd_ctx* c, int mode, const float* probs) {
+    return !c->D.bf16 || c->cfg.logits_out != SD_LOGITS_AS_NEEDED || mode == SD_STOCHASTIC ||
+           probs != nullptr;
+}
+
 // Device work of one pass: staging upload, forward + sampler (or the
 // sampler alone on caller logits), result download.  No allocation, no
 // memset: the whole sequence can be captured into a graph.
@@ -826,10 +859,11 @@ static sd_status enqueue_pass(sd_ctx* c, Slot& s, const BatchView& bv, const flo
             launch_sampler(c->D, bv, s.bufs, logits, st);
             rs = hip_status(hipGetLastError());
         } else {
-            rs = enqueue_forward(c, s, bv, st);
+            int groups = 0;
+            rs = enqueue_forward(c, s, bv, st, pass_writes_logits(c, bv.mode, probs), &groups);
             if (rs == SD_OK) {
                 ProfScope ps(c, SD_K_SAMPLER, st);
-                launch_sampler(c->D, bv, s.bufs, s.bufs.logits, st);
+                launch_sampler(c->D, bv, s.bufs, s.bufs.logits, st, groups);
                 if (probs) launch_probs(c->D, bv, s.bufs, s.bufs.logits, probs, st);
                 rs = hip_status(hipGetLastError());
             }
@@ -951,6 +985,7 @@ static sd_status submit(sd_ctx* c, int32_t batch, int32_t n_users, const int32_t
     s.nd = nd;
     s.batch = batch;
     s.sample_only = sample_only;
+    s.logits_ok = sample_only || pass_writes_logits(c, mode, probs);
     int n_items = 0, rows_max = 0;
     build_stage(c, s, mode, !sample_only, &n_items, &rows_max);
     BatchView bv = make_view(c, s);
@@ -1070,7 +1105,7 @@ sd_status sd_accept(sd_ctx* c, int32_t batch, int32_t* n_accepted, int32_t* out_
 sd_status sd_debug_logits(sd_ctx* c, int32_t batch, float* dst, sd_stream stream) {
     if (!c || batch < 0 || !dst) return SD_EINVAL;
     Slot& s = c->slots[batch % c->cfg.max_pending];
-    if (!s.pending || s.batch != batch || s.sample_only) return SD_ESTATE;
+    if (!s.pending || s.batch != batch || s.sample_only || !s.logits_ok) return SD_ESTATE;
     hipStream_t st = (hipStream_t)stream;
     SD_HIP(hipStreamWaitEvent(st, s.done, 0));
     SD_HIP(hipMemcpyAsync(dst, s.bufs.logits, (size_t)s.T * c->D.V * 4, hipMemcpyDeviceToDevice, st));

@@ -72,6 +72,33 @@ __device__ __forceinline__ float wave_max(float v) {
     return v;
 }
 
+// Softmax statistics of a set of logits z: m = max z, s = sum exp(z - m),
+// and the argmax (value v, index i, the lowest index on ties).  Merging two
+// sets is exact in m, v and i and commutative bit for bit in s (the larger
+// maximum's sum plus the other one rescaled), so a butterfly leaves every
+// lane with the same result; only the grouping of the merges moves the
+// rounding of s.
+struct __attribute__((aligned(16))) VStat {
+    float m, s, v;
+    int i;
+};
+__device__ __forceinline__ VStat vstat_empty() { return VStat{-INFINITY, 0.f, -INFINITY, 0x7fffffff}; }
+__device__ __forceinline__ void merge_ms(float& m, float& s, float m2, float s2) {
+    if (m2 == -INFINITY) return;
+    if (m == -INFINITY) { m = m2; s = s2; return; }
+    if (m2 > m) { s = s * expf(m - m2) + s2; m = m2; }
+    else s += s2 * expf(m2 - m);
+}
+__device__ __forceinline__ VStat vstat_merge(VStat a, const VStat& b) {
+    merge_ms(a.m, a.s, b.m, b.s);
+    if (b.v > a.v || (b.v == a.v && b.i < a.i)) { a.v = b.v; a.i = b.i; }
+    return a;
+}
+__device__ __forceinline__ VStat vstat_shfl_xor(const VStat& a, int o) {
+    return VStat{__shfl_xor(a.m, o, 64), __shfl_xor(a.s, o, 64), __shfl_xor(a.v, o, 64),
+                 __shfl_xor(a.i, o, 64)};
+}
+
 // Block-wide sum for blockDim.x == 256 (4 waves); `red` holds 4 floats.
 __device__ __forceinline__ float block_sum_256(float v, float* red) {
     v = wave_sum(v);

@@ -99,6 +99,13 @@ struct SlotBufs {
     float* sstat;     // [Tmax][4] per-slot max, sum, argmax, accept
     float* spart;     // [Tmax * kVocabChunks][4] phase-A vocab-chunk partials
     float* spartB;    // [Bmax * kVocabChunks][4] phase-B partials
+    // phase-A statistics from the lm_head epilogue (bf16 configuration):
+    // per (slot, workgroup) row max, sum of exp(z - max), argmax value and
+    // index over the workgroup's vocab rows, [T][groups][4]; the logit of
+    // the draft that follows each slot; that draft token per slot (-1: none)
+    float* lstat;
+    float* zd;        // [Tmax]
+    int32_t* dnext;   // [Tmax]
     int32_t* result;  // [2*Bmax + 4]: n_acc, token, flags
     int bmax;
 };
@@ -108,7 +115,10 @@ void launch_prepare(const Dims& D, const BatchView& bv, const SlotBufs& sb, hipS
 void launch_attention(const Dims& D, const BatchView& bv, const SlotBufs& sb, const KVPool& kv,
                       int layer, hipStream_t s);
 
-enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+// EPI_LMSTAT (lm_head): phase-A statistics per (workgroup, slot) into
+// lstat, the logit of each slot's next draft into zd, and the logits
+// themselves into out when out is set; never split over k.
+enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LMSTAT = 3 };
 struct GemmCall {
     const void* X;    // [T][K] act type
     const void* Wp;   // bf16: packed weights (fragment order, virtual rows)
@@ -127,7 +137,16 @@ struct GemmCall {
     // rstd(t) = 1 / sqrt(sum_b norm_ss[t][b] / K + eps)
     const float* norm_ss;
     int norm_nb;
+    // EPI_LMSTAT outputs (see SlotBufs) and the number of statistic groups
+    // (workgroups) the launch writes
+    float* lstat;
+    float* zd;
+    const int32_t* dnext;
+    int* groups_out;
 };
+// Upper bound of the statistic groups of an lm_head of V rows (workgroups
+// of at least 128 rows, one more for rounding)
+inline int lm_stat_groups_max(int V) { return (V + 127) / 128 + 1; }
 // Returns the number of partial planes S (raw mode), else the splits used.
 int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_t s);
 // bf16 configuration: x[t] += sum_s part[s][t] (split order), h = x * gamma
@@ -151,8 +170,11 @@ size_t gemm_partial_floats(const Dims& D, int Tmax);
 void launch_pack(const void* s0, const void* s1, const void* s2, int seg1, int seg2, int mode,
                  int K, int vrows, void* dst, hipStream_t s);
 
+// Accept/resample of a batch.  groups = 0: phase A over the logits; groups
+// > 0: phase A from the lm_head epilogue's statistics (sb.lstat, groups
+// partials per slot, and sb.zd); logits then only feed phase B (stochastic).
 void launch_sampler(const Dims& D, const BatchView& bv, const SlotBufs& sb, const float* logits,
-                    hipStream_t s);
+                    hipStream_t s, int groups = 0);
 // probs[t][k] = exp(z[t][k] - m_t) / S_t from the sampler's per-slot
 // statistics (the same expression the race uses for p)
 void launch_probs(const Dims& D, const BatchView& bv, const SlotBufs& sb, const float* logits,

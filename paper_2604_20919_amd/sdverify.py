@@ -21,6 +21,7 @@ SD_OK, SD_EINVAL, SD_ENOMEM, SD_EHIP, SD_ESTATE, SD_EDEVICE, SD_ENOTIMPL, SD_ENO
 SD_NOALLOC_MAX_USERS, SD_NOALLOC_MAX_SLOTS, SD_NOALLOC_MAX_VOCAB = 64, 1024, 1 << 20
 SD_F32, SD_BF16 = 0, 1
 SD_GREEDY, SD_STOCHASTIC, SD_FORCE = 0, 1, 2
+SD_LOGITS_AS_NEEDED, SD_LOGITS_ALL, SD_LOGITS_UNFUSED = 0, 1, 2
 MODES = {"greedy": SD_GREEDY, "stochastic": SD_STOCHASTIC, "force": SD_FORCE}
 
 EXPORTS = ("sd_verify_query_sizes", "sd_verify_init", "sd_verify_destroy", "sd_user_reset",
@@ -36,7 +37,8 @@ class sd_config(ctypes.Structure):
         "n_layers", "d_model", "n_q_heads", "n_kv_heads", "head_dim", "d_ffn", "vocab", "qk_norm",
         "dtype", "page_tokens", "n_pages", "max_users", "max_draft", "max_batch_users",
         "max_batch_tokens", "max_ctx", "max_pending")] + [("rope_base", ctypes.c_float),
-                                                          ("rms_eps", ctypes.c_float)]
+                                                          ("rms_eps", ctypes.c_float),
+                                                          ("logits_out", ctypes.c_int32)]
 
 
 class sd_layer_weights(ctypes.Structure):
@@ -280,7 +282,7 @@ def sd_calib_mfma(sink_ptr: int, iters: int, stream: int = 0) -> float:
 
 def make_config(n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, vocab, qk_norm, dtype,
                 n_pages, max_users, max_draft, max_batch_users, max_batch_tokens, max_ctx,
-                max_pending=2, rope_base=1e6, rms_eps=1e-6) -> sd_config:
+                max_pending=2, rope_base=1e6, rms_eps=1e-6, logits_out=0) -> sd_config:
     return sd_config(n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, vocab, int(qk_norm),
                      int(dtype), 16, n_pages, max_users, max_draft, max_batch_users, max_batch_tokens,
-                     max_ctx, max_pending, float(rope_base), float(rms_eps))
+                     max_ctx, max_pending, float(rope_base), float(rms_eps), int(logits_out))

@@ -15,17 +15,18 @@ from . import sdverify as sv
 class Verifier:
     def __init__(self, shape, weight_ptrs: Dict[str, object], *, n_pages: int, max_users: int,
                  max_draft: int, max_batch_users: int, max_batch_tokens: int, max_ctx: int,
-                 max_pending: int = 2, device: str = "cuda"):
+                 max_pending: int = 2, logits_out: int = sv.SD_LOGITS_AS_NEEDED, device: str = "cuda"):
         """shape: object with n_layers, d_model, n_q_heads, n_kv_heads,
         head_dim, d_ffn, vocab, qk_norm, dtype ("f32"/"bf16"), rope_base,
         rms_eps.  weight_ptrs: "embed", "lm_head", "norm_f" -> device
         pointer, "layers" -> list of dicts with the sd_layer_weights field
-        names -> device pointer."""
+        names -> device pointer.  logits_out: which passes store fp32
+        logits (sd_config.logits_out; `logits()` needs them)."""
         dt = sv.SD_BF16 if shape.dtype == "bf16" else sv.SD_F32
         self.cfg = sv.make_config(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads,
                                   shape.head_dim, shape.d_ffn, shape.vocab, shape.qk_norm, dt,
                                   n_pages, max_users, max_draft, max_batch_users, max_batch_tokens,
-                                  max_ctx, max_pending, shape.rope_base, shape.rms_eps)
+                                  max_ctx, max_pending, shape.rope_base, shape.rms_eps, logits_out)
         kv_bytes, ws_bytes, wp_bytes = sv.sd_verify_query_sizes(self.cfg)
         self.kv_bytes, self.ws_bytes, self.wp_bytes = kv_bytes, ws_bytes, wp_bytes
         # 256-byte aligned by the caching allocator

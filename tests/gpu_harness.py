@@ -13,6 +13,7 @@ import torch
 import oracle
 import workload as wl
 from workload.device import DeviceWeights, batch_to_device, kv_rows
+from paper_2604_20919_amd import sdverify as sdv
 from paper_2604_20919_amd.verifier import Verifier
 
 
@@ -24,7 +25,11 @@ def layer_ptrs(dw: DeviceWeights):
 
 
 def make_verifier(w: wl.Workload, dw: DeviceWeights, max_pending: int = 2, extra_ctx: int = 0,
-                  max_batch_tokens: Optional[int] = None, max_draft: Optional[int] = None) -> Verifier:
+                  max_batch_tokens: Optional[int] = None, max_draft: Optional[int] = None,
+                  logits_out: int = sdv.SD_LOGITS_ALL) -> Verifier:
+    """A context for workload w.  Parity tests read every pass's logits, so
+    by default every pass stores them (the decisions still come from the
+    lm_head's fused statistics)."""
     m = w.model
     max_ctx = int((w.prefix_len + w.draft_len).max()) + 1 + extra_ctx
     pages = int(sum((p + l + 1 + extra_ctx + 15) // 16 for p, l in zip(w.prefix_len, w.draft_len))) + 8
@@ -32,7 +37,7 @@ def make_verifier(w: wl.Workload, dw: DeviceWeights, max_pending: int = 2, extra
     B = max(int((w.assign == n).sum()) for n in range(w.n_batches))
     return Verifier(m, layer_ptrs(dw), n_pages=pages, max_users=w.n_users,
                     max_draft=max_draft or int(w.draft_len.max()), max_batch_users=B, max_batch_tokens=T,
-                    max_ctx=max_ctx, max_pending=max_pending)
+                    max_ctx=max_ctx, max_pending=max_pending, logits_out=logits_out)
 
 
 def gpu_prefill(v: Verifier, user: int, tokens: np.ndarray, n_users: int, chunk: int = 16):
