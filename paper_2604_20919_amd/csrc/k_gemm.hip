@@ -476,10 +476,19 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 // a+1..2a the lo plane of slots 0..32a-1.  That is one tile fewer than two
 // planes of a + 1 tiles each; the epilogue adds each slot's hi and lo sums
 // (same lane of tiles m and m + a + 1, or lanes l and l ^ 16 of tile a).
-template <int MT, int NS, int KC, int EPI, bool SPLIT, int NW, int PL, int PD, bool PK = false>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, 2)))
+//
+// CS (column split): CS waves share one row unit and each multiplies MT/CS
+// of the slot tiles.  With NS = 2 (64 weight rows per wave) every B
+// fragment read from LDS then feeds two MFMAs instead of one: four SIMDs
+// issuing 32-cycle MFMAs ask for 64 bytes per clock of LDS reads instead
+// of 128, at the same accumulator count per wave.
+template <int MT, int NS, int KC, int EPI, bool SPLIT, int NW, int PL, int PD, bool PK = false, int CS = 1>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW > 8 ? NW / 4 : 1, NW > 8 ? NW / 4 : 2)))
 void k_gemm32(GemmP p) {
     static_assert(!PK || (PL == 2 && MT % 2 == 1), "packed planes: two planes, 2a + 1 tiles");
+    static_assert(MT % CS == 0 && NW % CS == 0 && (CS == 1 || (!PK && EPI != EPI_LMSTAT)),
+                  "column split: whole tiles per wave, no packed planes, no lm_head statistics");
+    constexpr int MTW = MT / CS;         // slot tiles per wave
     constexpr int PLS = PK ? 1 : PL;     // staged (and multiplied) planes
     constexpr int PA = MT / 2;           // packed: full tiles per plane
     constexpr int NTH = 64 * NW;         // threads per workgroup
@@ -492,8 +501,14 @@ void k_gemm32(GemmP p) {
     constexpr int XPT = (NPC + NTH - 1) / NTH;  // X pieces per thread
     constexpr bool XEVEN = NPC % NTH == 0;
     constexpr int PLANE = MT * 32 * LDX;  // LDS elements per plane
-    static_assert(2 * PLS * PLANE * 2 <= 160 * 1024, "X staging exceeds LDS");
-    __shared__ __attribute__((aligned(16))) bf16_t xs[2][PLS * PLANE];
+    // NXB X staging buffers of XBUF elements; the split epilogue stages its
+    // partial sums in the same memory, which may need more
+    constexpr int XBUF = PLS * PLANE;
+    constexpr int NXB = 2;
+    constexpr int STG_BYTES = SPLIT ? CS * 32 * (NW / CS * NS * 32 + 4) * 4 : 0;
+    constexpr int XS_ELEMS = 2 * NXB * XBUF >= STG_BYTES ? NXB * XBUF : STG_BYTES / 2;
+    static_assert(XS_ELEMS * 2 <= 160 * 1024, "staging exceeds LDS");
+    __shared__ __attribute__((aligned(16))) bf16_t xs[XS_ELEMS];
     __shared__ float rsl[SPLIT ? 1 : MT * ROWS_PER_TILE];  // per-slot RMSNorm factor
 
     const int split = SPLIT ? blockIdx.x % p.S : 0;
@@ -505,7 +520,9 @@ void k_gemm32(GemmP p) {
     // per-lane offsets, uniform chunk offsets.  Out-of-range reads return 0
     // (and fetch nothing: a wave without a unit points past the buffer).
     const int wv = __builtin_amdgcn_readfirstlane(wave);
-    const int unit = wgi * p.G / p.WPS + wv;
+    const int half = CS == 1 ? 0 : wv % CS;   // which MT/CS slot tiles
+    const int m0 = half * MTW;
+    const int unit = wgi * p.G / p.WPS + wv / CS;
     const bool has_unit = unit < (wgi + 1) * p.G / p.WPS;
     const uint64_t wbytes = (uint64_t)p.vcols * (uint64_t)p.K * 2u;
     const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
@@ -525,11 +542,11 @@ void k_gemm32(GemmP p) {
     const __amdgpu_buffer_rsrc_t xres =
         __builtin_amdgcn_make_buffer_rsrc((void*)p.X, (short)0, PL * p.T * p.K * 2, 0x00020000);
 
-    f32x16 acc[NS][MT];
+    f32x16 acc[NS][MTW];
 #pragma unroll
     for (int s = 0; s < NS; ++s)
 #pragma unroll
-        for (int m = 0; m < MT; ++m)
+        for (int m = 0; m < MTW; ++m)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[s][m][e] = 0.f;
 
@@ -576,7 +593,7 @@ void k_gemm32(GemmP p) {
             const int idx = threadIdx.x + i * NTH;
             const int pl = idx / NPP, pi = idx % NPP;
             if (XEVEN || idx < NPC)
-                *(uint4*)(&xs[buf][pl * PLANE + (pi / PPR) * LDX + (pi % PPR) * 8]) = x[i];
+                *(uint4*)(&xs[buf * XBUF + pl * PLANE + (pi / PPR) * LDX + (pi % PPR) * 8]) = x[i];
         }
     };
     auto load_w = [&](bf16x8 (&w)[KS][NS], int c) {
@@ -600,20 +617,22 @@ void k_gemm32(GemmP p) {
                 xf[pl][m] = *(const bf16x8*)(xb + pl * PLANE + (m * 32 + lc) * LDX + ks * 16 + 8 * lh);
     };
     auto compute = [&](int buf, const bf16x8 (&w)[KS][NS]) {
-        const bf16_t* xb = xs[buf];
-        bf16x8 xf[2][PLS][MT];
-        read_x(xf[0], xb, 0);
+        if constexpr (CS == 1) {
+            const bf16_t* xb = xs + buf * XBUF;
+            bf16x8 xf[2][PLS][MT];
+            read_x(xf[0], xb, 0);
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            if (ks + 1 < KS) read_x(xf[(ks + 1) & 1], xb, ks + 1);
+            for (int ks = 0; ks < KS; ++ks) {
+                if (ks + 1 < KS) read_x(xf[(ks + 1) & 1], xb, ks + 1);
 #pragma unroll
-            for (int pl = 0; pl < PLS; ++pl)
+                for (int pl = 0; pl < PLS; ++pl)
 #pragma unroll
-                for (int m = 0; m < MT; ++m)
+                    for (int m = 0; m < MT; ++m)
 #pragma unroll
-                    for (int s = 0; s < NS; ++s)
-                        acc[s][m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w[ks][s], xf[ks & 1][pl][m],
-                                                                             acc[s][m], 0, 0, 0);
+                        for (int s = 0; s < NS; ++s)
+                            acc[s][m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(w[ks][s], xf[ks & 1][pl][m],
+                                                                                 acc[s][m], 0, 0, 0);
+            }
         }
     };
 
@@ -643,6 +662,55 @@ void k_gemm32(GemmP p) {
             if (sl < NSL) rsl[sl] = p.nss != nullptr ? rstd_of(p, ssv[i]) : 1.0f;
         }
     }
+    if constexpr (CS > 1) {
+        // Two X buffers; per chunk c: the X loads of chunk c + 1 are issued
+        // first; phases (k-step, plane) follow, the next phase's fragments
+        // requested before this phase's NS * MTW MFMAs; after the last plane
+        // of a k-step its weight registers are reloaded with the same k-step
+        // of chunk c + 1 (one register set, each fragment requested about a
+        // chunk ahead); X(c + 1) is then stored to the other buffer and the
+        // barrier publishes it.
+        constexpr int NPH = KS * PLS;
+        static_assert(NPH % 2 == 0, "phase fragments alternate between two register sets");
+        bf16x8 xq[2][MTW];
+        auto read_phase = [&](bf16x8 (&xf)[MTW], int buf, int ph) {
+            const bf16_t* xb = xs + buf * XBUF;
+            const int ks = ph / PLS, pl = ph % PLS;
+#pragma unroll
+            for (int m = 0; m < MTW; ++m)
+                xf[m] = *(const bf16x8*)(xb + pl * PLANE + ((m0 + m) * 32 + lc) * LDX + ks * 16 + 8 * lh);
+        };
+        auto load_w_ks = [&](bf16x8 (&w)[NS], int c, int ks) {
+#pragma unroll
+            for (int s = 0; s < NS; ++s)
+                w[s] = __builtin_bit_cast(
+                    bf16x8, __builtin_amdgcn_raw_buffer_load_b128(wres, woff[s], (c * KS + ks) * 512, kWeightAux));
+        };
+        store_x(xr[0], 0);
+        __syncthreads();
+        read_phase(xq[0], 0, 0);
+        for (int c = c_begin; c < c_end; ++c) {
+            const int b = (c - c_begin) & 1;
+            const int cn = min(c + 1, c_last);
+            load_x(xr[0], cn);
+#pragma unroll
+            for (int ph = 0; ph < NPH; ++ph) {
+                if (ph + 1 < NPH) read_phase(xq[(ph + 1) & 1], b, ph + 1);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int m = 0; m < MTW; ++m)
+#pragma unroll
+                    for (int s = 0; s < NS; ++s)
+                        acc[s][m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wr[0][ph / PLS][s], xq[ph & 1][m],
+                                                                             acc[s][m], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
+                if (ph % PLS == PLS - 1) load_w_ks(wr[0][ph / PLS], cn, ph / PLS);
+            }
+            store_x(xr[0], b ^ 1);
+            __syncthreads();
+            read_phase(xq[0], b ^ 1, 0);
+        }
+    } else {
     store_x(xr[0], 0);
     __syncthreads();
     for (int c0 = c_begin; c0 < c_end; c0 += NB) {
@@ -658,6 +726,7 @@ void k_gemm32(GemmP p) {
             store_x(xr[(u + 1) % NB], ((c - c_begin) & 1) ^ 1);
             __syncthreads();
         }
+    }
     }
 
     // Accumulator layout: lane l holds slot t = 32*m + l % 32 and, in
@@ -684,7 +753,7 @@ void k_gemm32(GemmP p) {
         constexpr int MTO = PK ? PA + 1 : MT;
         constexpr int NSLOT = MTO * 32;
         static_assert(NW * NSLOT * (int)sizeof(VStat) <= (int)sizeof(xs), "statistics staging exceeds LDS");
-        VStat* stg = reinterpret_cast<VStat*>(&xs[0][0]);
+        VStat* stg = reinterpret_cast<VStat*>(xs);
 #pragma unroll
         for (int m = 0; m < MTO; ++m) {
             const int t = m * 32 + lc;
@@ -717,34 +786,42 @@ void k_gemm32(GemmP p) {
         return;
     }
     if constexpr (SPLIT) {
-        // one 32-slot tile at a time through the (now idle) staging buffer
-        constexpr int WR = NW * NS * 32;  // weight rows of the workgroup
+        // slot tiles m0 + m of every column half at a time through the (now
+        // idle) staging buffer, staged as [half][slot][row]
+        constexpr int WR = NW / CS * NS * 32;  // weight rows of the workgroup
         constexpr int LDR = WR + 4;
-        static_assert(32 * LDR * 4 <= (int)sizeof(xs), "partial staging exceeds the X buffer");
-        float* stg = reinterpret_cast<float*>(&xs[0][0]);
+        static_assert(CS * 32 * LDR * 4 <= (int)sizeof(xs), "partial staging exceeds the X buffer");
+        float* stg = reinterpret_cast<float*>(xs);
         const int u0 = wgi * p.G / p.WPS;
         const int nrow = ((wgi + 1) * p.G / p.WPS - u0) * NS * 32;
+        const int wrow = wv / CS;  // row unit within the workgroup
 #pragma unroll
-        for (int m = 0; m < (PK ? PA + 1 : MT); ++m) {
-            const int nsl = min(PK && m == PA ? 16 : 32, p.T - m * 32);
-            if (nsl <= 0) break;
+        for (int m = 0; m < (PK ? PA + 1 : MTW); ++m) {
+            if (m * 32 >= p.T) break;  // so are the other halves' tiles m + MTW * h
             if (has_unit) {
 #pragma unroll
                 for (int s = 0; s < NS; ++s)
 #pragma unroll
                     for (int q = 0; q < 4; ++q)
-                        *(f32x4*)(stg + lc * LDR + (wv * NS + s) * 32 + 8 * q + 4 * lh) =
+                        *(f32x4*)(stg + (half * 32 + lc) * LDR + (wrow * NS + s) * 32 + 8 * q + 4 * lh) =
                             f32x4{acc[s][m][4 * q], acc[s][m][4 * q + 1], acc[s][m][4 * q + 2], acc[s][m][4 * q + 3]};
             }
             __syncthreads();
-            store_partial_rows<NTH, WR>(p, stg, LDR, split, m * 32, nsl, u0 * NS * 32, nrow);
+#pragma unroll
+            for (int h = 0; h < CS; ++h) {
+                const int tile = h * MTW + m;
+                const int nsl = min(PK && m == PA ? 16 : 32, p.T - tile * 32);
+                if (nsl > 0)
+                    store_partial_rows<NTH, WR>(p, stg + h * 32 * LDR, LDR, split, tile * 32, nsl, u0 * NS * 32,
+                                                nrow);
+            }
             __syncthreads();
         }
         return;
     }
 #pragma unroll
-    for (int m = 0; m < (PK ? PA + 1 : MT); ++m) {
-        const int t = m * 32 + lc;
+    for (int m = 0; m < (PK ? PA + 1 : MTW); ++m) {
+        const int t = (m0 + m) * 32 + lc;
         if (!has_unit || t >= p.T || (PK && m == PA && lc >= 16)) continue;
         const float sc = rsl[t];
 #pragma unroll
@@ -892,13 +969,17 @@ __global__ void k_gemm_f32(GemmF p) {
 //     chunk fits in LDS.
 // FILL: choose the k splits to fill one wave of workgroups (the eight-wave
 // rule of choose_splits) even for four-wave tiles.
-struct GemmShape { int F, MT, NSUB, KC, NW, PD, PK, FILL = 0; };
+// F: MFMA form (16 or 32 rows); MT: slot tiles; NSUB: 16- or 32-row groups
+// per wave; KC: k per chunk; NW: waves per workgroup; PD: prefetch depth;
+// PK: packed planes; FILL: split policy of eight-wave tiles; CS: column
+// split (waves per row unit)
+struct GemmShape { int F, MT, NSUB, KC, NW, PD, PK, FILL = 0, CS = 1; };
 
 constexpr int kT32 = 97;  // first slot count served by the 32x32 form
 
 static int cu_count();
 
-static GemmShape shape_for(int T, int vcols, bool raw, int K) {
+static GemmShape shape_for(int T, int vcols, bool raw, int K, bool lmstat) {
     const bool wide = vcols % 256 == 0;
     // packed planes (2a + 1 tiles for 32a < T <= 32a + 16): split-K
     // partial GEMMs at 65..80 slots (QKV / O / down at T = 80: 29.5 / 23.7
@@ -933,7 +1014,14 @@ static GemmShape shape_for(int T, int vcols, bool raw, int K) {
     // of 2 x 256 rows then fits one workgroup of 256 weight rows per CU);
     // same-box probe at T = 240: gate/up 292 vs 392 us, QKV 63 vs 99, O 51
     // vs 93, down 143 vs 210 us against four waves with 64-k chunks
-    if (mt <= 8) return w8 ? GemmShape{32, 8, 1, 32, 8, 1, 0} : GemmShape{32, 8, 1, 64, 4, 1, 0};
+    if (mt <= 8) {
+        // 64-row units shared by two waves (four slot tiles each) with 64-k
+        // chunks: every B fragment feeds two MFMAs.  Same-box timing of the
+        // 32B shapes at T = 229 in isolation: gate/up 263 vs 293 us, QKV 57
+        // vs 59, O 52 vs 56, down 121 vs 137 us against 32-row units
+        if (vcols % 64 == 0 && !lmstat) return GemmShape{32, 8, 2, 64, 8, 1, 0, 0, 2};
+        return w8 ? GemmShape{32, 8, 1, 32, 8, 1, 0} : GemmShape{32, 8, 1, 64, 4, 1, 0};
+    }
     if (mt <= 10) return {32, 10, 1, 32, 4, 1, 0};
     if (mt <= 13) return {32, 13, 1, 16, 4, 1, 0};
     return {0, 0, 0, 0, 0, 0, 0};
@@ -944,7 +1032,7 @@ typedef void (*ReduceFn)(GemmP);
 
 // Activations always come as two planes (hi, lo); split-K kernels write raw
 // partial planes and the epilogue runs in the reducer.
-template <int F, int MT, int NW, int KC, int PD, bool SPLIT, bool PK = false>
+template <int F, int MT, int NW, int KC, int PD, bool SPLIT, bool PK = false, int CS = 1, int NS = 1>
 static GemmFn pick_epi(int epi) {
     if constexpr (F == 16) {
         if (SPLIT) return k_gemm16<MT, 2, KC, EPI_STORE, true, NW, 2, PD>;
@@ -955,12 +1043,14 @@ static GemmFn pick_epi(int epi) {
             default: return k_gemm16<MT, 2, KC, EPI_STORE, false, NW, 2, PD>;
         }
     } else {
-        if (SPLIT) return k_gemm32<MT, 1, KC, EPI_STORE, true, NW, 2, PD, PK>;
+        if (SPLIT) return k_gemm32<MT, NS, KC, EPI_STORE, true, NW, 2, PD, PK, CS>;
         switch (epi) {
-            case EPI_RESID: return k_gemm32<MT, 1, KC, EPI_RESID, false, NW, 2, PD, PK>;
-            case EPI_SWIGLU: return k_gemm32<MT, 1, KC, EPI_SWIGLU, false, NW, 2, PD, PK>;
-            case EPI_LMSTAT: return k_gemm32<MT, 1, KC, EPI_LMSTAT, false, NW, 2, PD, PK>;
-            default: return k_gemm32<MT, 1, KC, EPI_STORE, false, NW, 2, PD, PK>;
+            case EPI_RESID: return k_gemm32<MT, NS, KC, EPI_RESID, false, NW, 2, PD, PK, CS>;
+            case EPI_SWIGLU: return k_gemm32<MT, NS, KC, EPI_SWIGLU, false, NW, 2, PD, PK, CS>;
+            case EPI_LMSTAT:
+                if constexpr (CS == 1) return k_gemm32<MT, NS, KC, EPI_LMSTAT, false, NW, 2, PD, PK, CS>;
+                else return nullptr;
+            default: return k_gemm32<MT, NS, KC, EPI_STORE, false, NW, 2, PD, PK, CS>;
         }
     }
 }
@@ -994,8 +1084,10 @@ static GemmFn pick(const GemmShape& sh, int epi) {
         if (sh.MT == 7) return pick_epi<32, 7, 8, 64, 1, SPLIT, true>(epi);
         return nullptr;
     }
-    if (sh.F == 32 && sh.MT == 8)
+    if (sh.F == 32 && sh.MT == 8) {
+        if (sh.CS == 2) return pick_epi<32, 8, 8, 64, 1, SPLIT, false, 2, 2>(epi);
         return sh.NW == 8 ? pick_epi<32, 8, 8, 32, 1, SPLIT>(epi) : pick_epi<32, 8, 4, 64, 1, SPLIT>(epi);
+    }
     if (sh.F == 32 && sh.MT == 10) return pick_epi<32, 10, 4, 32, 1, SPLIT>(epi);
     if (sh.F == 32 && sh.MT == 13) return pick_epi<32, 13, 4, 16, 1, SPLIT>(epi);
     return sh.NW == 8 ? pick_nw<8, SPLIT>(sh, epi) : pick_nw<4, SPLIT>(sh, epi);
@@ -1077,8 +1169,8 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
         return 1;
     }
     const int vcols = g.epi == EPI_SWIGLU ? 2 * g.N : g.N;
-    const GemmShape sh = shape_for(g.T, vcols, g.raw != 0, g.K);
-    const int unit_rows = sh.F * sh.NSUB;  // weight rows of one wave
+    const GemmShape sh = shape_for(g.T, vcols, g.raw != 0, g.K, g.epi == EPI_LMSTAT);
+    const int unit_rows = sh.F * sh.NSUB;  // weight rows of one row unit
     GemmP p;
     p.X = (const bf16_t*)g.X;
     p.Wp = (const bf16_t*)g.Wp;
@@ -1090,7 +1182,8 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
     // workgroups of NW waves; a last partial workgroup when the row count is
     // not a multiple of NW units (its surplus waves load and store nothing)
     const int units = p.vcols / unit_rows;
-    p.tiles = (units + sh.NW - 1) / sh.NW;
+    const int upw = sh.NW / sh.CS;  // row units per workgroup
+    p.tiles = (units + upw - 1) / upw;
     int S = g.epi == EPI_LMSTAT ? 1 : choose_splits(p.tiles, p.kchunks, sh.FILL ? 8 : sh.NW);
     while (S > 1 && (size_t)S * g.T * p.vcols > sb.gpart_floats) {
         int t = S - 1;
