@@ -486,8 +486,8 @@ template <int MT, int NS, int KC, int EPI, bool SPLIT, int NW, int PL, int PD, b
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW > 8 ? NW / 4 : 1, NW > 8 ? NW / 4 : 2)))
 void k_gemm32(GemmP p) {
     static_assert(!PK || (PL == 2 && MT % 2 == 1), "packed planes: two planes, 2a + 1 tiles");
-    static_assert(MT % CS == 0 && NW % CS == 0 && (CS == 1 || (!PK && EPI != EPI_LMSTAT)),
-                  "column split: whole tiles per wave, no packed planes, no lm_head statistics");
+    static_assert(MT % CS == 0 && NW % CS == 0 && (CS == 1 || !PK),
+                  "column split: whole tiles per wave, no packed planes");
     constexpr int MTW = MT / CS;         // slot tiles per wave
     constexpr int PLS = PK ? 1 : PL;     // staged (and multiplied) planes
     constexpr int PA = MT / 2;           // packed: full tiles per plane
@@ -750,13 +750,15 @@ void k_gemm32(GemmP p) {
         // lane l holds slot 32m + l % 32 and rows 8q + 4(l/32) + 0..3 of its
         // 32-row group: a slot's rows sit in lanes l and l ^ 32
         static_assert(!SPLIT, "the lm_head statistics need whole k sums");
-        constexpr int MTO = PK ? PA + 1 : MT;
-        constexpr int NSLOT = MTO * 32;
-        static_assert(NW * NSLOT * (int)sizeof(VStat) <= (int)sizeof(xs), "statistics staging exceeds LDS");
+        // (column split: the NW / CS row units each stage every slot once)
+        constexpr int MTO = PK ? PA + 1 : MTW;
+        constexpr int NSLOT = (PK ? PA + 1 : MT) * 32;
+        constexpr int NU = NW / CS;  // row units per workgroup
+        static_assert(NU * NSLOT * (int)sizeof(VStat) <= (int)sizeof(xs), "statistics staging exceeds LDS");
         VStat* stg = reinterpret_cast<VStat*>(xs);
 #pragma unroll
         for (int m = 0; m < MTO; ++m) {
-            const int t = m * 32 + lc;
+            const int t = (m0 + m) * 32 + lc;
             VStat st = vstat_empty();
             if (has_unit && t < p.T && !(PK && m == PA && lc >= 16)) {
                 const float sc = rsl[t];
@@ -779,10 +781,10 @@ void k_gemm32(GemmP p) {
                 st = lane_stat(z, row, p.dnext[t], p.zd + t);
             }
             st = vstat_merge(st, vstat_shfl_xor(st, 32));
-            if (lh == 0) stg[wv * NSLOT + m * 32 + lc] = st;
+            if (lh == 0) stg[(wv / CS) * NSLOT + t] = st;
         }
         __syncthreads();
-        lmstat_merge_waves<NTH, NW, NSLOT>(p, stg, wgi);
+        lmstat_merge_waves<NTH, NU, NSLOT>(p, stg, wgi);
         return;
     }
     if constexpr (SPLIT) {
@@ -979,7 +981,7 @@ constexpr int kT32 = 97;  // first slot count served by the 32x32 form
 
 static int cu_count();
 
-static GemmShape shape_for(int T, int vcols, bool raw, int K, bool lmstat) {
+static GemmShape shape_for(int T, int vcols, bool raw, int K) {
     const bool wide = vcols % 256 == 0;
     // packed planes (2a + 1 tiles for 32a < T <= 32a + 16): split-K
     // partial GEMMs at 65..80 slots (QKV / O / down at T = 80: 29.5 / 23.7
@@ -1019,7 +1021,7 @@ static GemmShape shape_for(int T, int vcols, bool raw, int K, bool lmstat) {
         // chunks: every B fragment feeds two MFMAs.  Same-box timing of the
         // 32B shapes at T = 229 in isolation: gate/up 263 vs 293 us, QKV 57
         // vs 59, O 52 vs 56, down 121 vs 137 us against 32-row units
-        if (vcols % 64 == 0 && !lmstat) return GemmShape{32, 8, 2, 64, 8, 1, 0, 0, 2};
+        if (vcols % 64 == 0) return GemmShape{32, 8, 2, 64, 8, 1, 0, 0, 2};
         return w8 ? GemmShape{32, 8, 1, 32, 8, 1, 0} : GemmShape{32, 8, 1, 64, 4, 1, 0};
     }
     if (mt <= 10) return {32, 10, 1, 32, 4, 1, 0};
@@ -1047,9 +1049,7 @@ static GemmFn pick_epi(int epi) {
         switch (epi) {
             case EPI_RESID: return k_gemm32<MT, NS, KC, EPI_RESID, false, NW, 2, PD, PK, CS>;
             case EPI_SWIGLU: return k_gemm32<MT, NS, KC, EPI_SWIGLU, false, NW, 2, PD, PK, CS>;
-            case EPI_LMSTAT:
-                if constexpr (CS == 1) return k_gemm32<MT, NS, KC, EPI_LMSTAT, false, NW, 2, PD, PK, CS>;
-                else return nullptr;
+            case EPI_LMSTAT: return k_gemm32<MT, NS, KC, EPI_LMSTAT, false, NW, 2, PD, PK, CS>;
             default: return k_gemm32<MT, NS, KC, EPI_STORE, false, NW, 2, PD, PK, CS>;
         }
     }
@@ -1169,7 +1169,7 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
         return 1;
     }
     const int vcols = g.epi == EPI_SWIGLU ? 2 * g.N : g.N;
-    const GemmShape sh = shape_for(g.T, vcols, g.raw != 0, g.K, g.epi == EPI_LMSTAT);
+    const GemmShape sh = shape_for(g.T, vcols, g.raw != 0, g.K);
     const int unit_rows = sh.F * sh.NSUB;  // weight rows of one row unit
     GemmP p;
     p.X = (const bf16_t*)g.X;
