@@ -342,19 +342,31 @@ void build_stage(sd_ctx* c, Slot& s, int mode, bool with_items, int* n_items, in
     const int hkv = c->D.hkv;
     const int cap = std::max(c->attn_cap, s.B * hkv);
     long total = 0;
-    int max_ctx = 1;
-    for (int b = 0; b < s.B; ++b) {
-        const int ctx = c->users[s.users[b]].prefix + s.L[b] + 1;
-        total += ctx;
-        max_ctx = std::max(max_ctx, ctx);
-    }
+    for (int b = 0; b < s.B; ++b) total += c->users[s.users[b]].prefix + s.L[b] + 1;
+    // A token costs its share of the KV stream plus the products of the wave
+    // with the most 16-row query tiles (the four waves take tiles w, w+4,
+    // ...): a user whose (l+1)*G rows need two tiles per wave costs about
+    // 1.3x per token (measured: the products add ~6 us to the ~14 us KV
+    // stream of a one-tile layer at 80 slots), so its chunks are shortened
+    // in proportion and the items end together.
+    const int G = c->D.G();
+    auto weight = [&](int b) {  // cost per token in tenths
+        const int tiles = ceil_div((s.L[b] + 1) * G, 16);
+        return 10 + 3 * (ceil_div(tiles, 4) - 1);
+    };
+    auto user_chunk = [&](int b, int ch) {  // chunk length of user b for base length ch
+        return std::max(32, (int)((long)ch * 10 / weight(b)) & ~31);
+    };
     auto n_items_for = [&](int ch) {
         long n = 0;
-        for (int b = 0; b < s.B; ++b) n += ceil_div(c->users[s.users[b]].prefix + s.L[b] + 1, ch);
+        for (int b = 0; b < s.B; ++b)
+            n += ceil_div(c->users[s.users[b]].prefix + s.L[b] + 1, user_chunk(b, ch));
         return n * hkv;
     };
+    // (ends: once every user's chunk holds its whole context there are
+    // B * hkv <= cap items)
     int chunk = (int)std::max<long>(32, ((total * hkv + cap - 1) / cap + 31) & ~31L);
-    while (chunk < max_ctx && n_items_for(chunk) > cap) chunk += 32;
+    while (n_items_for(chunk) > cap) chunk += 32;
     for (int b = 0; b < s.B; ++b) {
         const User& u = c->users[s.users[b]];
         user[b] = s.users[b];
@@ -372,8 +384,10 @@ void build_stage(sd_ctx* c, Slot& s, int mode, bool with_items, int* n_items, in
         maxL = std::max(maxL, s.L[b]);
         if (with_items) {
             const int ctx = u.prefix + s.L[b] + 1;
-            // equal chunks for this user: as many as `chunk` needs, evened out
-            const int cb = (ceil_div(ctx, ceil_div(ctx, chunk)) + 31) & ~31;
+            // equal chunks for this user: as many as its chunk length needs,
+            // evened out
+            const int ub = user_chunk(b, chunk);
+            const int cb = (ceil_div(ctx, ceil_div(ctx, ub)) + 31) & ~31;
             const int nch = ceil_div(ctx, cb);
             for (int g = 0; g < hkv; ++g)
                 for (int ch = 0; ch < nch; ++ch) {
