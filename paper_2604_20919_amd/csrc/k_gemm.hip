@@ -73,7 +73,29 @@ struct GemmP {
     VStat* lstat;
     float* zd;
     const int32_t* dnext;
+    // stream-K (unsplit column-split GEMMs that leave CUs idle): the tiles x
+    // kchunks (row tile, chunk) pairs are dealt out in tile-major order as
+    // sk_nwg contiguous ranges of equal length, one per workgroup; a piece
+    // that does not end its tile leaves its sums in partial slot (tile,
+    // piece) of `part` and counts itself in sk_cnt[tile]; the tile's last
+    // piece waits for that count, adds the earlier pieces in order and runs
+    // the epilogue (sk_nwg = 0: off)
+    int sk_nwg, sk_maxp;
+    int* sk_cnt;
+    int32_t* flags;  // device error bits (bit 2: a stream-K wait gave up)
 };
+
+// stream-K: first pair of workgroup w's range, and the workgroup whose range
+// holds pair i
+__host__ __device__ __forceinline__ int sk_begin(int w, int total, int nwg) {
+    return (int)((long long)w * total / nwg);
+}
+__host__ __device__ __forceinline__ int sk_owner(int i, int total, int nwg) {
+    return (int)(((long long)(i + 1) * nwg - 1) / total);
+}
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+// polls of a stream-K wait before it gives up (a fraction of a second)
+constexpr int kSkSpinMax = 1 << 18;
 
 // lm_head epilogue, the part common to both MFMA forms: the per-wave
 // statistics of every slot (staged in LDS as [wave][slot]) are merged over
@@ -482,12 +504,15 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 // fragment read from LDS then feeds two MFMAs instead of one: four SIMDs
 // issuing 32-cycle MFMAs ask for 64 bytes per clock of LDS reads instead
 // of 128, at the same accumulator count per wave.
-template <int MT, int NS, int KC, int EPI, bool SPLIT, int NW, int PL, int PD, bool PK = false, int CS = 1>
+// SKF: stream-K (unsplit column-split GEMMs, see GemmP).
+template <int MT, int NS, int KC, int EPI, bool SPLIT, int NW, int PL, int PD, bool PK = false, int CS = 1,
+          bool SKF = false>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW > 8 ? NW / 4 : 1, NW > 8 ? NW / 4 : 2)))
 void k_gemm32(GemmP p) {
     static_assert(!PK || (PL == 2 && MT % 2 == 1), "packed planes: two planes, 2a + 1 tiles");
     static_assert(MT % CS == 0 && NW % CS == 0 && (CS == 1 || !PK),
                   "column split: whole tiles per wave, no packed planes");
+    static_assert(!SKF || (CS > 1 && !SPLIT && EPI == EPI_SWIGLU), "stream-K: the unsplit SwiGLU product");
     constexpr int MTW = MT / CS;         // slot tiles per wave
     constexpr int PLS = PK ? 1 : PL;     // staged (and multiplied) planes
     constexpr int PA = MT / 2;           // packed: full tiles per plane
@@ -511,10 +536,29 @@ void k_gemm32(GemmP p) {
     __shared__ __attribute__((aligned(16))) bf16_t xs[XS_ELEMS];
     __shared__ float rsl[SPLIT ? 1 : MT * ROWS_PER_TILE];  // per-slot RMSNorm factor
 
-    const int split = SPLIT ? blockIdx.x % p.S : 0;
-    const int wgi = SPLIT ? blockIdx.x / p.S : blockIdx.x;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int lc = lane & 31, lh = lane >> 5;
+    // Stream-K: the workgroup's range of (row tile, chunk) pairs is shorter
+    // than a tile, so it is one piece of a tile or two: the head of the last
+    // tile and the tail of the first, taken in that order (k increasing, so
+    // all workgroups walk the activation chunks nearly together and share
+    // them in L2).  Otherwise one piece: the whole k range of a split.
+    int sk_np = 1, sk_t[2] = {0, 0}, sk_b[2] = {0, 0}, sk_e[2] = {0, 0};
+    if constexpr (SKF) {
+        const int total = p.tiles * p.kchunks;
+        const int wb = sk_begin(blockIdx.x, total, p.sk_nwg), we = sk_begin(blockIdx.x + 1, total, p.sk_nwg);
+        const int t0 = wb / p.kchunks, t1 = (we - 1) / p.kchunks;
+        if (t0 == t1) {
+            sk_t[0] = t0; sk_b[0] = wb - t0 * p.kchunks; sk_e[0] = we - t0 * p.kchunks;
+        } else {
+            sk_np = 2;
+            sk_t[0] = t1; sk_b[0] = 0; sk_e[0] = we - t1 * p.kchunks;
+            sk_t[1] = t0; sk_b[1] = wb - t0 * p.kchunks; sk_e[1] = p.kchunks;
+        }
+    }
+    for (int piece = 0; piece < sk_np; ++piece) {
+    const int split = SPLIT ? blockIdx.x % p.S : 0;
+    const int wgi = SKF ? (piece == 0 ? sk_t[0] : sk_t[1]) : (SPLIT ? blockIdx.x / p.S : blockIdx.x);
 
     // Buffer resources: one uniform resource per operand, fixed 32-bit
     // per-lane offsets, uniform chunk offsets.  Out-of-range reads return 0
@@ -550,8 +594,8 @@ void k_gemm32(GemmP p) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[s][m][e] = 0.f;
 
-    const int c_begin = split * p.kchunks / p.S;
-    const int c_end = (split + 1) * p.kchunks / p.S;
+    const int c_begin = SKF ? (piece == 0 ? sk_b[0] : sk_b[1]) : split * p.kchunks / p.S;
+    const int c_end = SKF ? (piece == 0 ? sk_e[0] : sk_e[1]) : (split + 1) * p.kchunks / p.S;
 
     // Register-ring pipeline with prefetch distance PD chunks: while chunk c
     // is multiplied (X from LDS buffer c&1, W from ring set c % NB), X and W
@@ -729,6 +773,57 @@ void k_gemm32(GemmP p) {
     }
     }
 
+    int sk_ord = 0;  // earlier pieces of this tile to add (the tile's last piece)
+    if constexpr (SKF) {
+        // Partial sums travel through memory at system scope (written
+        // through, read past the caches), ordered by the count: stores, wait
+        // for them, barrier, then the count; the reader polls the count
+        // before it loads.  Slot layout: element j of thread i at j * NTH + i
+        // (16-byte pieces, coalesced).
+        constexpr int PER4 = NS * MTW * 4;  // 16-byte accumulator pieces per thread
+        const int total = p.tiles * p.kchunks;
+        const int ord = (int)blockIdx.x - sk_owner(wgi * p.kchunks, total, p.sk_nwg);
+        auto slot_rsrc = [&](int o) {
+            return __builtin_amdgcn_make_buffer_rsrc(
+                (void*)(p.part + ((size_t)wgi * p.sk_maxp + o) * (size_t)(NTH * PER4 * 4)), (short)0,
+                NTH * PER4 * 16, 0x00020000);
+        };
+        if (c_end < p.kchunks) {
+            const __amdgpu_buffer_rsrc_t r = slot_rsrc(ord);
+#pragma unroll
+            for (int s = 0; s < NS; ++s)
+#pragma unroll
+                for (int m = 0; m < MTW; ++m)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int j = (s * MTW + m) * 4 + q;
+                        const f32x4 v = f32x4{acc[s][m][4 * q], acc[s][m][4 * q + 1], acc[s][m][4 * q + 2],
+                                              acc[s][m][4 * q + 3]};
+                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r,
+                                                               (j * NTH + (int)threadIdx.x) * 16, 0, 17);
+                    }
+            wait_vm<0>();
+            __syncthreads();
+            if (threadIdx.x == 0)
+                __hip_atomic_fetch_add(p.sk_cnt + wgi, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+            continue;
+        }
+        if (ord > 0) {
+            if (threadIdx.x == 0) {
+                int spins = 0;
+                while (__hip_atomic_load(p.sk_cnt + wgi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) < ord) {
+                    if (++spins > kSkSpinMax) {
+                        atomicOr(p.flags, 4);
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(2);
+                }
+                __hip_atomic_store(p.sk_cnt + wgi, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+            }
+            __syncthreads();
+            sk_ord = ord;  // added tile by tile in the epilogue (fewer live registers)
+        }
+    }
     // Accumulator layout: lane l holds slot t = 32*m + l % 32 and, in
     // registers 4q..4q+3, weight rows 8q + 4*(l/32) + 0..3 of its group.
     // Packed planes: slot t's sums are those of tile m and tile m + a + 1
@@ -823,6 +918,29 @@ void k_gemm32(GemmP p) {
     }
 #pragma unroll
     for (int m = 0; m < (PK ? PA + 1 : MTW); ++m) {
+        if constexpr (SKF) {
+            // the earlier pieces' sums of this slot tile, in piece order
+            for (int o = 0; o < sk_ord; ++o) {
+                const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+                    (void*)(p.part + ((size_t)wgi * p.sk_maxp + o) * (size_t)(NTH * NS * MTW * 16)), (short)0,
+                    NTH * NS * MTW * 64, 0x00020000);
+                u32x4 v[NS][4];
+#pragma unroll
+                for (int s = 0; s < NS; ++s)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        v[s][q] = __builtin_amdgcn_raw_buffer_load_b128(
+                            r, (((s * MTW + m) * 4 + q) * NTH + (int)threadIdx.x) * 16, 0, 17);
+#pragma unroll
+                for (int s = 0; s < NS; ++s)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const f32x4 f = __builtin_bit_cast(f32x4, v[s][q]);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) acc[s][m][4 * q + e] += f[e];
+                    }
+            }
+        }
         const int t = (m0 + m) * 32 + lc;
         if (!has_unit || t >= p.T || (PK && m == PA && lc >= 16)) continue;
         const float sc = rsl[t];
@@ -846,6 +964,7 @@ void k_gemm32(GemmP p) {
                                     sc);
             }
         }
+    }
     }
 }
 
@@ -1035,7 +1154,7 @@ typedef void (*ReduceFn)(GemmP);
 // Activations always come as two planes (hi, lo); split-K kernels write raw
 // partial planes and the epilogue runs in the reducer.
 template <int F, int MT, int NW, int KC, int PD, bool SPLIT, bool PK = false, int CS = 1, int NS = 1>
-static GemmFn pick_epi(int epi) {
+static GemmFn pick_epi(int epi, bool skf = false) {
     if constexpr (F == 16) {
         if (SPLIT) return k_gemm16<MT, 2, KC, EPI_STORE, true, NW, 2, PD>;
         switch (epi) {
@@ -1045,6 +1164,8 @@ static GemmFn pick_epi(int epi) {
             default: return k_gemm16<MT, 2, KC, EPI_STORE, false, NW, 2, PD>;
         }
     } else {
+        if constexpr (CS > 1 && !SPLIT)
+            if (skf) return epi == EPI_SWIGLU ? k_gemm32<MT, NS, KC, EPI_SWIGLU, false, NW, 2, PD, PK, CS, true> : nullptr;
         if (SPLIT) return k_gemm32<MT, NS, KC, EPI_STORE, true, NW, 2, PD, PK, CS>;
         switch (epi) {
             case EPI_RESID: return k_gemm32<MT, NS, KC, EPI_RESID, false, NW, 2, PD, PK, CS>;
@@ -1078,14 +1199,14 @@ static GemmFn pick_nw(const GemmShape& sh, int epi) {
 }
 
 template <bool SPLIT>
-static GemmFn pick(const GemmShape& sh, int epi) {
+static GemmFn pick(const GemmShape& sh, int epi, bool skf = false) {
     if (sh.PK) {
         if (sh.MT == 5) return SPLIT ? pick_epi<32, 5, 8, 64, 2, true, true>(epi) : nullptr;
         if (sh.MT == 7) return pick_epi<32, 7, 8, 64, 1, SPLIT, true>(epi);
         return nullptr;
     }
     if (sh.F == 32 && sh.MT == 8) {
-        if (sh.CS == 2) return pick_epi<32, 8, 8, 64, 1, SPLIT, false, 2, 2>(epi);
+        if (sh.CS == 2) return pick_epi<32, 8, 8, 64, 1, SPLIT, false, 2, 2>(epi, skf);
         return sh.NW == 8 ? pick_epi<32, 8, 8, 32, 1, SPLIT>(epi) : pick_epi<32, 8, 4, 64, 1, SPLIT>(epi);
     }
     if (sh.F == 32 && sh.MT == 10) return pick_epi<32, 10, 4, 32, 1, SPLIT>(epi);
@@ -1144,8 +1265,11 @@ size_t gemm_partial_floats(const Dims& D, int Tmax) {
     if (!D.bf16) return (size_t)Tmax * (size_t)std::max(D.nqkv(), D.d);
     // the split count is bounded by the CU count over the tile count, so
     // S * vcols <= ~2 * (CUs * NT) for every call; reserve generously
+    // (three planes' worth also holds the stream-K partial slots of the
+    // gate/up product at 225-256 slots: 200 tiles x 2 x 65536 floats on the
+    // Qwen3-32B shape)
     const size_t widest = (size_t)std::max(std::max(D.nqkv(), D.d), 2 * D.F);
-    return (size_t)Tmax * std::max<size_t>(widest * 2, (size_t)65536);
+    return (size_t)Tmax * std::max<size_t>(widest * 3, (size_t)65536);
 }
 
 
@@ -1204,6 +1328,27 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
     p.zd = g.zd;
     p.dnext = g.dnext;
     if (g.groups_out) *g.groups_out = p.tiles;
+    // Stream-K for an unsplit column-split SwiGLU product that leaves CUs
+    // idle (gate/up at 225-256 slots: 200 row tiles of 256 rows on 256 CUs)
+    p.sk_nwg = 0;
+    p.sk_maxp = 0;
+    p.sk_cnt = g.sk_cnt;
+    p.flags = g.flags;
+    if (!g.raw && g.epi == EPI_SWIGLU && sh.CS > 1 && S == 1 && g.sk_cnt && g.flags &&
+        p.tiles < cu_count() && p.tiles <= kSkCounters) {
+        const int total = p.tiles * p.kchunks, nwg = std::min(cu_count(), total);
+        int maxp = 0;  // most pieces of a tile before its last
+        for (int t = 0; t < p.tiles; ++t)
+            maxp = std::max(maxp, sk_owner(t * p.kchunks + p.kchunks - 1, total, nwg) -
+                                      sk_owner(t * p.kchunks, total, nwg));
+        const size_t slot_floats = (size_t)64 * sh.NW * sh.NSUB * (sh.MT / sh.CS) * 16;
+        if (maxp >= 1 && (size_t)p.tiles * maxp * slot_floats <= sb.gpart_floats) {
+            p.sk_nwg = nwg;
+            p.sk_maxp = maxp;
+            hipLaunchKernelGGL(pick<false>(sh, g.epi, true), dim3(nwg), dim3(64 * sh.NW), 0, s, p);
+            return 1;
+        }
+    }
     if (g.raw) {
         // S partial planes [S][T][N] for a fused consumer to reduce
         hipLaunchKernelGGL(pick<true>(sh, EPI_STORE), dim3(p.tiles * S), dim3(64 * sh.NW), 0, s, p);

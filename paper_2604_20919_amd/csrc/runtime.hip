@@ -39,7 +39,7 @@ struct Layout {
         st_ioff, st_flags, st_prow, st_bytes;
     // slot buffers (byte offsets within the slot)
     size_t stage, tok, cs, x, ssq, h, ffn, qbuf, attn, apart, aml, gpart, logits, sstat, spart,
-        spartB, lstat, zd, dnext, result, slot_bytes;
+        spartB, lstat, zd, dnext, skcnt, result, slot_bytes;
     size_t gpart_floats;
     int nsq;
     // global region after the slots
@@ -154,6 +154,7 @@ Layout plan(const sd_config& c) {
     L.lstat = take(D.bf16 ? (size_t)lm_stat_groups_max(D.V) * L.Tmax * 4 * 4 : 16);
     L.zd = take((size_t)L.Tmax * 4);
     L.dnext = take((size_t)L.Tmax * 4);
+    L.skcnt = take((size_t)kSkCounters * 4);
     L.result = take((size_t)(2 * L.Bmax + 4) * 4);
     L.slot_bytes = s;
     L.total = align_up(L.slot_bytes * (size_t)c.max_pending);
@@ -512,6 +513,8 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
             gu.epi = EPI_SWIGLU;
             gu.out = sb.ffn;
             gu.ldo = D.F;
+            gu.sk_cnt = sb.skcnt;
+            gu.flags = bv.flags;
             launch_gemm(D, gu, sb, st);
         }
         {
@@ -716,6 +719,7 @@ sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_poo
         b.lstat = (float*)(s.base + L.lstat);
         b.zd = (float*)(s.base + L.zd);
         b.dnext = (int32_t*)(s.base + L.dnext);
+        b.skcnt = (int*)(s.base + L.skcnt);
         b.result = (int32_t*)(s.base + L.result);
         b.bmax = L.Bmax;
     }
@@ -726,6 +730,9 @@ sd_status sd_verify_init(const sd_config* cfg, const sd_weights* w, void* kv_poo
         const Dims& D = c->D;
         const size_t kv_bytes = (size_t)D.L * cfg->n_pages * 2 * D.hkv * kPageTokens * D.hd * c->kv.esize;
         ok &= hipMemset(kv_pool, 0, kv_bytes) == hipSuccess;
+        // the stream-K piece counters start at zero (each launch leaves them so)
+        for (int i = 0; ok && i < cfg->max_pending; ++i)
+            ok &= hipMemset(c->slots[i].bufs.skcnt, 0, (size_t)kSkCounters * 4) == hipSuccess;
     }
     if (ok && c->D.bf16) {
         // repack the projection matrices and the lm_head into fragment order

@@ -106,6 +106,7 @@ struct SlotBufs {
     float* lstat;
     float* zd;        // [Tmax]
     int32_t* dnext;   // [Tmax]
+    int* skcnt;       // [kSkCounters] stream-K piece counters, zero between launches
     int32_t* result;  // [2*Bmax + 4]: n_acc, token, flags
     int bmax;
 };
@@ -143,7 +144,12 @@ struct GemmCall {
     float* zd;
     const int32_t* dnext;
     int* groups_out;
+    // stream-K of the gate/up product (see k_gemm.hip): per-tile piece
+    // counters (kSkCounters, zero between launches) and the device error bits
+    int* sk_cnt;
+    int32_t* flags;
 };
+constexpr int kSkCounters = 4096;
 // Upper bound of the statistic groups of an lm_head of V rows (workgroups
 // of at least 128 rows, one more for rounding)
 inline int lm_stat_groups_max(int V) { return (V + 127) / 128 + 1; }
