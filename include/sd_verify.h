@@ -42,7 +42,8 @@ enum {
     SD_ENOMEM = -2,   /* KV page pool exhausted or workspace too small */
     SD_EHIP = -3,     /* a HIP runtime call failed */
     SD_ESTATE = -4,   /* call out of order (batch pending / not pending) */
-    SD_EDEVICE = -5,  /* the GPU found bad input data (token id out of range) */
+    SD_EDEVICE = -5,  /* the GPU found bad input data (token id out of range), or a
+                         bounded wait of one workgroup for another gave up */
     SD_ENOTIMPL = -6, /* configuration not supported by this build */
     SD_ENODEV = -7,   /* no usable gfx950 device */
     SD_ELIMIT = -8    /* input beyond the fixed limits of sd_sample_logits_noalloc */
@@ -332,7 +333,10 @@ sd_status sd_draft_batch(sd_ctx* ctx, int32_t batch, int32_t n_users, const int3
  *               := out_token, pages trimmed to the new length; 0 = leave the
  *               user state unchanged (repeatable measurements)
  * Entries of users outside the batch are not touched.  Returns SD_EDEVICE,
- * without committing, if the GPU saw a token id >= vocab.
+ * without committing, if the GPU saw a token id >= vocab, or if a workgroup
+ * of the split gate/up product stopped waiting for the partial sums of
+ * another (a bounded wait, well under a second); the results are
+ * then not written.
  */
 sd_status sd_accept(sd_ctx* ctx, int32_t batch, int32_t* n_accepted, int32_t* out_token,
                     int32_t commit);
@@ -351,6 +355,16 @@ sd_status sd_sample_logits(sd_ctx* ctx, int32_t batch, int32_t n_users, const in
  * `stream`.  SD_ESTATE if the batch is not pending or its pass stored no
  * logits (sd_config.logits_out). */
 sd_status sd_debug_logits(sd_ctx* ctx, int32_t batch, float* dst, sd_stream stream);
+
+/* Diagnostic: bound of the waits in the split gate/up product of passes
+ * enqueued after this call.  When the product is split over more
+ * workgroups than its row tiles, the workgroup that finishes a tile polls a
+ * counter until every earlier workgroup of the tile has left its partial
+ * sums; after max_polls polls it gives up, and sd_accept of that batch
+ * returns SD_EDEVICE.  max_polls = 0 gives up at once (to test that error
+ * path); a negative value restores the default (2^18 polls).  Passes whose
+ * product takes no split are not affected. */
+sd_status sd_debug_wait_limit(sd_ctx* ctx, int32_t max_polls);
 
 /*
  * For callers that cannot allocate device memory -- code under HIP graph

@@ -80,7 +80,8 @@ struct GemmP {
     // piece) of `part` and counts itself in sk_cnt[tile]; the tile's last
     // piece waits for that count, adds the earlier pieces in order and runs
     // the epilogue (sk_nwg = 0: off)
-    int sk_nwg, sk_maxp;
+    // the piece waits for at most sk_polls polls of the count
+    int sk_nwg, sk_maxp, sk_polls;
     int* sk_cnt;
     int32_t* flags;  // device error bits (bit 2: a stream-K wait gave up)
 };
@@ -94,8 +95,6 @@ __host__ __device__ __forceinline__ int sk_owner(int i, int total, int nwg) {
     return (int)(((long long)(i + 1) * nwg - 1) / total);
 }
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-// polls of a stream-K wait before it gives up (a fraction of a second)
-constexpr int kSkSpinMax = 1 << 18;
 
 // lm_head epilogue, the part common to both MFMA forms: the per-wave
 // statistics of every slot (staged in LDS as [wave][slot]) are merged over
@@ -810,15 +809,19 @@ void k_gemm32(GemmP p) {
         }
         if (ord > 0) {
             if (threadIdx.x == 0) {
-                int spins = 0;
-                while (__hip_atomic_load(p.sk_cnt + wgi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) < ord) {
-                    if (++spins > kSkSpinMax) {
+                for (int polls = 0;; ++polls) {
+                    if (polls >= p.sk_polls) {
                         atomicOr(p.flags, 4);
                         break;
                     }
+                    if (__hip_atomic_load(p.sk_cnt + wgi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) >= ord)
+                        break;
                     __builtin_amdgcn_s_sleep(2);
                 }
-                __hip_atomic_store(p.sk_cnt + wgi, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+                // back to zero once every earlier piece has counted, also
+                // after a wait that gave up (the stream runs the next launch
+                // only when all of this one's workgroups have ended)
+                __hip_atomic_fetch_sub(p.sk_cnt + wgi, ord, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
             }
             __syncthreads();
             sk_ord = ord;  // added tile by tile in the epilogue (fewer live registers)
@@ -1332,6 +1335,7 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
     // idle (gate/up at 225-256 slots: 200 row tiles of 256 rows on 256 CUs)
     p.sk_nwg = 0;
     p.sk_maxp = 0;
+    p.sk_polls = g.sk_polls;
     p.sk_cnt = g.sk_cnt;
     p.flags = g.flags;
     if (!g.raw && g.epi == EPI_SWIGLU && sh.CS > 1 && S == 1 && g.sk_cnt && g.flags &&

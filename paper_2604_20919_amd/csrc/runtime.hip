@@ -224,6 +224,7 @@ struct sd_ctx {
     Slot slots[kMaxPending];
     int device = 0;
     int attn_cap = 512;  // attention work items that run in one wave of workgroups
+    int sk_polls = kSkPollsDefault;  // bound of the stream-K waits
     // diagnostic timing of one kernel class
     int prof_class = 0;
     int prof_used = 0;
@@ -515,6 +516,7 @@ sd_status enqueue_forward(sd_ctx* c, Slot& s, const BatchView& bv, hipStream_t s
             gu.ldo = D.F;
             gu.sk_cnt = sb.skcnt;
             gu.flags = bv.flags;
+            gu.sk_polls = c->sk_polls;
             launch_gemm(D, gu, sb, st);
         }
         {
@@ -904,7 +906,7 @@ static std::vector<int64_t> launch_key(sd_ctx* c, const Slot& s, const BatchView
     std::vector<int64_t> k = {bv.B, bv.T, bv.nd, bv.mode, (int64_t)bv.seed, (int64_t)bv.round,
                               bv.n_items, bv.rows_max, (int64_t)(intptr_t)bv.drafts,
                               (int64_t)(intptr_t)bv.q, (int64_t)(intptr_t)bv.accept_u,
-                              (int64_t)(intptr_t)st};
+                              (int64_t)(intptr_t)st, c->sk_polls};
     for (int b = 0; b < s.B; ++b) {
         k.push_back(s.users[b]);
         k.push_back(s.L[b]);
@@ -1130,6 +1132,12 @@ sd_status sd_debug_logits(sd_ctx* c, int32_t batch, float* dst, sd_stream stream
     hipStream_t st = (hipStream_t)stream;
     SD_HIP(hipStreamWaitEvent(st, s.done, 0));
     SD_HIP(hipMemcpyAsync(dst, s.bufs.logits, (size_t)s.T * c->D.V * 4, hipMemcpyDeviceToDevice, st));
+    return SD_OK;
+}
+
+sd_status sd_debug_wait_limit(sd_ctx* c, int32_t max_polls) {
+    if (!c) return SD_EINVAL;
+    c->sk_polls = max_polls < 0 ? kSkPollsDefault : max_polls;
     return SD_OK;
 }
 

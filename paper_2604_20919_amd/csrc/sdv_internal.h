@@ -145,11 +145,15 @@ struct GemmCall {
     const int32_t* dnext;
     int* groups_out;
     // stream-K of the gate/up product (see k_gemm.hip): per-tile piece
-    // counters (kSkCounters, zero between launches) and the device error bits
+    // counters (kSkCounters, zero between launches), the device error bits
+    // and the polls of a wait before it gives up
     int* sk_cnt;
     int32_t* flags;
+    int sk_polls;
 };
 constexpr int kSkCounters = 4096;
+// polls of a stream-K wait before it gives up (a fraction of a second)
+constexpr int kSkPollsDefault = 1 << 18;
 // Upper bound of the statistic groups of an lm_head of V rows (workgroups
 // of at least 128 rows, one more for rounding)
 inline int lm_stat_groups_max(int V) { return (V + 127) / 128 + 1; }

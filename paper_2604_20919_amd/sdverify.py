@@ -27,7 +27,7 @@ MODES = {"greedy": SD_GREEDY, "stochastic": SD_STOCHASTIC, "force": SD_FORCE}
 EXPORTS = ("sd_verify_query_sizes", "sd_verify_init", "sd_verify_destroy", "sd_user_reset",
            "sd_user_release", "sd_user_state", "sd_kv_write", "sd_kv_read", "sd_verify_batch",
            "sd_verify_batch_graph", "sd_verify_batch_sparse", "sd_draft_batch", "sd_accept", "sd_sample_logits",
-           "sd_sample_logits_noalloc", "sd_debug_logits", "sd_profile_begin", "sd_profile_end",
+           "sd_sample_logits_noalloc", "sd_debug_logits", "sd_debug_wait_limit", "sd_profile_begin", "sd_profile_end",
            "sd_calib_hbm", "sd_calib_mfma", "sd_status_str")
 SD_K_QKV, SD_K_ATTN, SD_K_O, SD_K_GATEUP, SD_K_DOWN, SD_K_LMHEAD, SD_K_SAMPLER, SD_K_SMALL = range(1, 9)
 
@@ -87,6 +87,7 @@ def lib() -> ctypes.CDLL:
         L.sd_sample_logits.argtypes = [vp, i32, i32, vp, vp, vp, vp, vp, i32, u64, u64, vp, vp]
         L.sd_sample_logits_noalloc.argtypes = [i32, vp, vp, i32, vp, vp, vp, i32, u64, u64, vp, vp, vp]
         L.sd_debug_logits.argtypes = [vp, i32, vp, vp]
+        L.sd_debug_wait_limit.argtypes = [vp, i32]
         L.sd_profile_begin.argtypes = [vp, i32, i32]
         L.sd_profile_end.argtypes = [vp, P(ctypes.c_double), P(i32)]
         L.sd_calib_hbm.argtypes = [vp, ctypes.c_size_t, i32, i32, P(ctypes.c_double), vp]
@@ -252,6 +253,10 @@ def sd_accept(ctx: int, batch: int, n_users: int, commit: bool = False):
 
 def sd_debug_logits(ctx: int, batch: int, dst, stream=None) -> None:
     _check("sd_debug_logits", lib().sd_debug_logits(ctx, batch, _dev(dst), _stream(stream)))
+
+
+def sd_debug_wait_limit(ctx: int, max_polls: int) -> None:
+    _check("sd_debug_wait_limit", lib().sd_debug_wait_limit(ctx, max_polls))
 
 
 def sd_profile_begin(ctx: int, kclass: int, max_launches: int = 4096) -> None:

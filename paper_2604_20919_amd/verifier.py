@@ -100,6 +100,10 @@ class Verifier:
     def accept(self, batch: int, n_users: int, commit: bool = False):
         return sv.sd_accept(self.ctx, batch, n_users, commit)
 
+    def wait_limit(self, max_polls: int) -> None:
+        """Bound of the split gate/up product's waits (negative: default)."""
+        sv.sd_debug_wait_limit(self.ctx, max_polls)
+
     def logits(self, batch: int, T: int, stream=None) -> torch.Tensor:
         out = torch.empty((T, self.vocab), dtype=torch.float32, device="cuda")
         sv.sd_debug_logits(self.ctx, batch, out, stream)

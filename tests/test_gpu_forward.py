@@ -7,6 +7,7 @@ import torch
 
 import oracle
 import workload as wl
+from paper_2604_20919_amd import sdverify as sdv
 from gpu_harness import (assert_decisions, compare_decisions, gpu_prefill, load_synthetic_kv,
                          logit_rel_err, make_verifier, run_gpu, run_oracle)
 from workload.device import DeviceWeights, batch_to_device
@@ -203,17 +204,8 @@ def test_determinism_two_runs_bit_identical():
     v.close()
 
 
-@pytest.mark.parametrize("T_target", [17, 64, 65, 70, 75, 80, 96, 97, 105, 112, 113, 150, 224, 225, 250,
-                                      256, 257, 300, 320, 321, 416])
-def test_bf16_every_gemm_tile_class(T_target):
-    """Query-slot totals that select each GEMM tile class, and both sides of
-    every boundary between them: the 16x16 form up to 96 slots, the 32x32
-    form above (eight-wave tiles up to 256 slots, four-wave tiles above;
-    32-k chunks at 225..320 slots, 16-k chunks above 320), the
-    packed-plane 32x32 tiles (split-K partials at 65..80 slots, every GEMM
-    at 97..112, with and without padding in the mixed tile), split-K and
-    unsplit paths, up to the 416-slot maximum."""
-    rng = np.random.default_rng(T_target)
+def _ragged_draft_lengths(T_target, rng):
+    """Draft lengths 1..12 whose slot total (l + 1 per user) is T_target."""
     L, T = [], 0
     while T < T_target:
         rem = T_target - T
@@ -227,6 +219,21 @@ def test_bf16_every_gemm_tile_class(T_target):
         L.append(l)
         T += l + 1
     assert T == T_target
+    return L
+
+
+@pytest.mark.parametrize("T_target", [17, 64, 65, 70, 75, 80, 96, 97, 105, 112, 113, 150, 224, 225, 250,
+                                      256, 257, 300, 320, 321, 416])
+def test_bf16_every_gemm_tile_class(T_target):
+    """Query-slot totals that select each GEMM tile class, and both sides of
+    every boundary between them: the 16x16 form up to 96 slots, the 32x32
+    form above (eight-wave tiles up to 256 slots, four-wave tiles above;
+    32-k chunks at 225..320 slots, 16-k chunks above 320), the
+    packed-plane 32x32 tiles (split-K partials at 65..80 slots, every GEMM
+    at 97..112, with and without padding in the mixed tile), split-K and
+    unsplit paths, up to the 416-slot maximum."""
+    rng = np.random.default_rng(T_target)
+    L = _ragged_draft_lengths(T_target, rng)
     prefix = [int(p) for p in rng.integers(0, 200, size=len(L))]
     w = wl.custom_workload("tiny-bf16", prefix, L, seed=40 + T_target, q_sigma=1.0)
     dw = DeviceWeights(w.model, w.seed, gamma="uniform")
@@ -238,4 +245,44 @@ def test_bf16_every_gemm_tile_class(T_target):
     gpu = run_gpu(v, w, 0, b, "stochastic", seed=2, round_=3)
     rl, ref = run_oracle(w, b, "stochastic", seed=2, round_=3, weights=ws)
     _check(w, b, gpu, rl, ref, 2e-2, f"tiny-bf16/T={b.T}", "stochastic")
+    v.close()
+
+
+@pytest.mark.parametrize("T_target", [225, 240, 256])
+def test_split_gate_up_over_all_cus(T_target):
+    """At 225..256 slots a gate/up product of more than 128 and fewer than
+    256 row tiles is split over one workgroup per CU, each taking an equal
+    run of (tile, k-chunk) pairs; a tile's last workgroup adds the partial
+    sums the earlier ones left and applies SwiGLU.  Parity with the oracle
+    on a model whose 20480-wide feed-forward layer takes that form, then the
+    error path of the bounded wait: a limit of zero polls makes the pass
+    report a device error without committing, and the pass after it (limit
+    restored) is bit-identical to the first, so the tile counters came back
+    to zero."""
+    rng = np.random.default_rng(100 + T_target)
+    L = _ragged_draft_lengths(T_target, rng)
+    prefix = [int(p) for p in rng.integers(0, 300, size=len(L))]
+    w = wl.custom_workload("tiny-wide-ffn", prefix, L, seed=70 + T_target, q_sigma=1.0)
+    dw = DeviceWeights(w.model, w.seed, gamma="uniform")
+    v = make_verifier(w, dw)
+    load_synthetic_kv(v, w)
+    b = w.batch(0)
+    assert b.T == T_target
+    ws = oracle.WeightSource(w.model, w.seed, "uniform")
+    gpu = run_gpu(v, w, 0, b, "stochastic", seed=4, round_=1)
+    rl, ref = run_oracle(w, b, "stochastic", seed=4, round_=1, weights=ws)
+    _check(w, b, gpu, rl, ref, 2e-2, f"tiny-wide-ffn/T={b.T}", "stochastic")
+
+    state = [v.user_state(int(u)) for u in b.users]
+    v.wait_limit(0)
+    drafts, q, au = batch_to_device(b)
+    v.verify(0, w.assign, w.draft_len, drafts, q, "stochastic", 4, 1, au)
+    with pytest.raises(sdv.SdError) as e:
+        v.accept(0, w.n_users, True)
+    assert e.value.status == sdv.SD_EDEVICE
+    assert [v.user_state(int(u)) for u in b.users] == state
+    v.wait_limit(-1)
+    again = run_gpu(v, w, 0, b, "stochastic", seed=4, round_=1)
+    assert np.array_equal(again.logits, gpu.logits)
+    assert np.array_equal(again.n_acc, gpu.n_acc) and np.array_equal(again.token, gpu.token)
     v.close()

@@ -131,6 +131,9 @@ MODELS: Dict[str, ModelShape] = {
     "tiny-qknorm": ModelShape("tiny-qknorm", 2, 256, 4, 2, 64, 512, 1024, 1e4, 1e-6, True, "f32"),
     # bf16 toy decoder with the 32B head layout (hd 128, 8 q per kv head)
     "tiny-bf16": ModelShape("tiny-bf16", 2, 512, 8, 1, 128, 1024, 2048, 1e6, 1e-6, True, "bf16"),
+    # the same with a feed-forward width near Qwen3-32B's: 160 gate/up row
+    # tiles of 256 rows, more than half and fewer than all of 256 CUs
+    "tiny-wide-ffn": ModelShape("tiny-wide-ffn", 2, 512, 8, 1, 128, 20480, 2048, 1e6, 1e-6, True, "bf16"),
     "qwen3-1.7b": ModelShape("qwen3-1.7b", 28, 2048, 16, 8, 128, 6144, 151936, 1e6, 1e-6, True, "bf16"),
     "qwen3-32b": ModelShape("qwen3-32b", 64, 5120, 64, 8, 128, 25600, 151936, 1e6, 1e-6, True, "bf16"),
 }
