@@ -695,7 +695,7 @@ void k_gemm32(GemmP p) {
     }
 #pragma unroll
     for (int u = 0; u < PD; ++u) {
-        load_x(xr[u], min(c_begin + u, c_last));
+        if constexpr (CS == 1) load_x(xr[u], min(c_begin + u, c_last));
         load_w(wr[u], min(c_begin + u, c_last));
     }
     if constexpr (!SPLIT) {
@@ -706,22 +706,65 @@ void k_gemm32(GemmP p) {
         }
     }
     if constexpr (CS > 1) {
-        // Two X buffers; per chunk c: the X loads of chunk c + 1 are issued
-        // first; phases (k-step, plane) follow, the next phase's fragments
-        // requested before this phase's NS * MTW MFMAs; after the last plane
-        // of a k-step its weight registers are reloaded with the same k-step
-        // of chunk c + 1 (one register set, each fragment requested about a
-        // chunk ahead); X(c + 1) is then stored to the other buffer and the
-        // barrier publishes it.
+        // Two X buffers; per chunk c: the direct loads of X(c + 1) into the
+        // other buffer are issued first; phases (k-step, plane) follow, the
+        // next phase's fragments requested before this phase's NS * MTW
+        // MFMAs; after the last plane of a k-step its weight registers are
+        // reloaded with the same k-step of chunk c + 1 (one register set,
+        // each fragment requested about a chunk ahead); the wave then waits
+        // for its direct loads and the barrier publishes the buffer.
         constexpr int NPH = KS * PLS;
         static_assert(NPH % 2 == 0, "phase fragments alternate between two register sets");
+        // X is staged by direct global-to-LDS loads: a chunk is 64 blocks of
+        // 1 KB, block (plane, tile, row group of 8) holding 8 rows of 64 k
+        // (128 B each) whose 16-byte pieces are XOR-swizzled by the row
+        // (piece q at position q ^ ((row >> 1) & 7), row within the tile), so
+        // that the fragment reads of 16 rows hit 16 different bank groups.
+        // A wave's direct load fills one block (lane l: row l / 8, position
+        // l % 8), so each lane fetches the piece that belongs to its
+        // position; each wave loads eight blocks per chunk.
+        static_assert(MT == 8 && KC == 64 && PLS == 2 && NW == 8 && MTW == 4,
+                      "direct X staging: 64 blocks per chunk, 8 per wave");
+        constexpr int DBUF = PLS * MT * 32 * KC;  // bf16 elements per staged chunk
+        static_assert(2 * DBUF <= XS_ELEMS, "two staged chunks fit the staging array");
+        typedef __attribute__((address_space(3))) void lds_void;
+        uint32_t doff[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int blk = wv * 8 + i, pl = blk >> 5, mt = (blk >> 2) & 7, rb = blk & 3;
+            const int lrow = rb * 8 + (lane >> 3);
+            const int row = min(mt * 32 + lrow, p.T - 1);
+            const int pc = (lane & 7) ^ ((lrow >> 1) & 7);
+            doff[i] = (((uint32_t)pl * (uint32_t)p.T + (uint32_t)row) * (uint32_t)p.K + (uint32_t)pc * 8u) * 2u;
+        }
+        auto dma_x = [&](int c, int buf) {
+            bf16_t* base = xs + buf * DBUF + wv * 8 * 512;
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(xres, (lds_void*)(base + i * 512), 16, (int)doff[i],
+                                                         c * KC * 2, 0, kActAux);
+        };
+        // fragment reads in inline assembly: the compiler cannot tell them from
+        // the direct loads into the other buffer and would wait for every
+        // load in flight before them; their completion is waited for
+        // explicitly, with the fragments as operands
+        const uint32_t xs_addr = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16_t*)xs;
+        uint32_t loff[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+            loff[ks] = (uint32_t)((lc >> 3) * 1024 + (lc & 7) * 128 + (((2 * ks + lh) ^ ((lc >> 1) & 7)) * 16));
         bf16x8 xq[2][MTW];
         auto read_phase = [&](bf16x8 (&xf)[MTW], int buf, int ph) {
-            const bf16_t* xb = xs + buf * XBUF;
             const int ks = ph / PLS, pl = ph % PLS;
-#pragma unroll
-            for (int m = 0; m < MTW; ++m)
-                xf[m] = *(const bf16x8*)(xb + pl * PLANE + ((m0 + m) * 32 + lc) * LDX + ks * 16 + 8 * lh);
+            const uint32_t a = xs_addr + (uint32_t)(buf * DBUF * 2) + loff[ks] + (uint32_t)((pl * MT + m0) * 4096);
+            asm volatile(
+                "ds_read_b128 %0, %4\n\t"
+                "ds_read_b128 %1, %4 offset:4096\n\t"
+                "ds_read_b128 %2, %4 offset:8192\n\t"
+                "ds_read_b128 %3, %4 offset:12288"
+                : "=&v"(xf[0]), "=&v"(xf[1]), "=&v"(xf[2]), "=&v"(xf[3])
+                : "v"(a)
+                : "memory");
         };
         auto load_w_ks = [&](bf16x8 (&w)[NS], int c, int ks) {
 #pragma unroll
@@ -729,16 +772,23 @@ void k_gemm32(GemmP p) {
                 w[s] = __builtin_bit_cast(
                     bf16x8, __builtin_amdgcn_raw_buffer_load_b128(wres, woff[s], (c * KS + ks) * 512, kWeightAux));
         };
-        store_x(xr[0], 0);
+        dma_x(c_begin, 0);
         __syncthreads();
         read_phase(xq[0], 0, 0);
         for (int c = c_begin; c < c_end; ++c) {
             const int b = (c - c_begin) & 1;
             const int cn = min(c + 1, c_last);
-            load_x(xr[0], cn);
+            dma_x(cn, b ^ 1);
 #pragma unroll
             for (int ph = 0; ph < NPH; ++ph) {
-                if (ph + 1 < NPH) read_phase(xq[(ph + 1) & 1], b, ph + 1);
+                if (ph + 1 < NPH) {
+                    read_phase(xq[(ph + 1) & 1], b, ph + 1);
+                    asm volatile("s_waitcnt lgkmcnt(4)"
+                                 : "+v"(xq[ph & 1][0]), "+v"(xq[ph & 1][1]), "+v"(xq[ph & 1][2]), "+v"(xq[ph & 1][3]));
+                } else {
+                    asm volatile("s_waitcnt lgkmcnt(0)"
+                                 : "+v"(xq[ph & 1][0]), "+v"(xq[ph & 1][1]), "+v"(xq[ph & 1][2]), "+v"(xq[ph & 1][3]));
+                }
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int m = 0; m < MTW; ++m)
@@ -749,9 +799,12 @@ void k_gemm32(GemmP p) {
                 __builtin_amdgcn_sched_barrier(0);
                 if (ph % PLS == PLS - 1) load_w_ks(wr[0][ph / PLS], cn, ph / PLS);
             }
-            store_x(xr[0], b ^ 1);
-            __syncthreads();
-            read_phase(xq[0], b ^ 1, 0);
+            // this wave's direct loads of chunk cn precede the NS * KS weight
+            // loads issued since; the barrier then publishes every wave's
+            // block (all reads of the other buffer were waited for above)
+            wait_vm<NS * KS>();
+            barrier_nofence();
+            if (c + 1 < c_end) read_phase(xq[0], b ^ 1, 0);
         }
     } else {
     store_x(xr[0], 0);
