@@ -28,8 +28,8 @@ def _pass(v, w, n, b, dev, mode, stream, graph, seed=5, round_=0, commit=False):
     return n_acc[b.users].copy(), tok[b.users].copy(), lg.cpu().numpy()
 
 
-def _setup(prefix, draft, assign, seed):
-    w = wl.custom_workload("tiny-bf16", prefix, draft, seed=seed, assign=assign)
+def _setup(prefix, draft, assign, seed, model="tiny-bf16"):
+    w = wl.custom_workload(model, prefix, draft, seed=seed, assign=assign)
     dw = DeviceWeights(w.model, w.seed)
     v = make_verifier(w, dw, max_pending=max(2, w.n_batches), extra_ctx=64)
     load_synthetic_kv(v, w)
@@ -66,6 +66,28 @@ def test_graph_replays_match_eager(mode):
     v.close()
 
 
+def test_graph_replays_of_the_split_gate_up_product():
+    """At 240 slots the 20480-wide gate/up product of the wide-FFN toy model
+    is split over one workgroup per CU with per-tile counters that every
+    launch must leave at zero; replays of the captured pass (eager passes and
+    other work between them) stay bit-identical to the eager pass."""
+    prefix = [int(x) for x in np.random.default_rng(3).integers(0, 400, 20)]
+    w, dw, v, (b,) = _setup(prefix, [11] * 20, None, 9, model="tiny-wide-ffn")
+    assert b.T == 240
+    dev = batch_to_device(b)
+    st = torch.cuda.Stream()
+    ref = _pass(v, w, 0, b, dev, "stochastic", st, graph=False)
+    scratch = torch.randn(1 << 20, device="cuda")
+    for rep in range(4):
+        got = _pass(v, w, 0, b, dev, "stochastic", st, graph=True)
+        assert np.array_equal(got[0], ref[0]) and np.array_equal(got[1], ref[1]), rep
+        assert np.array_equal(got[2], ref[2]), f"replay {rep}: logits differ"
+        scratch.mul_(1.0001).add_(0.5)
+        eager = _pass(v, w, 0, b, dev, "stochastic", st, graph=False)
+        assert np.array_equal(eager[2], ref[2])
+    v.close()
+
+
 def test_graph_batches_on_alternating_streams():
     """Four batches in flight at once on two streams, each replayed from its
     own slot's graph, as the pipelined workload runs them."""
@@ -89,6 +111,33 @@ def test_graph_batches_on_alternating_streams():
             lg = lgt.cpu().numpy()
             assert np.array_equal(n_acc[b.users], refs[n][0]) and np.array_equal(tok[b.users], refs[n][1])
             assert np.array_equal(lg, refs[n][2]), (rep, n)
+    v.close()
+
+
+@pytest.mark.parametrize("graph", [False, True])
+def test_split_gate_up_batches_on_two_streams(graph):
+    """Two 240-slot batches of the wide-FFN toy model in flight at once on
+    two streams (each pass's split gate/up product uses its own slot's tile
+    counters, and its waits end while the other pass shares the CUs), three
+    times over, eagerly or from graphs; every pass equals the batch's pass
+    run alone."""
+    prefix = [int(x) for x in np.random.default_rng(4).integers(0, 400, 40)]
+    assign = [i % 2 for i in range(40)]
+    w, dw, v, batches = _setup(prefix, [11] * 40, assign, 23, model="tiny-wide-ffn")
+    assert [b.T for b in batches] == [240, 240]
+    devs = [batch_to_device(b) for b in batches]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    refs = [_pass(v, w, n, b, devs[n], "stochastic", streams[0], graph=False) for n, b in enumerate(batches)]
+    for rep in range(3):
+        for n in range(2):
+            d, q, au = devs[n]
+            v.verify(n, w.assign, w.draft_len, d, q, "stochastic", 5, 0, au, stream=streams[n], graph=graph)
+        for n, b in enumerate(batches):
+            lgt = v.logits(n, b.T, stream=streams[n])
+            n_acc, tok = v.accept(n, w.n_users)
+            torch.cuda.synchronize()
+            assert np.array_equal(n_acc[b.users], refs[n][0]) and np.array_equal(tok[b.users], refs[n][1])
+            assert np.array_equal(lgt.cpu().numpy(), refs[n][2]), (rep, n)
     v.close()
 
 
