@@ -525,8 +525,9 @@ void k_gemm32(GemmP p) {
     constexpr int XPT = (NPC + NTH - 1) / NTH;  // X pieces per thread
     constexpr bool XEVEN = NPC % NTH == 0;
     constexpr int PLANE = MT * 32 * LDX;  // LDS elements per plane
-    // NXB X staging buffers of XBUF elements; the split epilogue stages its
-    // partial sums in the same memory, which may need more
+    // NXB X staging buffers of XBUF elements (padded rows; the column-split
+    // form keeps two unpadded chunks in the same array); the split epilogue
+    // stages its partial sums in the same memory, which may need more
     constexpr int XBUF = PLS * PLANE;
     constexpr int NXB = 2;
     constexpr int STG_BYTES = SPLIT ? CS * 32 * (NW / CS * NS * 32 + 4) * 4 : 0;
@@ -596,10 +597,12 @@ void k_gemm32(GemmP p) {
     const int c_begin = SKF ? (piece == 0 ? sk_b[0] : sk_b[1]) : split * p.kchunks / p.S;
     const int c_end = SKF ? (piece == 0 ? sk_e[0] : sk_e[1]) : (split + 1) * p.kchunks / p.S;
 
-    // Register-ring pipeline with prefetch distance PD chunks: while chunk c
-    // is multiplied (X from LDS buffer c&1, W from ring set c % NB), X and W
-    // of chunk c+PD are requested into ring set (c+PD) % NB, and X(c+1),
-    // requested PD-1 chunks earlier, is stored to the other LDS buffer.  The
+    // Register-ring pipeline with prefetch distance PD chunks (the form
+    // without column split; the column-split form below stages X by direct
+    // loads): while chunk c is multiplied (X from LDS buffer c&1, W from
+    // ring set c % NB), X and W of chunk c+PD are requested into ring set
+    // (c+PD) % NB, and X(c+1), requested PD-1 chunks earlier, is stored to
+    // the other LDS buffer.  The
     // loop is unrolled by NB so that ring indices are compile-time constants
     // (register copies would force waits on loads still in flight), the
     // loads are unconditional (the chunk index is clamped; the last steps
