@@ -82,6 +82,10 @@ struct GemmP {
     // the epilogue (sk_nwg = 0: off)
     // the piece waits for at most sk_polls polls of the count
     int sk_nwg, sk_maxp, sk_polls;
+    // column-split form at 225-240 slots: the last slot tile holds the hi
+    // rows of slots 224-239 in its rows 0-15 and their lo rows in rows 16-31
+    // (one tile-plane instead of two); 0: off
+    int pkl;
     int* sk_cnt;
     int32_t* flags;  // device error bits (bit 2: a stream-K wait gave up)
 };
@@ -736,9 +740,13 @@ void k_gemm32(GemmP p) {
         for (int i = 0; i < 8; ++i) {
             const int blk = wv * 8 + i, pl = blk >> 5, mt = (blk >> 2) & 7, rb = blk & 3;
             const int lrow = rb * 8 + (lane >> 3);
-            const int row = min(mt * 32 + lrow, p.T - 1);
             const int pc = (lane & 7) ^ ((lrow >> 1) & 7);
-            doff[i] = (((uint32_t)pl * (uint32_t)p.T + (uint32_t)row) * (uint32_t)p.K + (uint32_t)pc * 8u) * 2u;
+            // packed last tile: rows 0-15 from the hi plane, 16-31 from the lo
+            // plane, of the same 16 slots
+            const bool pk = p.pkl && pl == 0 && mt == MT - 1;
+            const int spl = pk ? lrow >> 4 : pl;
+            const int row = min(mt * 32 + (pk ? lrow & 15 : lrow), p.T - 1);
+            doff[i] = (((uint32_t)spl * (uint32_t)p.T + (uint32_t)row) * (uint32_t)p.K + (uint32_t)pc * 8u) * 2u;
         }
         auto dma_x = [&](int c, int buf) {
             bf16_t* base = xs + buf * DBUF + wv * 8 * 512;
@@ -752,6 +760,7 @@ void k_gemm32(GemmP p) {
         // load in flight before them; their completion is waited for
         // explicitly, with the fragments as operands
         const uint32_t xs_addr = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16_t*)xs;
+        const bool pkl_half = p.pkl && half == CS - 1;  // this wave holds the packed tile
         uint32_t loff[KS];
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
@@ -797,8 +806,9 @@ void k_gemm32(GemmP p) {
                 for (int m = 0; m < MTW; ++m)
 #pragma unroll
                     for (int s = 0; s < NS; ++s)
-                        acc[s][m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wr[0][ph / PLS][s], xq[ph & 1][m],
-                                                                             acc[s][m], 0, 0, 0);
+                        if (!(m == MTW - 1 && ph % PLS == 1 && pkl_half))  // packed tile: one plane-phase
+                            acc[s][m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wr[0][ph / PLS][s], xq[ph & 1][m],
+                                                                                 acc[s][m], 0, 0, 0);
                 __builtin_amdgcn_sched_barrier(0);
                 if (ph % PLS == PLS - 1) load_w_ks(wr[0][ph / PLS], cn, ph / PLS);
             }
@@ -883,6 +893,21 @@ void k_gemm32(GemmP p) {
             sk_ord = ord;  // added tile by tile in the epilogue (fewer live registers)
         }
     }
+    // Packed last tile of the column-split form (its wave's tile MTW - 1):
+    // slot 224 + i's sums are those of lanes l and l ^ 16 (i = l % 16),
+    // added by v_permlane16_swap; run after the earlier stream-K pieces'
+    // sums are in
+    const bool pkl_fold = CS > 1 && p.pkl && half == CS - 1;
+    auto fold_last = [&]() {
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const auto pr = __builtin_amdgcn_permlane16_swap(__float_as_uint(acc[s][MTW - 1][e]),
+                                                                 __float_as_uint(acc[s][MTW - 1][e]), false, false);
+                acc[s][MTW - 1][e] = __uint_as_float(pr[0]) + __uint_as_float(pr[1]);
+            }
+    };
     // Accumulator layout: lane l holds slot t = 32*m + l % 32 and, in
     // registers 4q..4q+3, weight rows 8q + 4*(l/32) + 0..3 of its group.
     // Packed planes: slot t's sums are those of tile m and tile m + a + 1
@@ -910,6 +935,7 @@ void k_gemm32(GemmP p) {
         constexpr int NU = NW / CS;  // row units per workgroup
         static_assert(NU * NSLOT * (int)sizeof(VStat) <= (int)sizeof(xs), "statistics staging exceeds LDS");
         VStat* stg = reinterpret_cast<VStat*>(xs);
+        if (pkl_fold) fold_last();
 #pragma unroll
         for (int m = 0; m < MTO; ++m) {
             const int t = (m0 + m) * 32 + lc;
@@ -951,6 +977,7 @@ void k_gemm32(GemmP p) {
         const int u0 = wgi * p.G / p.WPS;
         const int nrow = ((wgi + 1) * p.G / p.WPS - u0) * NS * 32;
         const int wrow = wv / CS;  // row unit within the workgroup
+        if (pkl_fold) fold_last();
 #pragma unroll
         for (int m = 0; m < (PK ? PA + 1 : MTW); ++m) {
             if (m * 32 >= p.T) break;  // so are the other halves' tiles m + MTW * h
@@ -1000,6 +1027,7 @@ void k_gemm32(GemmP p) {
                     }
             }
         }
+        if (m == MTW - 1 && pkl_fold) fold_last();
         const int t = (m0 + m) * 32 + lc;
         if (!has_unit || t >= p.T || (PK && m == PA && lc >= 16)) continue;
         const float sc = rsl[t];
@@ -1391,6 +1419,7 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
     // idle (gate/up at 225-256 slots: 200 row tiles of 256 rows on 256 CUs)
     p.sk_nwg = 0;
     p.sk_maxp = 0;
+    p.pkl = sh.CS > 1 && sh.MT == 8 && g.T > 224 && g.T <= 240;
     p.sk_polls = g.sk_polls;
     p.sk_cnt = g.sk_cnt;
     p.flags = g.flags;

@@ -222,13 +222,14 @@ def _ragged_draft_lengths(T_target, rng):
     return L
 
 
-@pytest.mark.parametrize("T_target", [17, 64, 65, 70, 75, 80, 96, 97, 105, 112, 113, 150, 224, 225, 250,
-                                      256, 257, 300, 320, 321, 416])
+@pytest.mark.parametrize("T_target", [17, 64, 65, 70, 75, 80, 96, 97, 105, 112, 113, 150, 224, 225, 232, 240,
+                                      241, 250, 256, 257, 300, 320, 321, 416])
 def test_bf16_every_gemm_tile_class(T_target):
     """Query-slot totals that select each GEMM tile class, and both sides of
     every boundary between them: the 16x16 form up to 96 slots, the 32x32
     form above (eight-wave tiles up to 256 slots, four-wave tiles above;
-    32-k chunks at 225..320 slots, 16-k chunks above 320), the
+    32-k chunks at 225..320 slots, 16-k chunks above 320; at 225..240 the
+    last slot tile holds both planes of its 16 slots), the
     packed-plane 32x32 tiles (split-K partials at 65..80 slots, every GEMM
     at 97..112, with and without padding in the mixed tile), split-K and
     unsplit paths, up to the 416-slot maximum."""
