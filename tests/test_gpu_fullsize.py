@@ -197,7 +197,7 @@ def test_qwen3_1p7b_full_batch_matches_oracle():
     v.close()
     del dw
     torch.cuda.empty_cache()
-    ref = oracle.forward(m, oracle.WeightSource(m, w.seed),
+    ref = oracle.forward(m, _Progress(m, w.seed),
                          oracle.KVSource(m, w.seed, b.users, b.prefix_len), b.prefix_len, b.n_slots,
                          b.slot_tokens())
     err = logit_rel_err(lg, ref)
