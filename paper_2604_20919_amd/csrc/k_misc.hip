@@ -389,8 +389,10 @@ __global__ __launch_bounds__(256) void k_qkrope(BatchView bv, const float* qkv, 
 // and four heads of one slot per wave.  Lane l of a head owns dims 4l..4l+3
 // and their rotation partners 64+4l..64+4l+3, so every partial-plane read is
 // a 16-byte load (a wave reads 1 KB per instruction instead of 256 B) and
-// the query and key rows leave as 8-byte stores.  One wave per workgroup,
-// so that few waves (small batches) still spread over the CUs.
+// the query and key rows leave as 8-byte stores.  Value heads take lanes of
+// their own (they are only summed, scaled and appended), so every wave
+// carries the same loads.  One wave per workgroup, so that few waves (small
+// batches) still spread over the CUs.
 __global__ __launch_bounds__(64) void k_qkrope_bf16(BatchView bv, const float* qkv, int S,
                                                      const float* cs, bf16_t* qbuf, KVPool kv,
                                                      int layer, const bf16_t* qn, const bf16_t* kn,
@@ -399,25 +401,24 @@ __global__ __launch_bounds__(64) void k_qkrope_bf16(BatchView bv, const float* q
     constexpr int HD = 128, HALF = 64;
     const int wave = blockIdx.x;
     const int lane = threadIdx.x, l = lane & 15;
-    const int nh = hq + hkv, ng = (nh + 3) >> 2;  // head groups of four per slot
+    // q, k and v heads (contiguous in the QKV output), four per wave
+    const int nh = hq + 2 * hkv, ng = (nh + 3) >> 2;
     const int t = wave / ng;
     if (t >= bv.T) return;
     const int h = (wave % ng) * 4 + (lane >> 4);
     const bool act = h < nh;
-    const bool is_q = h < hq;
-    const int nqkv = (hq + 2 * hkv) * HD;
+    const bool is_q = h < hq, is_v = h >= hq + hkv;
+    const int nqkv = nh * HD;
     const size_t plane = (size_t)bv.T * nqkv;
-    const int col = (is_q ? h * HD : hq * HD + (h - hq) * HD) + 4 * l;
-    const float* src = qkv + (size_t)t * nqkv + col;
-    const float* vs = qkv + (size_t)t * nqkv + (size_t)(hq + hkv) * HD + (size_t)(is_q ? 0 : h - hq) * HD + 4 * l;
+    const float* src = qkv + (size_t)t * nqkv + (size_t)h * HD + 4 * l;
     float ssb[kNormKMax / kNormBlock];
 #pragma unroll
     for (int b = 0; b < kNormKMax / kNormBlock; ++b)
         ssb[b] = nss != nullptr && b < nnb ? nss[(size_t)t * nnb + b] : 0.f;
     // partial planes added in split order, eight planes' loads in flight
-    f32x4 xa = f32x4{0.f, 0.f, 0.f, 0.f}, xb = xa, va = xa, vb = xa;
+    f32x4 xa = f32x4{0.f, 0.f, 0.f, 0.f}, xb = xa;
     for (int sp = 0; sp < S; sp += 8) {
-        f32x4 a0[8], a1[8], b0[8], b1[8];
+        f32x4 a0[8], a1[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const bool ok = act && sp + u < S;
@@ -425,25 +426,35 @@ __global__ __launch_bounds__(64) void k_qkrope_bf16(BatchView bv, const float* q
             const f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
             a0[u] = ok ? *(const f32x4*)(src + o) : z;
             a1[u] = ok ? *(const f32x4*)(src + o + HALF) : z;
-            b0[u] = ok && !is_q ? *(const f32x4*)(vs + o) : z;
-            b1[u] = ok && !is_q ? *(const f32x4*)(vs + o + HALF) : z;
         }
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             xa += a0[u];
             xb += a1[u];
-            va += b0[u];
-            vb += b1[u];
         }
     }
-    float rt = 1.0f;
     if (nss != nullptr) {
         float ssx = 0.f;
 #pragma unroll
         for (int b = 0; b < kNormKMax / kNormBlock; ++b) ssx += ssb[b];
-        rt = 1.0f / sqrtf(ssx / (float)d + eps);
+        const float rt = 1.0f / sqrtf(ssx / (float)d + eps);
         xa *= rt;
         xb *= rt;
+    }
+    const int b = bv.slot_b[t];
+    const int pos = bv.prefix[b] + bv.slot_j[t];
+    if (is_v) {
+        if (!act) return;
+        const int g = h - hq - hkv;
+        const int page = bv.page_table[(size_t)b * bv.max_pages + pos / kPageTokens];
+        const int off = pos % kPageTokens;
+        bf16_t* vd = (bf16_t*)kv.base + kv.v_off(layer, page, g);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            vd[(size_t)(4 * l + e) * kPageTokens + off] = f32_to_bf16(xa[e]);
+            vd[(size_t)(HALF + 4 * l + e) * kPageTokens + off] = f32_to_bf16(xb[e]);
+        }
+        return;
     }
     if (qk_norm) {
         float ss = 0.f;
@@ -481,20 +492,11 @@ __global__ __launch_bounds__(64) void k_qkrope_bf16(BatchView bv, const float* q
         return;
     }
     const int g = h - hq;
-    const int b = bv.slot_b[t];
-    const int pos = bv.prefix[b] + bv.slot_j[t];
     const int page = bv.page_table[(size_t)b * bv.max_pages + pos / kPageTokens];
     const int off = pos % kPageTokens;
-    bf16_t* base = (bf16_t*)kv.base;
-    bf16_t* kd = base + kv.k_off(layer, page, g) + (size_t)off * HD + 4 * l;
+    bf16_t* kd = (bf16_t*)kv.base + kv.k_off(layer, page, g) + (size_t)off * HD + 4 * l;
     *(uint2*)kd = pack_bf16x4(ya);
     *(uint2*)(kd + HALF) = pack_bf16x4(yb);
-    bf16_t* vd = base + kv.v_off(layer, page, g);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        vd[(size_t)(4 * l + e) * kPageTokens + off] = f32_to_bf16(va[e] * rt);
-        vd[(size_t)(HALF + 4 * l + e) * kPageTokens + off] = f32_to_bf16(vb[e] * rt);
-    }
 }
 
 void launch_qkv_finish(const Dims& D, const BatchView& bv, const SlotBufs& sb, const KVPool& kv,
@@ -502,7 +504,7 @@ void launch_qkv_finish(const Dims& D, const BatchView& bv, const SlotBufs& sb, c
                        hipStream_t s) {
     if (D.bf16) {
         // head_dim 128 (checked at init): four heads per wave
-        const int waves = bv.T * ((D.hq + D.hkv + 3) / 4);
+        const int waves = bv.T * ((D.hq + 2 * D.hkv + 3) / 4);
         hipLaunchKernelGGL(k_qkrope_bf16, dim3(waves), dim3(64), 0, s, bv, part, S, sb.cs,
                            (bf16_t*)sb.qbuf, kv, layer, (const bf16_t*)qn, (const bf16_t*)kn, D.hq,
                            D.hkv, D.qk_norm, D.eps, sb.ssq, sb.nsq, D.d);
