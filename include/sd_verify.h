@@ -44,7 +44,7 @@ enum {
     SD_ESTATE = -4,   /* call out of order (batch pending / not pending) */
     SD_EDEVICE = -5,  /* the GPU found bad input data (token id out of range), or a
                          bounded wait of one workgroup for another gave up */
-    SD_ENOTIMPL = -6, /* configuration not supported by this build */
+    SD_ENOTIMPL = -6, /* configuration the library does not implement */
     SD_ENODEV = -7,   /* no usable gfx950 device */
     SD_ELIMIT = -8    /* input beyond the fixed limits of sd_sample_logits_noalloc */
 };

@@ -192,7 +192,7 @@ __device__ __forceinline__ void swiglu_store4(const GemmP& p, int t, int col, f3
 // [slot][row] (row stride ldr floats), so that each 64-lane store writes
 // 1 KB of one partial-sum row instead of 32-byte pieces of 32 rows.  Writes
 // nsl slot rows starting at slot t0; only the first nrow rows are the
-// workgroup's.  (Same-box kernel traces at 80 slots: QKV / O / down
+// workgroup's.  (Kernel traces on one machine at 80 slots: QKV / O / down
 // 31.0 / 25.0 / 55.9 -> 29.8 / 23.7 / 53.5 us.)
 template <int NTH, int WR>
 __device__ __forceinline__ void store_partial_rows(const GemmP& p, const float* stg, int ldr, int split,
@@ -1220,11 +1220,11 @@ static GemmShape shape_for(int T, int vcols, bool raw, int K) {
     if (mt <= 7) return w8 ? GemmShape{32, mt, 1, 64, 8, 1, 0} : GemmShape{32, mt, 1, 64, 4, 1, 0};
     // 225..256 slots: eight waves with 32-k chunks (double-buffered staging
     // of 2 x 256 rows then fits one workgroup of 256 weight rows per CU);
-    // same-box probe at T = 240: gate/up 292 vs 392 us, QKV 63 vs 99, O 51
+    // probe on one machine at T = 240: gate/up 292 vs 392 us, QKV 63 vs 99, O 51
     // vs 93, down 143 vs 210 us against four waves with 64-k chunks
     if (mt <= 8) {
         // 64-row units shared by two waves (four slot tiles each) with 64-k
-        // chunks: every B fragment feeds two MFMAs.  Same-box timing of the
+        // chunks: every B fragment feeds two MFMAs.  Timing on one machine of the
         // 32B shapes at T = 229 in isolation: gate/up 263 vs 293 us, QKV 57
         // vs 59, O 52 vs 56, down 121 vs 137 us against 32-row units
         if (vcols % 64 == 0) return GemmShape{32, 8, 2, 64, 8, 1, 0, 0, 2};
