@@ -222,8 +222,8 @@ def _ragged_draft_lengths(T_target, rng):
     return L
 
 
-@pytest.mark.parametrize("T_target", [17, 64, 65, 70, 75, 80, 96, 97, 105, 112, 113, 150, 224, 225, 232, 240,
-                                      241, 250, 256, 257, 300, 320, 321, 416])
+@pytest.mark.parametrize("T_target", [17, 64, 65, 70, 75, 80, 96, 97, 105, 112, 113, 120, 128, 129, 150, 224, 225,
+                                      232, 240, 241, 250, 256, 257, 300, 320, 321, 416])
 def test_bf16_every_gemm_tile_class(T_target):
     """Query-slot totals that select each GEMM tile class, and both sides of
     every boundary between them: the 16x16 form up to 96 slots, the 32x32
