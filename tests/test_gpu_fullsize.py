@@ -1,7 +1,7 @@
 """Parity at the benchmark sizes.
 
 The Qwen3-32B-shaped workloads (16-user batch, 32-user ragged batch, four
-pipelined 16-user batches, plus two batches at 40 and 88 slots) run through
+pipelined 16-user batches, plus batches at 40, 88 and 132 slots) run through
 the C ABI exactly as the benchmark runs them, and the oracle recomputes
 users one by one (users are independent, so a user's logits and decisions
 do not depend on the rest of its batch):
@@ -10,8 +10,10 @@ do not depend on the rest of its batch):
     the user holding its first slot, plus the users with the shortest and
     the longest context (one attention chunk against several) and the most
     drafts;
-  * the pipelined batches: the user with most slots in the first batch and
-    the one with the longest prefix in the last.
+  * the pipelined batches: in the first batch (97..112 slots: packed
+    planes, a partly filled last slot tile) the user with most slots and
+    the one holding the last slot; in the last the one with the longest
+    prefix.
 All 32B workloads are drawn with one seed (their shapes and distributions
 are the benchmark's; the draws differ from the benchmark's own seeds) so
 that the host generates the 64 layers once for the oracle.  The
@@ -42,6 +44,9 @@ WORKLOADS32 = ("qwen3-32b-b16", "qwen3-32b-ragged32", "qwen3-32b-pipe4x16")
 CUSTOM32 = {
     "qwen3-32b-t40": ([100 + 37 * i for i in range(8)], [4] * 8),
     "qwen3-32b-t88": ([64 + 23 * i for i in range(16)], [4, 5] * 8),
+    # five 32-slot tiles of the 32x32 form (129..160 slots), which the
+    # pipelined batches reach with the benchmark's draws
+    "qwen3-32b-t132": ([64 + 23 * i for i in range(16)], [7] * 12 + [8] * 4),
 }
 MODES32 = {"qwen3-32b-b16": ("stochastic", "greedy")}
 TOL = 2e-2
@@ -66,7 +71,7 @@ def _pick(w: wl.Workload, n: int, b: wl.Batch):
     """Indices (within batch n) of the users the oracle recomputes."""
     if w.n_batches > 1:
         if n == 0:
-            return [int(np.argmax(b.draft_len))]
+            return sorted({int(np.argmax(b.draft_len)), len(b.users) - 1})
         return [int(np.argmax(b.prefix_len))] if n == w.n_batches - 1 else []
     if np.all(b.draft_len == b.draft_len[0]) and np.all(b.prefix_len == b.prefix_len[0]):
         return list(range(len(b.users)))
