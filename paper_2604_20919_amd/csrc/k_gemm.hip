@@ -1207,6 +1207,13 @@ static GemmShape shape_for(int T, int vcols, bool raw, int K) {
             const int s8 = std::min(std::max(1, K / 128 / 2), std::max(1, cu_count() / tiles8));
             if (10 * tiles8 * s8 < 9 * cu_count()) return GemmShape{16, mt, 2, 64, 4, 2, 0, 1};
         }
+        // SwiGLU products of fewer than a quarter as many 256-row tiles as
+        // CUs (the Qwen3-1.7B gate/up: 48): four-wave 128-row tiles, split
+        // as the eight-wave ones are (two splits, 192 workgroups; one
+        // machine at T = 60: gate/up with its reduction 25.7 -> 24.2 us per
+        // layer, the step 2.45-2.47 -> 2.42-2.43 ms; four splits 26.4 us,
+        // three 28.3 us, unsplit 28.7 us)
+        if (!raw && wide && vcols / 256 * 4 < cu_count()) return GemmShape{16, mt, 2, 64, 4, 2, 0, 1};
         // the lm_head (151936 rows: not a multiple of 256) takes the
         // eight-wave tiles too; its last workgroup has fewer units
         if (wide || (!raw && vcols % 32 == 0)) return GemmShape{16, mt, 2, 128, 8, 1, 0};
