@@ -1214,6 +1214,13 @@ static GemmShape shape_for(int T, int vcols, bool raw, int K) {
         // layer, the step 2.45-2.47 -> 2.42-2.43 ms; four splits 26.4 us,
         // three 28.3 us, unsplit 28.7 us)
         if (!raw && wide && vcols / 256 * 4 < cu_count()) return GemmShape{16, mt, 2, 64, 4, 2, 0, 1};
+        // an lm_head over a short k (the Qwen3-1.7B one: 151936 x 2048,
+        // weight-bound at these slot counts) on four-wave 128-row tiles:
+        // 1187 shorter workgroups leave a shorter tail than 594 eight-wave
+        // ones at one per CU (one machine at T = 60: 158 -> 143-148 us; the
+        // Qwen3-32B lm_head at T = 80, MFMA-heavier, is slower that way:
+        // 338-350 -> 359-363 us)
+        if (!raw && !wide && vcols % 32 == 0 && K <= 2048) return GemmShape{16, mt, 2, 64, 4, 2, 0};
         // the lm_head (151936 rows: not a multiple of 256) takes the
         // eight-wave tiles too; its last workgroup has fewer units
         if (wide || (!raw && vcols % 32 == 0)) return GemmShape{16, mt, 2, 128, 8, 1, 0};
@@ -1403,6 +1410,13 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
     const int upw = sh.NW / sh.CS;  // row units per workgroup
     p.tiles = (units + upw - 1) / upw;
     int S = g.epi == EPI_LMSTAT ? 1 : choose_splits(p.tiles, p.kchunks, sh.FILL ? 8 : sh.NW);
+    // four-wave split-K tiles over a short k (the Qwen3-1.7B QKV and O
+    // projections, k = 2048): half the splits, so each split keeps four
+    // 64-k chunks and the consumer reads half the partial planes (one
+    // machine at T = 60, each with its consumer: QKV 18.8 -> 18.4 us, O
+    // 14.3 -> 14.0 us per layer; the down projection, k = 6144, is slower
+    // so: 19.4 -> 20.0 us)
+    if (g.raw && sh.NW == 4 && sh.FILL && g.K <= 2048) S = std::max(1, S / 2);
     while (S > 1 && (size_t)S * g.T * p.vcols > sb.gpart_floats) {
         int t = S - 1;
         while (t > 1 && p.kchunks % t) --t;
