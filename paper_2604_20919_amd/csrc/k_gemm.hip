@@ -214,7 +214,11 @@ __device__ __forceinline__ void store_partial_rows(const GemmP& p, const float* 
 // stores are ordered so that the rows written together sit 16/R rows apart
 // (R rows per 32 lanes), which also spreads them over every bank.  With 8
 // (stride 272 or 144 bytes) rows 0 and 15 of a read share banks.
-template <int MT, int NSUB, int KC, int EPI, bool SPLIT, int NW, int PL, int PD, int XPAD = 16>
+// LA (split SwiGLU product reduced by its last split): the S workgroups of
+// a row tile each take a k range, store their sums and count themselves;
+// the one that counts last adds every split's sums in split order and
+// runs the SwiGLU epilogue, so no separate reduction kernel is needed.
+template <int MT, int NSUB, int KC, int EPI, bool SPLIT, int NW, int PL, int PD, int XPAD = 16, bool LA = false>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, 2)))
 void k_gemm16(GemmP p) {
     constexpr int NTH = 64 * NW;         // threads per workgroup
@@ -230,14 +234,17 @@ void k_gemm16(GemmP p) {
     constexpr int PLANE = MT * 16 * LDX;  // LDS elements per plane
     static_assert(EPI != EPI_SWIGLU || NSUB % 2 == 0, "SwiGLU pairs gate/up sub-tiles");
     static_assert(2 * PL * PLANE * 2 <= 160 * 1024, "X staging exceeds LDS");
+    static_assert(!LA || (!SPLIT && EPI == EPI_SWIGLU), "last-split reduction: the SwiGLU product");
     __shared__ __attribute__((aligned(16))) bf16_t xs[2][PL * PLANE];
     __shared__ float rsl[SPLIT ? 1 : MT * ROWS_PER_TILE];  // per-slot RMSNorm factor
+    __shared__ int la_count;  // LA: splits of this tile counted before this one
 
     // k split of this workgroup (consecutive workgroups take consecutive
     // splits, so with S a divisor of 8 every XCD works on one k range) and
     // its range of wave units
-    const int split = SPLIT ? blockIdx.x % p.S : 0;
-    const int wgi = SPLIT ? blockIdx.x / p.S : blockIdx.x;
+    constexpr bool KSPLIT = SPLIT || LA;
+    const int split = KSPLIT ? blockIdx.x % p.S : 0;
+    const int wgi = KSPLIT ? blockIdx.x / p.S : blockIdx.x;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int lr = lane & 15, lg = lane >> 4;
     const int mt_act = (p.T + 15) >> 4;
@@ -426,6 +433,65 @@ void k_gemm16(GemmP p) {
             store_x(xr[(u + 1) % NB], ((c - c_begin) & 1) ^ 1);
             __syncthreads();
         }
+    }
+
+    if constexpr (LA) {
+        // The tile's splits exchange their sums through memory at system
+        // scope (written through, read past the caches), ordered by the
+        // count: each split stores into a slot of its own, waits for the
+        // stores, passes a barrier and counts; the split that counts last
+        // (no waiting anywhere: every split goes on or leaves at once)
+        // resets the count and loads the other slots.  Slot layout: piece
+        // j = s * MT + m of thread i at j * NTH + i (16 bytes, coalesced).
+        constexpr int PER = NSUB * MT;  // 16-byte accumulator pieces per thread
+        const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(p.part + (size_t)wgi * p.S * (size_t)(NTH * PER * 4)), (short)0, p.S * NTH * PER * 16,
+            0x00020000);
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s)
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[s][m]), r,
+                                                       ((split * PER + s * MT + m) * NTH + (int)threadIdx.x) * 16,
+                                                       0, 17);
+        wait_vm<0>();
+        __syncthreads();
+        if (threadIdx.x == 0)
+            la_count = __hip_atomic_fetch_add(p.sk_cnt + wgi, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        __syncthreads();
+        if (la_count < p.S - 1) return;
+        // every split has counted: back to zero for the next launch
+        if (threadIdx.x == 0) __hip_atomic_store(p.sk_cnt + wgi, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        // all splits' sums in split order (this split's from its registers)
+        f32x4 tot[NSUB][MT];
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s)
+#pragma unroll
+            for (int m = 0; m < MT; ++m) tot[s][m] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int sp = 0; sp < p.S; ++sp) {
+            if (sp == split) {
+#pragma unroll
+                for (int s = 0; s < NSUB; ++s)
+#pragma unroll
+                    for (int m = 0; m < MT; ++m) tot[s][m] += acc[s][m];
+                continue;
+            }
+            u32x4 v[NSUB][MT];
+#pragma unroll
+            for (int s = 0; s < NSUB; ++s)
+#pragma unroll
+                for (int m = 0; m < MT; ++m)
+                    v[s][m] = __builtin_amdgcn_raw_buffer_load_b128(
+                        r, ((sp * PER + s * MT + m) * NTH + (int)threadIdx.x) * 16, 0, 17);
+#pragma unroll
+            for (int s = 0; s < NSUB; ++s)
+#pragma unroll
+                for (int m = 0; m < MT; ++m) tot[s][m] += __builtin_bit_cast(f32x4, v[s][m]);
+        }
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s)
+#pragma unroll
+            for (int m = 0; m < MT; ++m) acc[s][m] = tot[s][m];
     }
 
     if constexpr (EPI == EPI_LMSTAT) {
@@ -1315,6 +1381,19 @@ static GemmFn pick(const GemmShape& sh, int epi, bool skf = false) {
     return sh.NW == 8 ? pick_nw<8, SPLIT>(sh, epi) : pick_nw<4, SPLIT>(sh, epi);
 }
 
+// the last-split SwiGLU product on the four-wave 16x16 tiles
+static GemmFn pick_la(const GemmShape& sh) {
+    if (sh.F != 16 || sh.NW != 4 || sh.NSUB != 2 || sh.KC != 64 || sh.PD != 2) return nullptr;
+    switch (sh.MT) {
+        case 2: return k_gemm16<2, 2, 64, EPI_SWIGLU, false, 4, 2, 2, 16, true>;
+        case 3: return k_gemm16<3, 2, 64, EPI_SWIGLU, false, 4, 2, 2, 16, true>;
+        case 4: return k_gemm16<4, 2, 64, EPI_SWIGLU, false, 4, 2, 2, 16, true>;
+        case 5: return k_gemm16<5, 2, 64, EPI_SWIGLU, false, 4, 2, 2, 16, true>;
+        case 6: return k_gemm16<6, 2, 64, EPI_SWIGLU, false, 4, 2, 2, 16, true>;
+    }
+    return nullptr;
+}
+
 static ReduceFn pick_reduce(int epi) {
     switch (epi) {
         case EPI_RESID: return k_splitk_reduce<EPI_RESID>;
@@ -1465,6 +1544,17 @@ int launch_gemm(const Dims& D, const GemmCall& g, const SlotBufs& sb, hipStream_
     } else if (S == 1) {
         hipLaunchKernelGGL(pick<false>(sh, g.epi), dim3(p.tiles), dim3(64 * sh.NW), 0, s, p);
     } else {
+        // a split SwiGLU product on four-wave tiles: its last split adds the
+        // others' sums (slots of NTH x NSUB x MT x 4 floats per split and
+        // tile) and runs the epilogue, no reduction kernel
+        const size_t la_floats = (size_t)p.tiles * S * (64 * sh.NW) * sh.NSUB * sh.MT * 4;
+        const GemmFn la = g.epi == EPI_SWIGLU && g.sk_cnt && p.tiles <= kSkCounters && la_floats <= sb.gpart_floats
+                              ? pick_la(sh)
+                              : nullptr;
+        if (la) {
+            hipLaunchKernelGGL(la, dim3(p.tiles * S), dim3(64 * sh.NW), 0, s, p);
+            return S;
+        }
         hipLaunchKernelGGL(pick<true>(sh, g.epi), dim3(p.tiles * S), dim3(64 * sh.NW), 0, s, p);
         const int ncols = g.epi == EPI_SWIGLU ? p.vcols / 2 : p.vcols;
         const int n = g.T * (ncols / 4);
