@@ -249,6 +249,28 @@ def test_bf16_every_gemm_tile_class(T_target):
     v.close()
 
 
+@pytest.mark.parametrize("T_target", [40, 120])
+def test_split_gate_up_with_reduction_kernel(T_target):
+    """A gate/up product of 96 row tiles of 256 rows (a 12288-wide
+    feed-forward layer) below 225 slots is split over k in two, and a
+    separate kernel adds the halves and applies SwiGLU: the form for
+    products too wide for the four-wave tiles and too narrow to fill the
+    CUs unsplit.  Parity with the oracle."""
+    rng = np.random.default_rng(300 + T_target)
+    L = _ragged_draft_lengths(T_target, rng)
+    prefix = [int(p) for p in rng.integers(0, 300, size=len(L))]
+    w = wl.custom_workload("tiny-mid-ffn", prefix, L, seed=110 + T_target, q_sigma=1.0)
+    dw = DeviceWeights(w.model, w.seed, gamma="uniform")
+    v = make_verifier(w, dw)
+    load_synthetic_kv(v, w)
+    b = w.batch(0)
+    assert b.T == T_target
+    gpu = run_gpu(v, w, 0, b, "stochastic", seed=4, round_=1)
+    rl, ref = run_oracle(w, b, "stochastic", seed=4, round_=1, weights=oracle.WeightSource(w.model, w.seed, "uniform"))
+    _check(w, b, gpu, rl, ref, 2e-2, f"tiny-mid-ffn/T={b.T}", "stochastic")
+    v.close()
+
+
 @pytest.mark.parametrize("T_target", [225, 240, 256])
 def test_split_gate_up_over_all_cus(T_target):
     """At 225..256 slots a gate/up product of more than 128 and fewer than

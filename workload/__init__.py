@@ -134,6 +134,10 @@ MODELS: Dict[str, ModelShape] = {
     # the same with a feed-forward width near Qwen3-32B's: 160 gate/up row
     # tiles of 256 rows, more than half and fewer than all of 256 CUs
     "tiny-wide-ffn": ModelShape("tiny-wide-ffn", 2, 512, 8, 1, 128, 20480, 2048, 1e6, 1e-6, True, "bf16"),
+    # 96 gate/up row tiles: split over k in two and added by a separate
+    # reduction (too wide for the four-wave tiles, too narrow to fill the
+    # CUs unsplit)
+    "tiny-mid-ffn": ModelShape("tiny-mid-ffn", 2, 512, 8, 1, 128, 12288, 2048, 1e6, 1e-6, True, "bf16"),
     "qwen3-1.7b": ModelShape("qwen3-1.7b", 28, 2048, 16, 8, 128, 6144, 151936, 1e6, 1e-6, True, "bf16"),
     "qwen3-32b": ModelShape("qwen3-32b", 64, 5120, 64, 8, 128, 25600, 151936, 1e6, 1e-6, True, "bf16"),
 }
