@@ -1276,9 +1276,10 @@ static GemmShape shape_for(int T, int vcols, bool raw, int K) {
         // SwiGLU products of fewer than a quarter as many 256-row tiles as
         // CUs (the Qwen3-1.7B gate/up: 48): four-wave 128-row tiles, split
         // as the eight-wave ones are (two splits, 192 workgroups; one
-        // machine at T = 60: gate/up with its reduction 25.7 -> 24.2 us per
-        // layer, the step 2.45-2.47 -> 2.42-2.43 ms; four splits 26.4 us,
-        // three 28.3 us, unsplit 28.7 us)
+        // machine at T = 60, then with a separate reduction kernel: gate/up
+        // 25.7 -> 24.2 us per layer, the step 2.45-2.47 -> 2.42-2.43 ms;
+        // four splits 26.4 us, three 28.3 us, unsplit 28.7 us).  The split
+        // is now reduced by its last split (launch_gemm): 23.1 us.
         if (!raw && wide && vcols / 256 * 4 < cu_count()) return GemmShape{16, mt, 2, 64, 4, 2, 0, 1};
         // an lm_head over a short k (the Qwen3-1.7B one: 151936 x 2048,
         // weight-bound at these slot counts) on four-wave 128-row tiles:
