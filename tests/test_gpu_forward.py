@@ -249,6 +249,37 @@ def test_bf16_every_gemm_tile_class(T_target):
     v.close()
 
 
+@pytest.mark.parametrize("T_target", [17, 40, 96])
+def test_last_split_gate_up_repeats_and_never_waits(T_target):
+    """Below 97 slots the toy bf16 model's gate/up product (8 row tiles of
+    128 rows) is split over k in four, and whichever split of a tile counts
+    last adds the others' sums in split order and applies SwiGLU.  Parity
+    with the oracle; a second pass bit-identical to the first (the tile
+    counters came back to zero, the sum order does not depend on which
+    split comes last); and with the stream-K wait bound at zero polls the
+    pass still succeeds, since this form never waits."""
+    rng = np.random.default_rng(400 + T_target)
+    L = _ragged_draft_lengths(T_target, rng)
+    prefix = [int(p) for p in rng.integers(0, 300, size=len(L))]
+    w = wl.custom_workload("tiny-bf16", prefix, L, seed=130 + T_target, q_sigma=1.0)
+    dw = DeviceWeights(w.model, w.seed, gamma="uniform")
+    v = make_verifier(w, dw)
+    load_synthetic_kv(v, w)
+    b = w.batch(0)
+    assert b.T == T_target
+    gpu = run_gpu(v, w, 0, b, "stochastic", seed=4, round_=1)
+    rl, ref = run_oracle(w, b, "stochastic", seed=4, round_=1, weights=oracle.WeightSource(w.model, w.seed, "uniform"))
+    _check(w, b, gpu, rl, ref, 2e-2, f"tiny-bf16/T={b.T}", "stochastic")
+    again = run_gpu(v, w, 0, b, "stochastic", seed=4, round_=1)
+    assert np.array_equal(again.logits, gpu.logits)
+    assert np.array_equal(again.n_acc, gpu.n_acc) and np.array_equal(again.token, gpu.token)
+    v.wait_limit(0)
+    bounded = run_gpu(v, w, 0, b, "stochastic", seed=4, round_=1)
+    v.wait_limit(-1)
+    assert np.array_equal(bounded.logits, gpu.logits)
+    v.close()
+
+
 @pytest.mark.parametrize("T_target", [40, 120])
 def test_split_gate_up_with_reduction_kernel(T_target):
     """A gate/up product of 96 row tiles of 256 rows (a 12288-wide
