@@ -251,7 +251,7 @@ def test_bf16_every_gemm_tile_class(T_target):
 
 @pytest.mark.parametrize("T_target", [17, 40, 96])
 def test_last_split_gate_up_repeats_and_never_waits(T_target):
-    """Below 97 slots the toy bf16 model's gate/up product (8 row tiles of
+    """Below 97 slots the toy bf16 model's gate/up product (16 row tiles of
     128 rows) is split over k in four, and whichever split of a tile counts
     last adds the others' sums in split order and applies SwiGLU.  Parity
     with the oracle; a second pass bit-identical to the first (the tile
